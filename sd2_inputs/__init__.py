@@ -1,0 +1,156 @@
+"""Seeded synthetic inputs (weights, prompts) shared by the oracle and the GPU path.
+
+Only value generation lives here: the C generator in ``gen.c`` (Philox4x32-10 +
+Box-Muller, see its header) and the tensor-id scheme below.  Weights are
+N(0, 0.02) for every matrix (embeddings, projections, LM heads and the steering
+projection W_s); RMSNorm gains are 1.  bf16 tensors are returned as numpy
+``uint16`` arrays holding the bf16 bit patterns, f32 tensors as ``float32``.
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+from .configs import Dims, Workload, PRESETS, BY_NAME, TINY, SMALL, LLAMA8B, LLAMA8B_BATCHED, LLAMA70B  # noqa: F401
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "libsd2gen.so")
+_lib = None
+
+WEIGHT_STD = 0.02
+LAYER_TENSORS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+_MATRIX_IDS = {"wq": 0, "wk": 1, "wv": 2, "wo": 3, "w_gate": 4, "w_up": 5, "w_down": 6}
+VERIFIER, DRAFTER = 0, 1
+
+
+def build(force: bool = False) -> str:
+    """Compile gen.c into libsd2gen.so next to it."""
+    if force or not os.path.exists(_SO):
+        cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", _SO + ".tmp",
+               os.path.join(_HERE, "gen.c"), "-lm"]
+        subprocess.check_call(cmd)
+        os.replace(_SO + ".tmp", _SO)
+    return _SO
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_SO)
+        u64, u32, i32 = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int32
+        lib.gen_normal_bf16.argtypes = [ctypes.c_void_p, u64, u64, u32, ctypes.c_double]
+        lib.gen_normal_f32.argtypes = [ctypes.c_void_p, u64, u64, u32, ctypes.c_double]
+        lib.gen_prompt.argtypes = [ctypes.c_void_p, u64, u64, u32, i32]
+        lib.gen_prompt_lens.argtypes = [ctypes.c_void_p, u64, u64, i32, i32]
+        lib.gen_philox_block.argtypes = [ctypes.c_void_p, u64, ctypes.c_void_p]
+        _lib = lib
+    return _lib
+
+
+def tensor_id(model: int, layer: int, name: str) -> int:
+    """Generator stream of one tensor: model 0 = verifier, 1 = drafter, 2 = steering."""
+    if name == "embed":
+        return ((model + 1) << 20) | 0
+    if name == "lm_head":
+        return ((model + 1) << 20) | 1
+    if name == "w_s":
+        return 3 << 20
+    return ((model + 1) << 20) | ((layer + 1) << 4) | _MATRIX_IDS[name]
+
+
+def normal(shape, dtype: str, seed: int, tid: int, scale: float = WEIGHT_STD) -> np.ndarray:
+    lib = _load()
+    n = int(np.prod(shape))
+    if dtype == "bf16":
+        out = np.empty(shape, dtype=np.uint16)
+        lib.gen_normal_bf16(out.ctypes.data, n, seed, tid, scale)
+    elif dtype == "f32":
+        out = np.empty(shape, dtype=np.float32)
+        lib.gen_normal_f32(out.ctypes.data, n, seed, tid, scale)
+    else:
+        raise ValueError(dtype)
+    return out
+
+
+def ones(shape, dtype: str) -> np.ndarray:
+    if dtype == "bf16":
+        return np.full(shape, 0x3F80, dtype=np.uint16)
+    return np.ones(shape, dtype=np.float32)
+
+
+def layer_shapes(dm: Dims):
+    hd = dm.head_dim
+    return {
+        "attn_norm": (dm.d_model,),
+        "wq": (dm.n_heads * hd, dm.d_model),
+        "wk": (dm.n_kv_heads * hd, dm.d_model),
+        "wv": (dm.n_kv_heads * hd, dm.d_model),
+        "wo": (dm.d_model, dm.n_heads * hd),
+        "ffn_norm": (dm.d_model,),
+        "w_gate": (dm.d_ff, dm.d_model),
+        "w_up": (dm.d_ff, dm.d_model),
+        "w_down": (dm.d_model, dm.d_ff),
+    }
+
+
+def layer_tensor(wl: Workload, model: int, layer: int, name: str) -> np.ndarray:
+    dm = wl.verifier if model == VERIFIER else wl.drafter
+    shp = layer_shapes(dm)[name]
+    if name.endswith("_norm"):
+        return ones(shp, wl.dtype)
+    return normal(shp, wl.dtype, wl.seed, tensor_id(model, layer, name))
+
+
+def model_weights(wl: Workload, model: int) -> dict:
+    """All weights of one model as host arrays: embed, layers[l][9], final_norm, lm_head."""
+    dm = wl.verifier if model == VERIFIER else wl.drafter
+    return {
+        "embed": normal((dm.vocab, dm.d_model), wl.dtype, wl.seed, tensor_id(model, 0, "embed")),
+        "layers": [[layer_tensor(wl, model, l, n) for n in LAYER_TENSORS] for l in range(dm.n_layers)],
+        "final_norm": ones((dm.d_model,), wl.dtype),
+        "lm_head": normal((dm.vocab, dm.d_model), wl.dtype, wl.seed, tensor_id(model, 0, "lm_head")),
+    }
+
+
+def iter_model_tensors(wl: Workload, model: int):
+    """Yield (key, array) one tensor at a time, so a caller can stream large models."""
+    dm = wl.verifier if model == VERIFIER else wl.drafter
+    yield ("embed",), normal((dm.vocab, dm.d_model), wl.dtype, wl.seed, tensor_id(model, 0, "embed"))
+    for l in range(dm.n_layers):
+        for n in LAYER_TENSORS:
+            yield ("layers", l, n), layer_tensor(wl, model, l, n)
+    yield ("final_norm",), ones((dm.d_model,), wl.dtype)
+    yield ("lm_head",), normal((dm.vocab, dm.d_model), wl.dtype, wl.seed, tensor_id(model, 0, "lm_head"))
+
+
+def steer_weights(wl: Workload) -> np.ndarray:
+    """W_s, shape [d_drafter][d_verifier]."""
+    return normal((wl.drafter.d_model, wl.verifier.d_model), wl.dtype, wl.seed, tensor_id(2, 0, "w_s"))
+
+
+def prompt_lens(wl: Workload) -> np.ndarray:
+    lo, hi = wl.prompt
+    if lo == hi:
+        return np.full((wl.batch,), lo, dtype=np.int32)
+    out = np.empty((wl.batch,), dtype=np.int32)
+    _load().gen_prompt_lens(out.ctypes.data, wl.batch, wl.seed, lo, hi)
+    return out
+
+
+def prompts(wl: Workload):
+    """(tokens int32 [B][max_prompt] zero-padded, lens int32 [B])."""
+    lens = prompt_lens(wl)
+    toks = np.zeros((wl.batch, wl.max_prompt), dtype=np.int32)
+    lib = _load()
+    for b in range(wl.batch):
+        row = np.empty((int(lens[b]),), dtype=np.int32)
+        lib.gen_prompt(row.ctypes.data, int(lens[b]), wl.seed, b, wl.verifier.vocab)
+        toks[b, : lens[b]] = row
+    return toks, lens
+
+
+def bf16_to_f32(a: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns (uint16) to float32."""
+    return (a.astype(np.uint32) << 16).view(np.float32)

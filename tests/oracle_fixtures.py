@@ -1,0 +1,49 @@
+"""Small helpers shared by the oracle tests: custom tiny workloads and weight sets."""
+import numpy as np
+
+import sd2_inputs as si
+from sd2_inputs.configs import Dims, Workload
+
+# Grouped-query shapes (H/Hkv = 4) at a size the float64 oracle runs in milliseconds.
+GQA = Workload(
+    name="gqa-tiny", verifier=Dims(3, 128, 8, 2, 256, 512, 5e5), drafter=Dims(2, 64, 4, 2, 192, 512, 5e5),
+    dtype="bf16", k=3, batch=2, prompt=(5, 9), new_tokens=24, temperature=1.0, seed=7)
+
+# Vocabulary of 8 for exact enumeration of one round's output law.
+LAW = Workload(
+    name="law-v8", verifier=Dims(2, 16, 2, 1, 32, 8, 1e4), drafter=Dims(1, 16, 2, 2, 32, 8, 1e4),
+    dtype="f32", k=2, batch=1, prompt=(4, 4), new_tokens=64, temperature=1.0, seed=3)
+
+
+def scaled_weights(wl, model, scale):
+    """Model weights drawn from the shared generator with a custom standard deviation."""
+    dm = wl.verifier if model == si.VERIFIER else wl.drafter
+    w = {
+        "embed": si.normal((dm.vocab, dm.d_model), wl.dtype, wl.seed, si.tensor_id(model, 0, "embed"), scale),
+        "layers": [],
+        "final_norm": si.ones((dm.d_model,), wl.dtype),
+        "lm_head": si.normal((dm.vocab, dm.d_model), wl.dtype, wl.seed, si.tensor_id(model, 0, "lm_head"), scale),
+    }
+    shapes = si.layer_shapes(dm)
+    for l in range(dm.n_layers):
+        row = []
+        for n in si.LAYER_TENSORS:
+            if n.endswith("_norm"):
+                row.append(si.ones(shapes[n], wl.dtype))
+            else:
+                row.append(si.normal(shapes[n], wl.dtype, wl.seed, si.tensor_id(model, l, n), scale))
+        w["layers"].append(row)
+    return w
+
+
+def weights(wl):
+    return si.model_weights(wl, 0), si.model_weights(wl, 1), si.steer_weights(wl)
+
+
+def zeros_like_ws(wl):
+    ws = si.steer_weights(wl)
+    return np.zeros_like(ws)
+
+
+def to_f64(a, dtype):
+    return si.bf16_to_f32(a).astype(np.float64) if dtype == "bf16" else a.astype(np.float64)

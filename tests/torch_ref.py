@@ -1,0 +1,60 @@
+"""Independent float64 forward of the SwiGLU decoder with PyTorch library ops.
+
+Used only to pin the oracle's model forward.  It shares nothing with the
+oracle: attention is ``torch.nn.functional.scaled_dot_product_attention``
+with a causal mask, RoPE is a complex rotation (``torch.polar``), the MLP uses
+``torch.nn.functional.silu``, and the matrix products are ``torch`` matmuls.
+"""
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+import sd2_inputs as si
+
+
+def _t(a, dtype):
+    if dtype == "bf16":
+        return torch.from_numpy(si.bf16_to_f32(a)).double()
+    return torch.from_numpy(a).double()
+
+
+def rope_complex(x, pos, theta):
+    """x [..., T, hd]; pairs (i, i + hd/2) rotated by pos * theta^(-2i/hd)."""
+    hd = x.shape[-1]
+    half = hd // 2
+    freqs = theta ** (-torch.arange(half, dtype=torch.float64) * 2.0 / hd)
+    ang = pos.double()[:, None] * freqs[None, :]
+    rot = torch.polar(torch.ones_like(ang), ang)
+    z = torch.complex(x[..., :half], x[..., half:]) * rot
+    return torch.cat([z.real, z.imag], dim=-1)
+
+
+def forward(dm, w, dtype, toks, add=None):
+    """Causal forward of a whole sequence; returns (final-norm hidden [T][d], logits [T][V])."""
+    T = len(toks)
+    d, H, Hkv, hd = dm.d_model, dm.n_heads, dm.n_kv_heads, dm.head_dim
+    toks_t = torch.as_tensor(np.asarray(toks, dtype=np.int64))
+    x = _t(w["embed"], dtype)[toks_t]
+    if add is not None:
+        x = x + torch.as_tensor(add, dtype=torch.float64)
+    pos = torch.arange(T)
+
+    def norm(v, g):
+        return v * torch.rsqrt(v.pow(2).mean(-1, keepdim=True) + dm.rms_eps) * _t(g, dtype)
+
+    for layer in w["layers"]:
+        an, wq, wk, wv, wo, fn, wg, wu, wd = layer
+        n = norm(x, an)
+        q = (n @ _t(wq, dtype).T).view(T, H, hd).transpose(0, 1)
+        k = (n @ _t(wk, dtype).T).view(T, Hkv, hd).transpose(0, 1)
+        v = (n @ _t(wv, dtype).T).view(T, Hkv, hd).transpose(0, 1)
+        q = rope_complex(q, pos, dm.rope_theta)
+        k = rope_complex(k, pos, dm.rope_theta)
+        k = k.repeat_interleave(H // Hkv, dim=0)
+        v = v.repeat_interleave(H // Hkv, dim=0)
+        o = F.scaled_dot_product_attention(q[None], k[None], v[None], is_causal=True)[0]
+        x = x + o.transpose(0, 1).reshape(T, H * hd) @ _t(wo, dtype).T
+        n2 = norm(x, fn)
+        x = x + (F.silu(n2 @ _t(wg, dtype).T) * (n2 @ _t(wu, dtype).T)) @ _t(wd, dtype).T
+    hF = norm(x, w["final_norm"])
+    return hF.numpy(), (hF @ _t(w["lm_head"], dtype).T).numpy()
