@@ -1,0 +1,159 @@
+/*
+ * sd2.h -- C ABI of the MI355X (gfx950) SD^2 speculative-decoding round.
+ *
+ * One round of SD^2 ("Steering Pretrained Drafters during Speculative
+ * Decoding", Berdoz, Rheinboldt, Wattenhofer) on one GPU:
+ *   1. the drafter proposes k tokens autoregressively, every processed token's
+ *      input embedding carrying the current steering vector s
+ *      (Sec. "Drafting": the steering term is computed once per drafting stage
+ *      since it does not depend on the draft position, and it also conditions
+ *      the keys/values the drafter caches);
+ *   2. the verifier scores the block [last committed token, k drafts] in one
+ *      parallel forward (Sec. "Verification");
+ *   3. speculative rejection sampling (Leviathan et al. 2023, cited in Sec.
+ *      "Verification") accepts a prefix of n drafts and draws one final token,
+ *      so the block yields n + 1 tokens (Sec. "Metrics", block efficiency);
+ *   4. the steering vector for the next round is W_s applied to the verifier's
+ *      final-norm hidden state at the position of the last token returned
+ *      (Sec. "Verification"); cache lengths roll back to the accepted prefix.
+ *
+ * Conventions for every call:
+ *  - All pointers named "device" are HIP device pointers owned by the caller;
+ *    they must stay valid until sd2_destroy.  The library allocates no device
+ *    memory: all state lives in the caller's workspace.
+ *  - Calls are asynchronous on the HIP stream given to sd2_create, except
+ *    sd2_debug_read, which synchronises that stream.  Argument and capacity
+ *    errors are detected on the host and returned before anything is enqueued.
+ *    HIP errors are returned as SD2_ERR_HIP by the call that observes them.
+ *  - A handle is not thread-safe; use one handle per stream.  No C++ exception
+ *    crosses this interface.
+ *  - Weight matrices are row-major [out][in] ("W x" layout), untied LM head,
+ *    no biases.  bf16 tensors hold bfloat16 bit patterns.
+ */
+#ifndef SD2_H
+#define SD2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sd2_status;
+#define SD2_OK 0
+#define SD2_ERR_INVALID_ARG (-1)   /* bad shape, pointer, alignment or size */
+#define SD2_ERR_CAPACITY (-2)      /* prompt + generation would exceed max_seq_len */
+#define SD2_ERR_STATE (-3)         /* e.g. sd2_round before sd2_prefill */
+#define SD2_ERR_HIP (-4)           /* a HIP runtime call failed; see sd2_last_error */
+#define SD2_ERR_UNSUPPORTED (-5)   /* valid request this build does not handle */
+
+typedef struct sd2_handle* sd2_handle_t;
+
+typedef enum { SD2_F32 = 0, SD2_BF16 = 1 } sd2_dtype;
+
+/* Shape of one SwiGLU decoder (the paper's models all use SwiGLU MLPs, eq. (1)).
+ * head_dim = d_model / n_heads must be even and at most 128; n_heads must be a
+ * multiple of n_kv_heads (grouped-query attention); d_model, n_heads*head_dim
+ * and d_ff must be multiples of 64. */
+typedef struct {
+    int32_t n_layers, d_model, n_heads, n_kv_heads, d_ff, vocab;
+    float rope_theta;  /* rotate-half RoPE base */
+    float rms_eps;     /* RMSNorm: x / sqrt(mean(x^2) + eps) * gain */
+} sd2_dims;
+
+/* Device pointers of one model, all of the configuration's dtype.
+ * layers points to a HOST array of n_layers * 9 device pointers, per layer in
+ * the order attn_norm[d], wq[H*hd][d], wk[Hkv*hd][d], wv[Hkv*hd][d],
+ * wo[d][H*hd], ffn_norm[d], w_gate[F][d], w_up[F][d], w_down[d][F].  The host
+ * array is copied by sd2_create; every device pointer must be 16-byte aligned. */
+typedef struct {
+    const void* embed;             /* [vocab][d] */
+    const void* const* layers;     /* host array of n_layers*9 device pointers */
+    const void* final_norm;        /* [d] */
+    const void* lm_head;           /* [vocab][d] */
+} sd2_weights;
+
+typedef struct {
+    sd2_dims verifier, drafter;    /* both models must share the vocabulary */
+    sd2_dtype dtype;
+    int32_t k;                     /* draft length, 1..32 */
+    int32_t max_batch;             /* sequences per round, 1..256 */
+    int32_t max_seq_len;           /* capacity per sequence: >= prompt + max_new_tokens + k + 1 */
+    int32_t max_new_tokens;        /* generated tokens per sequence; its last round is truncated */
+    float temperature;             /* 0 => greedy (argmax drafts, accept iff draft == verifier argmax) */
+    uint64_t seed;                 /* Philox4x32-10 key of every random draw */
+} sd2_config;
+
+/* Bytes of device workspace sd2_create needs for cfg (0 if cfg is invalid). */
+size_t sd2_workspace_bytes(const sd2_config* cfg);
+
+/*
+ * Create a handle.  verifier/drafter: model weights; w_steer: device [d_drafter][d_verifier]
+ * steering projection W_s (s = W_s h, paper Sec. "Verification"/"Drafting");
+ * workspace: device buffer of at least sd2_workspace_bytes(cfg) bytes, 256-byte aligned;
+ * hip_stream: the hipStream_t every call enqueues on (NULL = default stream).
+ * On success *out receives the handle.  Enqueues small table-initialisation kernels.
+ */
+sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                      const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
+                      sd2_handle_t* out);
+
+/*
+ * Prefill `batch` sequences (1..max_batch) with their prompts.
+ * tokens: device int32 [batch][max_prompt], row b holding lens[b] prompt ids in [0, vocab);
+ * lens: device int32 [batch], each in [1, max_prompt]; max_prompt: host bound on lens.
+ * Both models process positions 0..len-2 (the drafter with zero steering); the first
+ * round's steering vector is W_s applied to the verifier's final-norm hidden state at
+ * position len-2 (zero when len == 1).  Returns SD2_ERR_CAPACITY when
+ * max_prompt + max_new_tokens + k + 1 > max_seq_len.  Resets all per-sequence state.
+ */
+sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, const int32_t* lens,
+                       int32_t max_prompt);
+
+/*
+ * One speculative round for every prefilled sequence.
+ * out_tokens: device int32 [batch][k+1]: row b gets the accepted drafts followed by the
+ *             final token (only the first out_counts[b] entries are meaningful);
+ * out_counts: device int32 [batch]: tokens emitted this round (n+1, truncated at the
+ *             max_new_tokens budget), 0 once the sequence has finished.
+ * Returns SD2_ERR_STATE before sd2_prefill.
+ */
+sd2_status sd2_round(sd2_handle_t h, int32_t* out_tokens, int32_t* out_counts);
+
+/*
+ * Test hook: like sd2_round, but the trajectory follows caller-supplied decisions.
+ * forced: device int32 [batch][k+2] = k drafts, accepted count n, final token y per
+ * sequence.  The library still computes its own decisions from its own logits and
+ * records them (sd2_debug_read SD2_DBG_OWN_*); drafting, verification, commit and
+ * steering then proceed with the forced values.
+ */
+sd2_status sd2_round_forced(sd2_handle_t h, const int32_t* forced, int32_t* out_tokens, int32_t* out_counts);
+
+/* Destroy a handle (NULL is a no-op).  Does not free caller memory. */
+sd2_status sd2_destroy(sd2_handle_t h);
+
+/* Static text for a status code. */
+const char* sd2_status_string(sd2_status s);
+
+/* Text of the last HIP error observed by handle h (empty if none). */
+const char* sd2_last_error(sd2_handle_t h);
+
+/* What sd2_debug_read copies (all host-side, after synchronising the stream). */
+#define SD2_DBG_LOGITS_V 1    /* float [batch][k+1][vocab]: last round's verifier logits */
+#define SD2_DBG_LOGITS_D 2    /* float [batch][k][vocab]: last round's drafter logits (row j drew draft j) */
+#define SD2_DBG_STEER 3       /* float [batch][d_drafter]: current steering vector s */
+#define SD2_DBG_OWN_DRAFTS 4  /* int32 [batch][k]: drafts the library drew itself last round */
+#define SD2_DBG_OWN_N 5       /* int32 [batch]: accepted count the library computed itself */
+#define SD2_DBG_OWN_Y 6       /* int32 [batch]: final token the library drew itself */
+#define SD2_DBG_STATE 7       /* int32 [batch][5]: t, len_verifier, len_drafter, produced, done */
+#define SD2_DBG_HIST 8        /* int32 [batch][max_seq_len]: committed tokens */
+#define SD2_DBG_HIDDEN_V 9    /* float [batch][k+1][d_verifier]: last verify pass's final-norm hidden states */
+
+/* Copy a debug buffer of the last round into host memory dst (bytes must match). */
+sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SD2_H */

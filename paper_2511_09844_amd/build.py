@@ -1,0 +1,39 @@
+"""Compile the gfx950 HIP library libsd2.so in-tree (hipcc, no JIT cache)."""
+import os
+import shutil
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SO = os.path.join(HERE, "libsd2.so")
+SOURCES = ["csrc/kernels.hip", "csrc/engine.hip"]
+ARCH = "gfx950"
+
+
+def hipcc() -> str:
+    p = shutil.which("hipcc")
+    if p:
+        return p
+    p = "/opt/rocm/bin/hipcc"
+    if os.path.exists(p):
+        return p
+    raise RuntimeError("hipcc not found: the SD2 library needs ROCm's hipcc to build")
+
+
+def build(verbose: bool = False) -> str:
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+           # packed fp32 instructions are kept out of every kernel
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-Wall", "-o", SO + ".tmp"] + [os.path.join(HERE, s) for s in SOURCES]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + res.stderr)
+    if verbose:
+        msgs = [l for l in res.stderr.splitlines() if "packed-fp32-ops' is not a recognized" not in l]
+        if msgs:
+            print("\n".join(msgs))
+    os.replace(SO + ".tmp", SO)
+    return SO
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,116 @@
+// Private host/device interface of the SD^2 engine: workspace layout and kernel launchers.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sd2.h"
+
+namespace sd2 {
+
+constexpr int kMaxK = 32;
+constexpr int kVocabChunks = 64;     // vocabulary slices per row in the sampler's partial reductions
+constexpr int kPrefillRows = 512;    // rows per prefill chunk (all sequences together)
+
+struct ModelDev {
+    sd2_dims dm;
+    int hd, qkv_dim;
+    const void* embed;
+    const void* layer[9 * 128];      // per layer: attn_norm, wq, wk, wv, wo, ffn_norm, w_gate, w_up, w_down
+    const void* final_norm;
+    const void* lm_head;
+    // workspace-resident
+    float* kc;                        // K cache [layer][batch][kv_head][cap][hd]
+    float* vc;                        // V cache, same layout
+    float* rope_cos;                  // [cap][hd/2]
+    float* rope_sin;
+    float* x;                         // residual stream [maxm][d]
+};
+
+enum WIdx { kAttnNorm = 0, kWq, kWk, kWv, kWo, kFfnNorm, kWg, kWu, kWd };
+
+// Partial result of a vocabulary slice for one row.
+struct VPart {
+    float m;     // max of scores
+    float s;     // sum of exp(score - m)   (or second field for argmax partials)
+    float best;  // best perturbed score
+    int idx;     // its token
+    float best2; // fallback score (final draw: plain p-Gumbel)
+    int idx2;
+    int flag;    // final draw: residual had positive mass in this slice
+    int pad;
+};
+
+struct Workspace {
+    // per-sequence state, int32 [max_batch]
+    int32_t *t, *len_v, *len_d, *produced, *done;
+    int32_t* hist;          // [max_batch][cap]
+    float* steer;           // [max_batch][d_D]
+    float* hcap;            // [max_batch][d_V] verifier residual captured at prefill
+    // row plans
+    int32_t* row_pos;       // [maxm]
+    int32_t* row_seq;       // [maxm]
+    int32_t* lm_map_d;      // [k][2*max_batch] drafter LM-head output rows per step
+    int32_t* steer_map;     // [max_batch]
+    int32_t* ident_map;     // [max_batch] 0..max_batch-1
+    // activations
+    float* qkv;             // [maxm][max qkv_dim]
+    float* attn;            // [maxm][max H*hd]
+    float* ffh;             // [maxm][max F]
+    float* logits_v;        // [max_batch][k+1][V]
+    float* logits_d;        // [max_batch][k][V]
+    float* hidden_dbg;      // [max_batch*(k+1)][d_V]
+    VPart* part;            // [max_batch*(2k+1)][kVocabChunks]
+    float* lse_v;           // [max_batch][k+1]
+    float* lse_d;           // [max_batch][k]
+    int32_t* argmax_v;      // [max_batch][k+1] (greedy)
+    // decisions
+    int32_t* drafts;        // [max_batch][k] effective drafts
+    int32_t* own_drafts;    // [max_batch][k]
+    int32_t* n_eff;         // [max_batch]
+    int32_t* own_n;
+    int32_t* own_y;
+    int32_t* forced;        // [max_batch][k+2]
+    int32_t* forced_on;     // [1]
+};
+
+struct Engine {
+    sd2_config cfg;
+    ModelDev mv, md;
+    const void* w_steer;
+    Workspace ws;
+    int cap, maxm, batch;
+    bool prefilled;
+    hipStream_t stream;
+    bool bf16;
+    char err[256];
+    bool use_graph;
+    hipGraphExec_t graph_exec;
+    hipGraph_t graph;
+    int graph_batch;
+    int32_t* graph_out_tokens;
+    int32_t* graph_out_counts;
+};
+
+size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm);
+
+// ---- launchers (kernels.hip) ----
+void launch_rope_table(hipStream_t s, ModelDev& m, int cap);
+void launch_init_maps(hipStream_t s, Engine& e);
+enum PlanKind { kPlanDraft1 = 0, kPlanDraftJ = 1, kPlanVerify = 2, kPlanPrefill = 3 };
+void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
+                       const int32_t* prompt_len, int max_prompt, int chunk);
+void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows);
+enum Epi { kEpiStore = 0, kEpiAdd = 1, kEpiSwiglu = 2 };
+void launch_gemv(hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K, const void* gamma,
+                 float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y, int ldy,
+                 const int32_t* out_map);
+void launch_draft_pick(hipStream_t s, Engine& e, int j);
+void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t* out_counts);
+void launch_prefill_capture(hipStream_t s, Engine& e, int rows, const int32_t* prompt_len, int max_prompt);
+void launch_prefill_finish(hipStream_t s, Engine& e, int batch, const int32_t* prompt_tok, const int32_t* prompt_len,
+                           int max_prompt);
+void launch_rmsnorm_rows(hipStream_t s, const float* X, int rows, int d, const void* gamma, bool bf16, float eps,
+                         float* Y);
+void launch_set_flag(hipStream_t s, int32_t* flag, int v);
+
+}  // namespace sd2

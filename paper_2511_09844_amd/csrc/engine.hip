@@ -1,0 +1,405 @@
+// Host side of the SD^2 engine: argument checks, workspace carving, the round's kernel
+// sequence (recorded once into a HIP graph and replayed), prefill, and the C ABI.
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+
+#include "engine.h"
+
+using namespace sd2;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Carver {
+    char* base;
+    size_t off = 0;
+    template <typename T>
+    T* take(size_t count) {
+        off = align_up(off);
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+bool dims_ok(const sd2_dims& d) {
+    if (d.n_layers < 1 || d.n_layers > 128 || d.d_model < 64 || d.n_heads < 1 || d.n_kv_heads < 1 ||
+        d.d_ff < 64 || d.vocab < 2)
+        return false;
+    if (d.d_model % d.n_heads || d.n_heads % d.n_kv_heads) return false;
+    int hd = d.d_model / d.n_heads;
+    if (hd % 2 || hd > 128 || hd % 4) return false;
+    if (d.d_model % 64 || (d.n_heads * hd) % 64 || d.d_ff % 64) return false;
+    // every GEMV input row must fit the 64 KiB of LDS a workgroup stages it in
+    if (d.d_model > 16384 || d.d_ff > 16384) return false;
+    if (!(d.rope_theta > 0.f) || !(d.rms_eps >= 0.f)) return false;
+    return true;
+}
+
+bool config_ok(const sd2_config* c) {
+    if (!c) return false;
+    if (!dims_ok(c->verifier) || !dims_ok(c->drafter)) return false;
+    if (c->verifier.vocab != c->drafter.vocab) return false;
+    if (c->dtype != SD2_F32 && c->dtype != SD2_BF16) return false;
+    if (c->k < 1 || c->k > kMaxK) return false;
+    if (c->max_batch < 1 || c->max_batch > 256) return false;
+    if (c->max_new_tokens < 1) return false;
+    if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;
+    if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
+    return true;
+}
+
+int max_rows(const sd2_config& c) {
+    int B = c.max_batch;
+    return std::max(std::max(B * (c.k + 1), 2 * B), kPrefillRows);
+}
+
+void model_dims(ModelDev* m, const sd2_dims& d) {
+    m->dm = d;
+    m->hd = d.d_model / d.n_heads;
+    m->qkv_dim = (d.n_heads + 2 * d.n_kv_heads) * m->hd;
+}
+
+}  // namespace
+
+namespace sd2 {
+
+size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm_out) {
+    Carver cv{base};
+    int B = c.max_batch, k = c.k, cap = c.max_seq_len, V = c.verifier.vocab;
+    int maxm = max_rows(c);
+    if (maxm_out) *maxm_out = maxm;
+    ModelDev tv, td;
+    model_dims(&tv, c.verifier);
+    model_dims(&td, c.drafter);
+    ModelDev* ms[2] = {mv ? mv : &tv, md ? md : &td};
+    if (mv) model_dims(mv, c.verifier);
+    if (md) model_dims(md, c.drafter);
+    Workspace w{};
+    w.t = cv.take<int32_t>(B);
+    w.len_v = cv.take<int32_t>(B);
+    w.len_d = cv.take<int32_t>(B);
+    w.produced = cv.take<int32_t>(B);
+    w.done = cv.take<int32_t>(B);
+    w.hist = cv.take<int32_t>((size_t)B * cap);
+    w.steer = cv.take<float>((size_t)B * c.drafter.d_model);
+    w.hcap = cv.take<float>((size_t)B * c.verifier.d_model);
+    w.row_pos = cv.take<int32_t>(maxm);
+    w.row_seq = cv.take<int32_t>(maxm);
+    w.lm_map_d = cv.take<int32_t>((size_t)k * 2 * B);
+    w.steer_map = cv.take<int32_t>(B);
+    w.ident_map = cv.take<int32_t>(B);
+    int qkv = std::max(ms[0]->qkv_dim, ms[1]->qkv_dim);
+    int att = std::max(c.verifier.n_heads * ms[0]->hd, c.drafter.n_heads * ms[1]->hd);
+    int ff = std::max(c.verifier.d_ff, c.drafter.d_ff);
+    w.qkv = cv.take<float>((size_t)maxm * qkv);
+    w.attn = cv.take<float>((size_t)maxm * att);
+    w.ffh = cv.take<float>((size_t)maxm * ff);
+    w.logits_v = cv.take<float>((size_t)B * (k + 1) * V);
+    w.logits_d = cv.take<float>((size_t)B * k * V);
+    w.hidden_dbg = cv.take<float>((size_t)B * (k + 1) * c.verifier.d_model);
+    w.part = cv.take<VPart>((size_t)B * (2 * k + 1) * kVocabChunks);
+    w.lse_v = cv.take<float>((size_t)B * (k + 1));
+    w.lse_d = cv.take<float>((size_t)B * k);
+    w.argmax_v = cv.take<int32_t>((size_t)B * (k + 1));
+    w.drafts = cv.take<int32_t>((size_t)B * k);
+    w.own_drafts = cv.take<int32_t>((size_t)B * k);
+    w.n_eff = cv.take<int32_t>(B);
+    w.own_n = cv.take<int32_t>(B);
+    w.own_y = cv.take<int32_t>(B);
+    w.forced = cv.take<int32_t>((size_t)B * (k + 2));
+    w.forced_on = cv.take<int32_t>(1);
+    for (int i = 0; i < 2; ++i) {
+        ModelDev* m = ms[i];
+        const sd2_dims& d = m->dm;
+        size_t kv = (size_t)d.n_layers * B * d.n_kv_heads * cap * m->hd;
+        m->kc = cv.take<float>(kv);
+        m->vc = cv.take<float>(kv);
+        m->rope_cos = cv.take<float>((size_t)cap * (m->hd / 2));
+        m->rope_sin = cv.take<float>((size_t)cap * (m->hd / 2));
+        m->x = cv.take<float>((size_t)maxm * d.d_model);
+    }
+    if (ws) *ws = w;
+    return align_up(cv.off);
+}
+
+}  // namespace sd2
+
+namespace {
+
+sd2_status hip_fail(Engine* e, hipError_t err, const char* where) {
+    snprintf(e->err, sizeof(e->err), "%s: %s", where, hipGetErrorString(err));
+    return SD2_ERR_HIP;
+}
+
+sd2_status check_launch(Engine* e, const char* where) {
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return hip_fail(e, err, where);
+    return SD2_OK;
+}
+
+void lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map) {
+    const void* ws[1] = {m.lm_head};
+    int rws[1] = {m.dm.vocab};
+    launch_gemv(e.stream, e.bf16, m.x, nullptr, rows, m.dm.d_model, m.final_norm, m.dm.rms_eps, ws, rws, 1,
+                kEpiStore, Y, m.dm.vocab, out_map);
+}
+
+void steer_gemv(Engine& e, const float* X, const int32_t* in_map, int rows) {
+    const void* ws[1] = {e.w_steer};
+    int rws[1] = {e.md.dm.d_model};
+    launch_gemv(e.stream, e.bf16, X, in_map, rows, e.mv.dm.d_model, e.mv.final_norm, e.mv.dm.rms_eps, ws, rws, 1,
+                kEpiStore, e.ws.steer, e.md.dm.d_model, nullptr);
+}
+
+// The whole round, as a fixed sequence of kernels (no host decisions).
+void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
+    hipStream_t s = e.stream;
+    int B = e.batch, k = e.cfg.k;
+    for (int j = 1; j <= k; ++j) {
+        int rows = j == 1 ? 2 * B : B;
+        launch_plan_embed(s, e, e.md, j == 1 ? kPlanDraft1 : kPlanDraftJ, j, rows, nullptr, nullptr, 0, 1);
+        for (int l = 0; l < e.md.dm.n_layers; ++l) launch_layer(s, e, e.md, l, rows);
+        lm_head(e, e.md, rows, e.ws.logits_d, e.ws.lm_map_d + (size_t)(j - 1) * 2 * e.cfg.max_batch);
+        launch_draft_pick(s, e, j);
+    }
+    int rows = B * (k + 1);
+    launch_plan_embed(s, e, e.mv, kPlanVerify, 0, rows, nullptr, nullptr, 0, 1);
+    for (int l = 0; l < e.mv.dm.n_layers; ++l) launch_layer(s, e, e.mv, l, rows);
+    lm_head(e, e.mv, rows, e.ws.logits_v, nullptr);
+    launch_verify_decide(s, e, out_tokens, out_counts);
+    steer_gemv(e, e.mv.x, e.ws.steer_map, B);
+}
+
+void drop_graph(Engine& e) {
+    if (e.graph_exec) (void)hipGraphExecDestroy(e.graph_exec);
+    if (e.graph) (void)hipGraphDestroy(e.graph);
+    e.graph_exec = nullptr;
+    e.graph = nullptr;
+}
+
+sd2_status run_round(Engine* e, int32_t* out_tokens, int32_t* out_counts) {
+    // Replay the recorded round when the shape and output buffers are unchanged.
+    if (!e->use_graph) {
+        enqueue_round(*e, out_tokens, out_counts);
+        return check_launch(e, "round");
+    }
+    if (!e->graph_exec || e->graph_batch != e->batch || e->graph_out_tokens != out_tokens ||
+        e->graph_out_counts != out_counts) {
+        drop_graph(*e);
+        hipError_t err = hipStreamBeginCapture(e->stream, hipStreamCaptureModeThreadLocal);
+        if (err != hipSuccess) return hip_fail(e, err, "hipStreamBeginCapture");
+        enqueue_round(*e, out_tokens, out_counts);
+        err = hipStreamEndCapture(e->stream, &e->graph);
+        if (err != hipSuccess) return hip_fail(e, err, "hipStreamEndCapture");
+        err = hipGraphInstantiate(&e->graph_exec, e->graph, nullptr, nullptr, 0);
+        if (err != hipSuccess) return hip_fail(e, err, "hipGraphInstantiate");
+        e->graph_batch = e->batch;
+        e->graph_out_tokens = out_tokens;
+        e->graph_out_counts = out_counts;
+    }
+    hipError_t err = hipGraphLaunch(e->graph_exec, e->stream);
+    if (err != hipSuccess) return hip_fail(e, err, "hipGraphLaunch");
+    return SD2_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t sd2_workspace_bytes(const sd2_config* cfg) {
+    if (!config_ok(cfg)) return 0;
+    return carve(*cfg, nullptr, nullptr, nullptr, nullptr, nullptr);
+}
+
+const char* sd2_status_string(sd2_status s) {
+    switch (s) {
+        case SD2_OK: return "ok";
+        case SD2_ERR_INVALID_ARG: return "invalid argument";
+        case SD2_ERR_CAPACITY: return "capacity exceeded (max_seq_len)";
+        case SD2_ERR_STATE: return "invalid state (prefill first)";
+        case SD2_ERR_HIP: return "HIP runtime error";
+        case SD2_ERR_UNSUPPORTED: return "unsupported";
+        default: return "unknown status";
+    }
+}
+
+const char* sd2_last_error(sd2_handle_t h) {
+    if (!h) return "";
+    return reinterpret_cast<Engine*>(h)->err;
+}
+
+static bool aligned16(const void* p) { return p && ((uintptr_t)p % 16) == 0; }
+
+static bool weights_ok(const sd2_weights* w, const sd2_dims& d) {
+    if (!w || !aligned16(w->embed) || !w->layers || !aligned16(w->final_norm) || !aligned16(w->lm_head)) return false;
+    for (int i = 0; i < d.n_layers * 9; ++i)
+        if (!aligned16(w->layers[i])) return false;
+    return true;
+}
+
+sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                      const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
+                      sd2_handle_t* out) {
+    if (!out) return SD2_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (!config_ok(cfg)) return SD2_ERR_INVALID_ARG;
+    if (!weights_ok(verifier, cfg->verifier) || !weights_ok(drafter, cfg->drafter) || !aligned16(w_steer))
+        return SD2_ERR_INVALID_ARG;
+    if (!workspace || ((uintptr_t)workspace % kAlign) != 0) return SD2_ERR_INVALID_ARG;
+    size_t need = sd2_workspace_bytes(cfg);
+    if (workspace_bytes < need) return SD2_ERR_INVALID_ARG;
+    Engine* e = new (std::nothrow) Engine();
+    if (!e) return SD2_ERR_INVALID_ARG;
+    e->cfg = *cfg;
+    e->cap = cfg->max_seq_len;
+    e->bf16 = cfg->dtype == SD2_BF16;
+    e->stream = (hipStream_t)hip_stream;
+    e->w_steer = w_steer;
+    // Graph replay needs a capturable (non-null) stream; SD2_NO_GRAPH=1 forces eager launches.
+    e->use_graph = hip_stream != nullptr && getenv("SD2_NO_GRAPH") == nullptr;
+    carve(*cfg, (char*)workspace, &e->ws, &e->mv, &e->md, &e->maxm);
+    const sd2_weights* src[2] = {verifier, drafter};
+    ModelDev* dst[2] = {&e->mv, &e->md};
+    for (int i = 0; i < 2; ++i) {
+        dst[i]->embed = src[i]->embed;
+        dst[i]->final_norm = src[i]->final_norm;
+        dst[i]->lm_head = src[i]->lm_head;
+        for (int j = 0; j < dst[i]->dm.n_layers * 9; ++j) dst[i]->layer[j] = src[i]->layers[j];
+    }
+    hipError_t err = hipMemsetAsync(workspace, 0, need, e->stream);
+    if (err != hipSuccess) {
+        sd2_status st = hip_fail(e, err, "hipMemsetAsync");
+        delete e;
+        return st;
+    }
+    launch_rope_table(e->stream, e->mv, e->cap);
+    launch_rope_table(e->stream, e->md, e->cap);
+    launch_init_maps(e->stream, *e);
+    sd2_status st = check_launch(e, "create");
+    if (st != SD2_OK) {
+        delete e;
+        return st;
+    }
+    *out = reinterpret_cast<sd2_handle_t>(e);
+    return SD2_OK;
+}
+
+sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, const int32_t* lens,
+                       int32_t max_prompt) {
+    if (!h) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    if (batch < 1 || batch > e->cfg.max_batch || !tokens || !lens || max_prompt < 1) return SD2_ERR_INVALID_ARG;
+    if ((int64_t)max_prompt + e->cfg.max_new_tokens + e->cfg.k + 1 > e->cap) return SD2_ERR_CAPACITY;
+    hipStream_t s = e->stream;
+    e->batch = batch;
+    int chunk = std::max(1, std::min(max_prompt - 1, kPrefillRows / batch));
+    int rows = batch * chunk;
+    int nchunks = max_prompt > 1 ? (max_prompt - 1 + chunk - 1) / chunk : 0;
+    hipError_t err = hipMemsetAsync(e->ws.hcap, 0, sizeof(float) * (size_t)batch * e->mv.dm.d_model, s);
+    if (err != hipSuccess) return hip_fail(e, err, "hipMemsetAsync");
+    for (int c = 0; c < nchunks; ++c) {
+        launch_plan_embed(s, *e, e->mv, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
+        for (int l = 0; l < e->mv.dm.n_layers; ++l) launch_layer(s, *e, e->mv, l, rows);
+        launch_prefill_capture(s, *e, rows, lens, max_prompt);
+    }
+    steer_gemv(*e, e->ws.hcap, nullptr, batch);
+    for (int c = 0; c < nchunks; ++c) {
+        launch_plan_embed(s, *e, e->md, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
+        for (int l = 0; l < e->md.dm.n_layers; ++l) launch_layer(s, *e, e->md, l, rows);
+    }
+    launch_prefill_finish(s, *e, batch, tokens, lens, max_prompt);
+    sd2_status st = check_launch(e, "prefill");
+    if (st != SD2_OK) return st;
+    e->prefilled = true;
+    return SD2_OK;
+}
+
+sd2_status sd2_round(sd2_handle_t h, int32_t* out_tokens, int32_t* out_counts) {
+    if (!h || !out_tokens || !out_counts) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    if (!e->prefilled) return SD2_ERR_STATE;
+    launch_set_flag(e->stream, e->ws.forced_on, 0);
+    sd2_status st = check_launch(e, "round");
+    if (st != SD2_OK) return st;
+    return run_round(e, out_tokens, out_counts);
+}
+
+sd2_status sd2_round_forced(sd2_handle_t h, const int32_t* forced, int32_t* out_tokens, int32_t* out_counts) {
+    if (!h || !forced || !out_tokens || !out_counts) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    if (!e->prefilled) return SD2_ERR_STATE;
+    size_t bytes = sizeof(int32_t) * (size_t)e->batch * (e->cfg.k + 2);
+    hipError_t err = hipMemcpyAsync(e->ws.forced, forced, bytes, hipMemcpyDeviceToDevice, e->stream);
+    if (err != hipSuccess) return hip_fail(e, err, "hipMemcpyAsync");
+    launch_set_flag(e->stream, e->ws.forced_on, 1);
+    sd2_status st = check_launch(e, "round_forced");
+    if (st != SD2_OK) return st;
+    return run_round(e, out_tokens, out_counts);
+}
+
+sd2_status sd2_destroy(sd2_handle_t h) {
+    if (!h) return SD2_OK;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    drop_graph(*e);
+    delete e;
+    return SD2_OK;
+}
+
+sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes) {
+    if (!h || !dst_host) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    int B = e->batch, k = e->cfg.k, V = e->mv.dm.vocab;
+    if (B < 1) return SD2_ERR_STATE;
+    const void* src = nullptr;
+    size_t want = 0;
+    switch (what) {
+        case SD2_DBG_LOGITS_V: src = e->ws.logits_v; want = sizeof(float) * (size_t)B * (k + 1) * V; break;
+        case SD2_DBG_LOGITS_D: src = e->ws.logits_d; want = sizeof(float) * (size_t)B * k * V; break;
+        case SD2_DBG_STEER: src = e->ws.steer; want = sizeof(float) * (size_t)B * e->md.dm.d_model; break;
+        case SD2_DBG_OWN_DRAFTS: src = e->ws.own_drafts; want = sizeof(int32_t) * (size_t)B * k; break;
+        case SD2_DBG_OWN_N: src = e->ws.own_n; want = sizeof(int32_t) * (size_t)B; break;
+        case SD2_DBG_OWN_Y: src = e->ws.own_y; want = sizeof(int32_t) * (size_t)B; break;
+        case SD2_DBG_HIST: src = e->ws.hist; want = sizeof(int32_t) * (size_t)B * e->cap; break;
+        case SD2_DBG_STATE: want = sizeof(int32_t) * (size_t)B * 5; break;
+        case SD2_DBG_HIDDEN_V: src = e->ws.hidden_dbg; want = sizeof(float) * (size_t)B * (k + 1) * e->mv.dm.d_model; break;
+        default: return SD2_ERR_INVALID_ARG;
+    }
+    if (bytes != want) return SD2_ERR_INVALID_ARG;
+    if (what == SD2_DBG_HIDDEN_V) {
+        launch_rmsnorm_rows(e->stream, e->mv.x, B * (k + 1), e->mv.dm.d_model, e->mv.final_norm, e->bf16,
+                            e->mv.dm.rms_eps, e->ws.hidden_dbg);
+        sd2_status st = check_launch(e, "debug_read");
+        if (st != SD2_OK) return st;
+    }
+    hipError_t err = hipStreamSynchronize(e->stream);
+    if (err != hipSuccess) return hip_fail(e, err, "hipStreamSynchronize");
+    if (what == SD2_DBG_STATE) {
+        int32_t* out = (int32_t*)dst_host;
+        const int32_t* cols[5] = {e->ws.t, e->ws.len_v, e->ws.len_d, e->ws.produced, e->ws.done};
+        int32_t* tmp = new (std::nothrow) int32_t[B];
+        if (!tmp) return SD2_ERR_INVALID_ARG;
+        for (int c = 0; c < 5; ++c) {
+            err = hipMemcpy(tmp, cols[c], sizeof(int32_t) * B, hipMemcpyDeviceToHost);
+            if (err != hipSuccess) {
+                delete[] tmp;
+                return hip_fail(e, err, "hipMemcpy");
+            }
+            for (int b = 0; b < B; ++b) out[b * 5 + c] = tmp[b];
+        }
+        delete[] tmp;
+        return SD2_OK;
+    }
+    err = hipMemcpy(dst_host, src, want, hipMemcpyDeviceToHost);
+    if (err != hipSuccess) return hip_fail(e, err, "hipMemcpy");
+    return SD2_OK;
+}
+
+}  // extern "C"

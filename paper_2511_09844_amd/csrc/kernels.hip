@@ -1,0 +1,818 @@
+// SD^2 round kernels for gfx950: input planning, weight-streaming GEMV, RoPE/KV append,
+// grouped-query attention, and the vocabulary-wide sampler.
+#include <math.h>
+
+#include "device_common.h"
+#include "engine.h"
+
+namespace sd2 {
+
+// ===========================================================================
+// RoPE table: cos/sin(pos * theta^(-2i/hd)) evaluated in double, stored as float.
+// ===========================================================================
+__global__ void k_rope_table(float* __restrict__ c, float* __restrict__ s, int cap, int half, int hd, double theta) {
+    int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= cap * half) return;
+    int pos = idx / half, i = idx % half;
+    double ang = (double)pos * pow(theta, -2.0 * (double)i / (double)hd);
+    c[idx] = (float)cos(ang);
+    s[idx] = (float)sin(ang);
+}
+
+void launch_rope_table(hipStream_t s, ModelDev& m, int cap) {
+    int half = m.hd / 2;
+    int n = cap * half;
+    k_rope_table<<<(n + 255) / 256, 256, 0, s>>>(m.rope_cos, m.rope_sin, cap, half, m.hd, (double)m.dm.rope_theta);
+}
+
+// Static drafter LM-head output maps: step 1 has two rows per sequence (catch-up), of which
+// only the second (position t-1) produces logits; later steps have one row per sequence.
+__global__ void k_init_maps(int32_t* lm_map_d, int32_t* ident, int max_batch, int k) {
+    int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < max_batch) ident[r] = r;
+    for (int j = 0; j < k; ++j) {
+        int32_t* mp = lm_map_d + (size_t)j * 2 * max_batch;
+        if (j == 0) {
+            if (r < 2 * max_batch) mp[r] = (r & 1) ? (r >> 1) * k : -1;
+        } else {
+            if (r < max_batch) mp[r] = r * k + j;
+        }
+    }
+}
+
+void launch_init_maps(hipStream_t s, Engine& e) {
+    int n = 2 * e.cfg.max_batch;
+    k_init_maps<<<(n + 255) / 256, 256, 0, s>>>(e.ws.lm_map_d, e.ws.ident_map, e.cfg.max_batch, e.cfg.k);
+}
+
+// ===========================================================================
+// Row planning + embedding gather (+ steering injection for drafter rows).
+// One block per row.  Inactive rows get position -1 and a zero residual.
+// ===========================================================================
+struct PlanArgs {
+    int kind, j, k, batch, cap, vocab, d, chunk, max_prompt;
+    const int32_t *t, *len_d, *done, *hist, *drafts, *prompt_tok, *prompt_len;
+    const float* steer;
+    int add_steer;
+    int32_t *row_pos, *row_seq;
+    float* x;
+    const void* embed;
+};
+
+template <typename TW>
+__global__ __launch_bounds__(256) void k_plan_embed(PlanArgs a) {
+    int r = blockIdx.x;
+    int b, pos = -1, tok = 0;
+    bool active = false;
+    if (a.kind == kPlanDraft1) {
+        b = r >> 1;
+        int i = r & 1;
+        if (b < a.batch && !a.done[b]) {
+            int t = a.t[b], m = t - a.len_d[b];
+            if (i == 1) { pos = t - 1; active = true; }
+            else if (m == 2) { pos = t - 2; active = true; }
+            if (active) tok = a.hist[(size_t)b * a.cap + pos];
+        }
+    } else if (a.kind == kPlanDraftJ) {
+        b = r;
+        if (b < a.batch && !a.done[b]) {
+            pos = a.t[b] + a.j - 2;
+            tok = a.drafts[b * a.k + a.j - 2];
+            active = true;
+        }
+    } else if (a.kind == kPlanVerify) {
+        b = r / (a.k + 1);
+        int i = r % (a.k + 1);
+        if (b < a.batch && !a.done[b]) {
+            int t = a.t[b];
+            pos = t - 1 + i;
+            tok = i == 0 ? a.hist[(size_t)b * a.cap + t - 1] : a.drafts[b * a.k + i - 1];
+            active = true;
+        }
+    } else {  // prefill chunk
+        b = r / a.chunk;
+        int i = r % a.chunk;
+        pos = a.j * a.chunk + i;
+        if (b < a.batch && pos < min(a.prompt_len[b], a.max_prompt) - 1) {
+            tok = a.prompt_tok[(size_t)b * a.max_prompt + pos];
+            active = true;
+        }
+    }
+    if (!active) pos = -1;
+    tok = tok < 0 ? 0 : (tok >= a.vocab ? a.vocab - 1 : tok);
+    if (threadIdx.x == 0) {
+        a.row_pos[r] = pos;
+        a.row_seq[r] = b;
+    }
+    float* xr = a.x + (size_t)r * a.d;
+    const TW* er = (const TW*)a.embed + (size_t)tok * a.d;
+    const float* sr = a.steer + (size_t)b * a.d;
+    for (int i = threadIdx.x; i < a.d; i += blockDim.x) {
+        float v = 0.0f;
+        if (active) {
+            v = load_scalar<TW>(er, i);
+            if (a.add_steer) v += sr[i];
+        }
+        xr[i] = v;
+    }
+}
+
+void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
+                       const int32_t* prompt_len, int max_prompt, int chunk) {
+    PlanArgs a;
+    a.kind = kind; a.j = j; a.k = e.cfg.k; a.batch = e.batch; a.cap = e.cap; a.vocab = m.dm.vocab;
+    a.d = m.dm.d_model; a.chunk = chunk; a.max_prompt = max_prompt;
+    a.t = e.ws.t; a.len_d = e.ws.len_d; a.done = e.ws.done; a.hist = e.ws.hist; a.drafts = e.ws.drafts;
+    a.prompt_tok = prompt_tok; a.prompt_len = prompt_len;
+    a.steer = e.ws.steer;
+    a.add_steer = (&m == &e.md) && (kind == kPlanDraft1 || kind == kPlanDraftJ);
+    a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq; a.x = m.x; a.embed = m.embed;
+    if (e.bf16) k_plan_embed<uint16_t><<<rows, 256, 0, s>>>(a);
+    else k_plan_embed<float><<<rows, 256, 0, s>>>(a);
+}
+
+// ===========================================================================
+// GEMV: Y[m][n] (op)= sum_k W[n][k] * Xn[m][k], Xn = optional RMSNorm(X) * gamma.
+// W is streamed once per M-tile of rows; X rows are staged in LDS as fp32.
+// Segments let one launch cover Q|K|V (concatenated output columns) or gate|up
+// (paired rows, SwiGLU epilogue silu(gate) * up).
+// ===========================================================================
+struct GemvArgs {
+    const float* X;
+    const int32_t* in_map;
+    int M, K;
+    const void* gamma;
+    float eps;
+    const void* W[3];
+    int seg_rows[3];
+    int seg_off[3];
+    int nseg, N, epi;
+    float* Y;
+    int ldy;
+    const int32_t* out_map;
+};
+
+constexpr int kGemvThreads = 256;
+constexpr int kGemvRowsPerWave = 4;
+constexpr int kGemvRowsPerBlock = kGemvRowsPerWave * (kGemvThreads / kWave);
+
+template <typename TW>
+struct Vec16;
+template <>
+struct Vec16<uint16_t> {
+    static constexpr int N = 8;
+    __device__ static void load(const uint16_t* p, float* w) {
+        uint4 u = *(const uint4*)p;
+        w[0] = bf16_lo(u.x); w[1] = bf16_hi(u.x); w[2] = bf16_lo(u.y); w[3] = bf16_hi(u.y);
+        w[4] = bf16_lo(u.z); w[5] = bf16_hi(u.z); w[6] = bf16_lo(u.w); w[7] = bf16_hi(u.w);
+    }
+};
+template <>
+struct Vec16<float> {
+    static constexpr int N = 4;
+    __device__ static void load(const float* p, float* w) {
+        float4 u = *(const float4*)p;
+        w[0] = u.x; w[1] = u.y; w[2] = u.z; w[3] = u.w;
+    }
+};
+
+template <typename TW, int MT>
+__global__ __launch_bounds__(kGemvThreads) void k_gemv_vec(GemvArgs a) {
+    extern __shared__ float xs[];  // [MT][K]
+    __shared__ float red[kGemvThreads / kWave];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int K = a.K;
+    const int m0 = blockIdx.y * MT;
+    const int mc = min(MT, a.M - m0);
+
+    // ---- prologue: gather, optionally RMS-normalise, stage in LDS ----
+    for (int m = 0; m < MT; ++m) {
+        float* xr = xs + (size_t)m * K;
+        int src = -1;
+        if (m < mc) src = a.in_map ? a.in_map[m0 + m] : m0 + m;
+        float ss = 0.0f;
+        for (int k = tid; k < K; k += kGemvThreads) {
+            float v = src >= 0 ? a.X[(size_t)src * K + k] : 0.0f;
+            xr[k] = v;
+            ss += v * v;
+        }
+        if (a.gamma) {
+            ss = wave_sum(ss);
+            if (lane == 0) red[wave] = ss;
+            __syncthreads();
+            float tot = 0.0f;
+            for (int w = 0; w < kGemvThreads / kWave; ++w) tot += red[w];
+            float sc = rsqrtf(tot / (float)K + a.eps);
+            for (int k = tid; k < K; k += kGemvThreads) xr[k] = xr[k] * sc * load_scalar<TW>((const TW*)a.gamma, k);
+            __syncthreads();
+        }
+    }
+    __syncthreads();
+
+    constexpr int VN = Vec16<TW>::N;
+    const int nsub = a.epi == kEpiSwiglu ? 2 : 1;
+    for (int rr = 0; rr < kGemvRowsPerWave; ++rr) {
+        const int n = blockIdx.x * kGemvRowsPerBlock + wave * kGemvRowsPerWave + rr;
+        if (n >= a.N) break;
+        float acc[2][MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) { acc[0][m] = 0.0f; acc[1][m] = 0.0f; }
+        for (int sub = 0; sub < nsub; ++sub) {
+            const TW* wr;
+            if (a.epi == kEpiSwiglu) {
+                wr = (const TW*)a.W[sub] + (size_t)n * K;
+            } else {
+                int sgi = 0;
+                while (sgi + 1 < a.nseg && n >= a.seg_off[sgi + 1]) ++sgi;
+                wr = (const TW*)a.W[sgi] + (size_t)(n - a.seg_off[sgi]) * K;
+            }
+            for (int k = lane * VN; k < K; k += kWave * VN) {
+                float w[VN];
+                Vec16<TW>::load(wr + k, w);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const float* xv = xs + (size_t)m * K + k;
+                    float s = 0.0f;
+#pragma unroll
+                    for (int e2 = 0; e2 < VN; ++e2) s += w[e2] * xv[e2];
+                    acc[sub][m] += s;
+                }
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            acc[0][m] = wave_sum(acc[0][m]);
+            if (nsub == 2) acc[1][m] = wave_sum(acc[1][m]);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            if (lane == m && m < mc) {
+                int orow = a.out_map ? a.out_map[m0 + m] : m0 + m;
+                if (orow >= 0) {
+                    float* yp = a.Y + (size_t)orow * a.ldy + n;
+                    if (a.epi == kEpiStore) *yp = acc[0][m];
+                    else if (a.epi == kEpiAdd) *yp += acc[0][m];
+                    else *yp = silu(acc[0][m]) * acc[1][m];
+                }
+            }
+        }
+    }
+}
+
+void launch_gemv(hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K, const void* gamma,
+                 float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y, int ldy,
+                 const int32_t* out_map) {
+    GemvArgs a;
+    a.X = X; a.in_map = in_map; a.M = M; a.K = K; a.gamma = gamma; a.eps = eps;
+    int off = 0;
+    for (int i = 0; i < 3; ++i) {
+        a.W[i] = i < nseg ? W[i] : nullptr;
+        a.seg_rows[i] = i < nseg ? seg_rows[i] : 0;
+        a.seg_off[i] = off;
+        off += a.seg_rows[i];
+    }
+    a.nseg = nseg;
+    a.N = epi == kEpiSwiglu ? seg_rows[0] : off;
+    a.epi = epi; a.Y = Y; a.ldy = ldy; a.out_map = out_map;
+    // rows staged per pass: as many as fit 64 KiB of LDS, at most 8
+    int mt = 8;
+    while (mt > 1 && (mt / 2 >= M || (size_t)mt * K * 4 > 65536)) mt >>= 1;
+    dim3 grid((a.N + kGemvRowsPerBlock - 1) / kGemvRowsPerBlock, (M + mt - 1) / mt);
+    size_t sh = (size_t)mt * K * 4;
+#define SD2_GEMV_CASE(MTV)                                                                  \
+    case MTV:                                                                               \
+        if (bf16) k_gemv_vec<uint16_t, MTV><<<grid, kGemvThreads, sh, s>>>(a);             \
+        else k_gemv_vec<float, MTV><<<grid, kGemvThreads, sh, s>>>(a);                     \
+        break;
+    switch (mt) {
+        SD2_GEMV_CASE(1)
+        SD2_GEMV_CASE(2)
+        SD2_GEMV_CASE(4)
+        SD2_GEMV_CASE(8)
+    }
+#undef SD2_GEMV_CASE
+}
+
+// ===========================================================================
+// RoPE (rotate-half) on q in place and on k; append k, v of every active row to the cache.
+// ===========================================================================
+struct RopeArgs {
+    float* qkv;
+    int qkv_dim, H, Hkv, hd, cap, max_batch, layer;
+    const int32_t *row_pos, *row_seq;
+    const float *cosv, *sinv;
+    float *kc, *vc;
+};
+
+__global__ __launch_bounds__(128) void k_rope_append(RopeArgs a) {
+    int r = blockIdx.x;
+    int pos = a.row_pos[r];
+    if (pos < 0) return;
+    int b = a.row_seq[r];
+    int half = a.hd / 2;
+    float* q = a.qkv + (size_t)r * a.qkv_dim;
+    float* k = q + a.H * a.hd;
+    const float* v = k + a.Hkv * a.hd;
+    const float* cr = a.cosv + (size_t)pos * half;
+    const float* sr = a.sinv + (size_t)pos * half;
+    for (int idx = threadIdx.x; idx < a.H * half; idx += blockDim.x) {
+        int h = idx / half, i = idx % half;
+        float* qh = q + h * a.hd;
+        float x0 = qh[i], x1 = qh[i + half], c = cr[i], sn = sr[i];
+        qh[i] = x0 * c - x1 * sn;
+        qh[i + half] = x1 * c + x0 * sn;
+    }
+    size_t base = ((size_t)a.layer * a.max_batch + b) * a.Hkv;
+    for (int idx = threadIdx.x; idx < a.Hkv * half; idx += blockDim.x) {
+        int h = idx / half, i = idx % half;
+        const float* kh = k + h * a.hd;
+        float x0 = kh[i], x1 = kh[i + half], c = cr[i], sn = sr[i];
+        float* dst = a.kc + ((base + h) * a.cap + pos) * a.hd;
+        dst[i] = x0 * c - x1 * sn;
+        dst[i + half] = x1 * c + x0 * sn;
+    }
+    for (int idx = threadIdx.x; idx < a.Hkv * a.hd; idx += blockDim.x) {
+        int h = idx / a.hd, i = idx % a.hd;
+        a.vc[((base + h) * a.cap + pos) * a.hd + i] = v[idx];
+    }
+}
+
+// ===========================================================================
+// Attention: one block per (row, query head); causal over cache positions 0..pos.
+// ===========================================================================
+struct AttnArgs {
+    const float* qkv;
+    int qkv_dim, H, Hkv, hd, cap, max_batch, layer;
+    const int32_t *row_pos, *row_seq;
+    const float *kc, *vc;
+    float* out;
+    float scale;
+};
+
+constexpr int kAttnThreads = 128;
+
+__global__ __launch_bounds__(kAttnThreads) void k_attention(AttnArgs a) {
+    extern __shared__ float sc[];  // [cap]
+    __shared__ float qs[128];
+    __shared__ float red[kAttnThreads / kWave];
+    int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+    int lane = tid & (kWave - 1), wave = tid / kWave;
+    float* o = a.out + (size_t)r * a.H * a.hd + h * a.hd;
+    int pos = a.row_pos[r];
+    if (pos < 0) {
+        for (int i = tid; i < a.hd; i += kAttnThreads) o[i] = 0.0f;
+        return;
+    }
+    int b = a.row_seq[r];
+    int g = h / (a.H / a.Hkv);
+    const float* q = a.qkv + (size_t)r * a.qkv_dim + h * a.hd;
+    for (int i = tid; i < a.hd; i += kAttnThreads) qs[i] = q[i];
+    __syncthreads();
+    size_t base = (((size_t)a.layer * a.max_batch + b) * a.Hkv + g) * a.cap * a.hd;
+    const float* K = a.kc + base;
+    const float* Vv = a.vc + base;
+    float mx = -INFINITY;
+    for (int j = tid; j <= pos; j += kAttnThreads) {
+        const float* kj = K + (size_t)j * a.hd;
+        float d = 0.0f;
+        for (int i = 0; i < a.hd; i += 4) {
+            float4 kv = *(const float4*)(kj + i);
+            d += qs[i] * kv.x + qs[i + 1] * kv.y + qs[i + 2] * kv.z + qs[i + 3] * kv.w;
+        }
+        d *= a.scale;
+        sc[j] = d;
+        mx = fmaxf(mx, d);
+    }
+    mx = wave_max(mx);
+    if (lane == 0) red[wave] = mx;
+    __syncthreads();
+    mx = red[0];
+    for (int w = 1; w < kAttnThreads / kWave; ++w) mx = fmaxf(mx, red[w]);
+    __syncthreads();
+    float sum = 0.0f;
+    for (int j = tid; j <= pos; j += kAttnThreads) {
+        float e = expf(sc[j] - mx);
+        sc[j] = e;
+        sum += e;
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) red[wave] = sum;
+    __syncthreads();
+    float tot = 0.0f;
+    for (int w = 0; w < kAttnThreads / kWave; ++w) tot += red[w];
+    float inv = 1.0f / tot;
+    for (int i = tid; i < a.hd; i += kAttnThreads) {
+        float acc = 0.0f;
+        for (int j = 0; j <= pos; ++j) acc += sc[j] * Vv[(size_t)j * a.hd + i];
+        o[i] = acc * inv;
+    }
+}
+
+// ===========================================================================
+// One decoder layer on `rows` planned rows.
+// ===========================================================================
+void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows) {
+    const sd2_dims& dm = m.dm;
+    const void* const* W = m.layer + (size_t)layer * 9;
+    int hd = m.hd, H = dm.n_heads, Hkv = dm.n_kv_heads;
+    // QKV with the attention RMSNorm as prologue
+    {
+        const void* ws[3] = {W[kWq], W[kWk], W[kWv]};
+        int rws[3] = {H * hd, Hkv * hd, Hkv * hd};
+        launch_gemv(s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kAttnNorm], dm.rms_eps, ws, rws, 3, kEpiStore,
+                    e.ws.qkv, m.qkv_dim, nullptr);
+    }
+    {
+        RopeArgs a;
+        a.qkv = e.ws.qkv; a.qkv_dim = m.qkv_dim; a.H = H; a.Hkv = Hkv; a.hd = hd; a.cap = e.cap;
+        a.max_batch = e.cfg.max_batch; a.layer = layer; a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq;
+        a.cosv = m.rope_cos; a.sinv = m.rope_sin; a.kc = m.kc; a.vc = m.vc;
+        k_rope_append<<<rows, 128, 0, s>>>(a);
+    }
+    {
+        AttnArgs a;
+        a.qkv = e.ws.qkv; a.qkv_dim = m.qkv_dim; a.H = H; a.Hkv = Hkv; a.hd = hd; a.cap = e.cap;
+        a.max_batch = e.cfg.max_batch; a.layer = layer; a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq;
+        a.kc = m.kc; a.vc = m.vc; a.out = e.ws.attn; a.scale = 1.0f / sqrtf((float)hd);
+        k_attention<<<dim3(rows, H), kAttnThreads, (size_t)e.cap * 4, s>>>(a);
+    }
+    {
+        const void* ws[1] = {W[kWo]};
+        int rws[1] = {dm.d_model};
+        launch_gemv(s, e.bf16, e.ws.attn, nullptr, rows, H * hd, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x,
+                    dm.d_model, nullptr);
+    }
+    {
+        const void* ws[2] = {W[kWg], W[kWu]};
+        int rws[2] = {dm.d_ff, dm.d_ff};
+        launch_gemv(s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kFfnNorm], dm.rms_eps, ws, rws, 2, kEpiSwiglu,
+                    e.ws.ffh, dm.d_ff, nullptr);
+    }
+    {
+        const void* ws[1] = {W[kWd]};
+        int rws[1] = {dm.d_model};
+        launch_gemv(s, e.bf16, e.ws.ffh, nullptr, rows, dm.d_ff, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x, dm.d_model,
+                    nullptr);
+    }
+}
+
+// ===========================================================================
+// Sampler.  Vocabulary rows are cut into kVocabChunks slices; each slice writes a
+// partial, and one wave per sequence combines the 64 partials in a fixed order.
+// ===========================================================================
+struct SampArgs {
+    const float *logits_v, *logits_d;
+    int V, k, batch, chunk;  // chunk: slice length, a multiple of 4
+    float T;
+    uint64_t seed;
+    const int32_t *t, *done;
+    int32_t *drafts, *own_drafts, *n_eff, *own_n, *own_y, *steer_map;
+    const int32_t *forced, *forced_on;
+    VPart* part;
+    float *lse_v, *lse_d;
+    int32_t* argmax_v;
+    int j;
+    int32_t *out_tokens, *out_counts, *len_v, *len_d, *produced, *hist, *tt, *done_w;
+    int cap, max_new;
+};
+
+__device__ __forceinline__ int clamp_tok(int v, int V) { return v < 0 ? 0 : (v >= V ? V - 1 : v); }
+
+__device__ __forceinline__ void block_argbest(ArgBest& a, ArgBest* sh) {
+    int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    a = wave_argbest(a);
+    __syncthreads();
+    if (lane == 0) sh[wave] = a;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < (int)(blockDim.x / kWave); ++w)
+            if (better(sh[w].s, sh[w].i, a.s, a.i)) a = sh[w];
+    }
+}
+
+// Draft pick, partial: best of l/T + Gumbel (or l when greedy) over one vocabulary slice.
+__global__ __launch_bounds__(256) void k_pick_partial(SampArgs a) {
+    __shared__ ArgBest sh[4];
+    int c = blockIdx.x, b = blockIdx.y;
+    const float* row = a.logits_d + ((size_t)b * a.k + (a.j - 1)) * a.V;
+    int v0 = c * a.chunk, v1 = min(a.V, v0 + a.chunk);
+    uint32_t t = (uint32_t)a.t[b];
+    ArgBest best{-INFINITY, 0x7fffffff};
+    for (int q = v0 + 4 * threadIdx.x; q < v1; q += 4 * blockDim.x) {
+        if (a.T > 0.0f) {
+            U4 w = philox10(U4{(uint32_t)q >> 2, (uint32_t)a.j, t, (kDraft << 24) | (uint32_t)b}, (uint32_t)a.seed,
+                            (uint32_t)(a.seed >> 32));
+            uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+            for (int e2 = 0; e2 < 4 && q + e2 < v1; ++e2) {
+                float sc = row[q + e2] / a.T + gumbel(ws[e2]);
+                if (better(sc, q + e2, best.s, best.i)) best = ArgBest{sc, q + e2};
+            }
+        } else {
+            for (int e2 = 0; e2 < 4 && q + e2 < v1; ++e2) {
+                float sc = row[q + e2];
+                if (better(sc, q + e2, best.s, best.i)) best = ArgBest{sc, q + e2};
+            }
+        }
+    }
+    block_argbest(best, sh);
+    if (threadIdx.x == 0) {
+        VPart& p = a.part[(size_t)b * kVocabChunks + c];
+        p.best = best.s;
+        p.idx = best.i;
+    }
+}
+
+// Draft pick, final: combine the slices; record the library's own draft and the effective one.
+__global__ __launch_bounds__(64) void k_pick_final(SampArgs a) {
+    int b = blockIdx.x, lane = threadIdx.x;
+    const VPart& p = a.part[(size_t)b * kVocabChunks + lane];
+    ArgBest best = wave_argbest(ArgBest{p.best, p.idx});
+    if (lane == 0) {
+        int own = best.i;
+        int eff = *a.forced_on ? clamp_tok(a.forced[b * (a.k + 2) + a.j - 1], a.V) : own;
+        a.own_drafts[b * a.k + a.j - 1] = own;
+        a.drafts[b * a.k + a.j - 1] = eff;
+    }
+}
+
+void launch_draft_pick(hipStream_t s, Engine& e, int j);
+
+// Log-normaliser partials of the 2k+1 rows of each sequence (k+1 verifier rows, then k
+// drafter rows); greedy mode computes argmax partials of the verifier rows instead.
+__global__ __launch_bounds__(256) void k_row_partial(SampArgs a) {
+    __shared__ float shm[4], shs[4];
+    __shared__ ArgBest sha[4];
+    int c = blockIdx.x, rowid = blockIdx.y;
+    int per = 2 * a.k + 1;
+    int b = rowid / per, i = rowid % per;
+    const float* row = i <= a.k ? a.logits_v + ((size_t)b * (a.k + 1) + i) * a.V
+                                : a.logits_d + ((size_t)b * a.k + (i - a.k - 1)) * a.V;
+    int v0 = c * a.chunk, v1 = min(a.V, v0 + a.chunk);
+    VPart& p = a.part[(size_t)rowid * kVocabChunks + c];
+    if (a.T > 0.0f) {
+        float m = -INFINITY, sm = 0.0f;
+        for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) lse_merge(m, sm, row[v] / a.T, 1.0f);
+        wave_lse(m, sm);
+        int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+        if (lane == 0) { shm[wave] = m; shs[wave] = sm; }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            for (int w = 1; w < (int)(blockDim.x / kWave); ++w) lse_merge(m, sm, shm[w], shs[w]);
+            p.m = m;
+            p.s = sm;
+        }
+    } else {
+        ArgBest best{-INFINITY, 0x7fffffff};
+        if (i <= a.k)
+            for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x)
+                if (better(row[v], v, best.s, best.i)) best = ArgBest{row[v], v};
+        block_argbest(best, sha);
+        if (threadIdx.x == 0) { p.best = best.s; p.idx = best.i; }
+    }
+}
+
+// Accept/reject: one wave per sequence.
+__global__ __launch_bounds__(64) void k_accept(SampArgs a) {
+    int b = blockIdx.x, lane = threadIdx.x;
+    int per = 2 * a.k + 1;
+    __shared__ float lse[2 * kMaxK + 1];
+    __shared__ int amax[kMaxK + 1];
+    for (int i = 0; i < per; ++i) {
+        const VPart& p = a.part[((size_t)b * per + i) * kVocabChunks + lane];
+        if (a.T > 0.0f) {
+            float m = p.m, sm = p.s;
+            wave_lse(m, sm);
+            if (lane == 0) lse[i] = m + logf(sm);
+        } else if (i <= a.k) {
+            ArgBest best = wave_argbest(ArgBest{p.best, p.idx});
+            if (lane == 0) amax[i] = best.i;
+        }
+    }
+    if (lane != 0) return;
+    const int* dr = a.drafts + b * a.k;
+    uint32_t t = (uint32_t)a.t[b];
+    int n = 0;
+    if (a.T > 0.0f) {
+        for (int i = 0; i <= a.k; ++i) a.lse_v[b * (a.k + 1) + i] = lse[i];
+        for (int i = 0; i < a.k; ++i) a.lse_d[b * a.k + i] = lse[a.k + 1 + i];
+        for (int i = 0; i < a.k; ++i) {
+            int x = dr[i];
+            float lp = a.logits_v[((size_t)b * (a.k + 1) + i) * a.V + x] / a.T - lse[i];
+            float lq = a.logits_d[((size_t)b * a.k + i) * a.V + x] / a.T - lse[a.k + 1 + i];
+            float ratio = lp - lq;
+            float lu = logf(u01(rng_word(a.seed, (uint32_t)i, 0u, t, kAccept, (uint32_t)b, 0)));
+            if (!(lu < ratio)) break;
+            ++n;
+        }
+    } else {
+        for (int i = 0; i <= a.k; ++i) a.argmax_v[b * (a.k + 1) + i] = amax[i];
+        for (int i = 0; i < a.k; ++i) {
+            if (dr[i] != amax[i]) break;
+            ++n;
+        }
+    }
+    int eff = *a.forced_on ? min(max(a.forced[b * (a.k + 2) + a.k], 0), a.k) : n;
+    a.own_n[b] = n;
+    a.n_eff[b] = eff;
+    a.steer_map[b] = b * (a.k + 1) + eff;
+    if (a.T == 0.0f) a.own_y[b] = amax[eff];
+}
+
+// Final draw, partial: residual (p - q)+ with Gumbel noise after a rejection, and the plain
+// p-Gumbel score (bonus draw after full acceptance, or fallback for an empty residual).
+__global__ __launch_bounds__(256) void k_final_partial(SampArgs a) {
+    __shared__ ArgBest sh1[4], sh2[4];
+    __shared__ int shf[4];
+    int c = blockIdx.x, b = blockIdx.y;
+    int n = a.n_eff[b];
+    const float* pr = a.logits_v + ((size_t)b * (a.k + 1) + n) * a.V;
+    const float* qr = n < a.k ? a.logits_d + ((size_t)b * a.k + n) * a.V : nullptr;
+    float lp = a.lse_v[b * (a.k + 1) + n];
+    float lq = n < a.k ? a.lse_d[b * a.k + n] : 0.0f;
+    uint32_t t = (uint32_t)a.t[b];
+    int v0 = c * a.chunk, v1 = min(a.V, v0 + a.chunk);
+    ArgBest br{-INFINITY, 0x7fffffff}, bp{-INFINITY, 0x7fffffff};
+    int flag = 0;
+    for (int q = v0 + 4 * threadIdx.x; q < v1; q += 4 * blockDim.x) {
+        U4 w = philox10(U4{(uint32_t)q >> 2, 0u, t, (kFinal << 24) | (uint32_t)b}, (uint32_t)a.seed,
+                        (uint32_t)(a.seed >> 32));
+        uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+        for (int e2 = 0; e2 < 4 && q + e2 < v1; ++e2) {
+            int v = q + e2;
+            float g = gumbel(ws[e2]);
+            float sp = pr[v] / a.T + g;
+            if (better(sp, v, bp.s, bp.i)) bp = ArgBest{sp, v};
+            if (qr) {
+                float p = expf(pr[v] / a.T - lp);
+                float qq = expf(qr[v] / a.T - lq);
+                float r = p - qq;
+                if (r > 0.0f) {
+                    flag = 1;
+                    float sr = logf(r) + g;
+                    if (better(sr, v, br.s, br.i)) br = ArgBest{sr, v};
+                }
+            }
+        }
+    }
+    int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    int fl = __any(flag) ? 1 : 0;
+    if (lane == 0) shf[wave] = fl;
+    block_argbest(br, sh1);
+    block_argbest(bp, sh2);
+    if (threadIdx.x == 0) {
+        int f = 0;
+        for (int w = 0; w < (int)(blockDim.x / kWave); ++w) f |= shf[w];
+        VPart& p = a.part[(size_t)b * kVocabChunks + c];
+        p.best = br.s; p.idx = br.i; p.best2 = bp.s; p.idx2 = bp.i; p.flag = f;
+    }
+}
+
+// Combine the final-draw slices, then commit: emit tokens, append history, roll back lengths.
+__global__ __launch_bounds__(64) void k_commit(SampArgs a) {
+    int b = blockIdx.x, lane = threadIdx.x;
+    int y_own;
+    if (a.T > 0.0f) {
+        const VPart& p = a.part[(size_t)b * kVocabChunks + lane];
+        int n = a.n_eff[b];
+        bool res = (n < a.k) && __any(p.flag);
+        ArgBest best = res ? wave_argbest(ArgBest{p.flag ? p.best : -INFINITY, p.flag ? p.idx : 0x7fffffff})
+                           : wave_argbest(ArgBest{p.best2, p.idx2});
+        y_own = best.i;
+        if (lane == 0) a.own_y[b] = y_own;
+    } else {
+        y_own = a.own_y[b];
+    }
+    if (lane != 0) return;
+    int y = *a.forced_on ? clamp_tok(a.forced[b * (a.k + 2) + a.k + 1], a.V) : y_own;
+    int32_t* ot = a.out_tokens + b * (a.k + 1);
+    if (b >= a.batch || a.done_w[b]) {
+        a.out_counts[b] = 0;
+        for (int i = 0; i <= a.k; ++i) ot[i] = -1;
+        return;
+    }
+    int t = a.tt[b], n = a.n_eff[b];
+    int remaining = a.max_new - a.produced[b];
+    int count = min(n + 1, remaining);
+    int32_t* hs = a.hist + (size_t)b * a.cap;
+    for (int i = 0; i < n; ++i) hs[t + i] = a.drafts[b * a.k + i];
+    hs[t + n] = y;
+    for (int i = 0; i <= a.k; ++i) ot[i] = i < count ? hs[t + i] : -1;
+    a.out_counts[b] = count;
+    a.produced[b] += count;
+    if (a.produced[b] >= a.max_new) a.done_w[b] = 1;
+    a.len_v[b] = t + n;
+    a.len_d[b] = min(t + a.k - 1, t + n);
+    a.tt[b] = t + n + 1;
+}
+
+static SampArgs samp_args(Engine& e) {
+    SampArgs a;
+    a.logits_v = e.ws.logits_v; a.logits_d = e.ws.logits_d;
+    a.V = e.mv.dm.vocab; a.k = e.cfg.k; a.batch = e.batch;
+    a.chunk = ((a.V + kVocabChunks - 1) / kVocabChunks + 3) / 4 * 4;
+    a.T = e.cfg.temperature; a.seed = e.cfg.seed;
+    a.t = e.ws.t; a.done = e.ws.done;
+    a.drafts = e.ws.drafts; a.own_drafts = e.ws.own_drafts; a.n_eff = e.ws.n_eff; a.own_n = e.ws.own_n;
+    a.own_y = e.ws.own_y; a.steer_map = e.ws.steer_map;
+    a.forced = e.ws.forced; a.forced_on = e.ws.forced_on;
+    a.part = e.ws.part; a.lse_v = e.ws.lse_v; a.lse_d = e.ws.lse_d; a.argmax_v = e.ws.argmax_v;
+    a.j = 0;
+    a.out_tokens = nullptr; a.out_counts = nullptr;
+    a.len_v = e.ws.len_v; a.len_d = e.ws.len_d; a.produced = e.ws.produced; a.hist = e.ws.hist; a.tt = e.ws.t;
+    a.done_w = e.ws.done;
+    a.cap = e.cap; a.max_new = e.cfg.max_new_tokens;
+    return a;
+}
+
+void launch_draft_pick(hipStream_t s, Engine& e, int j) {
+    SampArgs a = samp_args(e);
+    a.j = j;
+    k_pick_partial<<<dim3(kVocabChunks, e.batch), 256, 0, s>>>(a);
+    k_pick_final<<<e.batch, 64, 0, s>>>(a);
+}
+
+void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t* out_counts) {
+    SampArgs a = samp_args(e);
+    a.out_tokens = out_tokens;
+    a.out_counts = out_counts;
+    int per = 2 * e.cfg.k + 1;
+    k_row_partial<<<dim3(kVocabChunks, e.batch * per), 256, 0, s>>>(a);
+    k_accept<<<e.batch, 64, 0, s>>>(a);
+    if (e.cfg.temperature > 0.0f) k_final_partial<<<dim3(kVocabChunks, e.batch), 256, 0, s>>>(a);
+    k_commit<<<e.batch, 64, 0, s>>>(a);
+}
+
+// ===========================================================================
+// Prefill helpers.
+// ===========================================================================
+// Keep the verifier residual of the row at position len-2 (the steering tap of the first round).
+__global__ void k_prefill_capture(const int32_t* row_pos, const int32_t* row_seq, const int32_t* prompt_len,
+                                  int max_prompt, const float* x, float* hcap, int d, int batch) {
+    int r = blockIdx.x;
+    int pos = row_pos[r];
+    if (pos < 0) return;
+    int b = row_seq[r];
+    if (b >= batch || pos != min(prompt_len[b], max_prompt) - 2) return;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) hcap[(size_t)b * d + i] = x[(size_t)r * d + i];
+}
+
+void launch_prefill_capture(hipStream_t s, Engine& e, int rows, const int32_t* prompt_len, int max_prompt) {
+    k_prefill_capture<<<rows, 256, 0, s>>>(e.ws.row_pos, e.ws.row_seq, prompt_len, max_prompt, e.mv.x, e.ws.hcap,
+                                           e.mv.dm.d_model, e.batch);
+}
+
+__global__ void k_prefill_finish(int batch, const int32_t* prompt_tok, const int32_t* prompt_len, int max_prompt,
+                                 int32_t* hist, int cap, int32_t* t, int32_t* len_v, int32_t* len_d,
+                                 int32_t* produced, int32_t* done, float* steer, int dD, int vocab) {
+    int b = blockIdx.x;
+    int p = min(max(prompt_len[b], 1), max_prompt);
+    for (int i = threadIdx.x; i < p; i += blockDim.x) {
+        int tok = prompt_tok[(size_t)b * max_prompt + i];
+        hist[(size_t)b * cap + i] = tok < 0 ? 0 : (tok >= vocab ? vocab - 1 : tok);
+    }
+    if (p < 2)
+        for (int i = threadIdx.x; i < dD; i += blockDim.x) steer[(size_t)b * dD + i] = 0.0f;
+    if (threadIdx.x == 0) {
+        t[b] = p;
+        len_v[b] = p - 1;
+        len_d[b] = p - 1;
+        produced[b] = 0;
+        done[b] = 0;
+    }
+}
+
+void launch_prefill_finish(hipStream_t s, Engine& e, int batch, const int32_t* prompt_tok, const int32_t* prompt_len,
+                           int max_prompt) {
+    k_prefill_finish<<<batch, 256, 0, s>>>(batch, prompt_tok, prompt_len, max_prompt, e.ws.hist, e.cap, e.ws.t,
+                                           e.ws.len_v, e.ws.len_d, e.ws.produced, e.ws.done, e.ws.steer,
+                                           e.md.dm.d_model, e.mv.dm.vocab);
+}
+
+// Final-norm rows (debug read of the verifier's hidden states).
+template <typename TW>
+__global__ void k_rmsnorm_rows(const float* X, int d, const TW* gamma, float eps, float* Y) {
+    __shared__ float red[4];
+    int r = blockIdx.x;
+    const float* x = X + (size_t)r * d;
+    float ss = 0.0f;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) ss += x[i] * x[i];
+    ss = wave_sum(ss);
+    int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
+    if (lane == 0) red[wave] = ss;
+    __syncthreads();
+    float tot = 0.0f;
+    for (int w = 0; w < (int)(blockDim.x / 64); ++w) tot += red[w];
+    float sc = rsqrtf(tot / (float)d + eps);
+    for (int i = threadIdx.x; i < d; i += blockDim.x) Y[(size_t)r * d + i] = x[i] * sc * load_scalar<TW>(gamma, i);
+}
+
+void launch_rmsnorm_rows(hipStream_t s, const float* X, int rows, int d, const void* gamma, bool bf16, float eps,
+                         float* Y) {
+    if (bf16) k_rmsnorm_rows<uint16_t><<<rows, 256, 0, s>>>(X, d, (const uint16_t*)gamma, eps, Y);
+    else k_rmsnorm_rows<float><<<rows, 256, 0, s>>>(X, d, (const float*)gamma, eps, Y);
+}
+
+__global__ void k_set_flag(int32_t* f, int v) { *f = v; }
+void launch_set_flag(hipStream_t s, int32_t* flag, int v) { k_set_flag<<<1, 1, 0, s>>>(flag, v); }
+
+}  // namespace sd2
