@@ -1,0 +1,214 @@
+"""Benchmark of one SD^2 speculative-decoding round on one MI355X.
+
+A step is one call of sd2_round: k steered drafter steps, the (k+1)-row verifier
+block forward, the accept/resample decision, commit with KV-length rollback and
+the steering projection, for every sequence of the batch.  Inputs are synthetic
+(seeded N(0, 0.02) weights, uniform-random prompt ids) with the shapes of the
+named workload; weights and prompts are resident in HBM before timing starts.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def weight_bytes(dm, esize):
+    hd = dm.head_dim
+    per_layer = (dm.n_heads * hd + 2 * dm.n_kv_heads * hd) * dm.d_model + dm.d_model * dm.n_heads * hd \
+        + 3 * dm.d_ff * dm.d_model
+    return (dm.n_layers * per_layer + dm.vocab * dm.d_model) * esize
+
+
+def kv_row_bytes(dm):
+    # K and V of one position across all layers, stored as fp32
+    return dm.n_layers * dm.n_kv_heads * dm.head_dim * 2 * 4
+
+
+def round_bytes(wl, t_avg):
+    """Algorithmic HBM bytes of one round for one sequence at round-start length t_avg:
+    every weight once per forward (verifier once, drafter k times, W_s once) plus the KV rows
+    each attention pass must read and the rows it appends."""
+    es = 2 if wl.dtype == "bf16" else 4
+    k = wl.k
+    w = weight_bytes(wl.verifier, es) + k * weight_bytes(wl.drafter, es) + wl.drafter.d_model * wl.verifier.d_model * es
+    kv_v = (t_avg + k + (k + 1)) * kv_row_bytes(wl.verifier)
+    kv_d = (k * t_avg + k * (k - 1) / 2 + (k + 1)) * kv_row_bytes(wl.drafter)
+    return w, kv_v, kv_d
+
+
+def cpu_baseline(wl, wv, wd, ws, toks, lens, budget_s):
+    """The oracle as it stands, on a bounded sample: prefill a short prompt prefix, then time rounds."""
+    import oracle
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    prefix = min(16, int(lens[0]))
+    o = oracle.Oracle(wl, wv, wd, ws, max_batch=1, cap=prefix + wl.new_tokens + wl.k + 1)
+    o.prefill_one(0, toks[0, :prefix])
+    tokens, rounds, t0 = 0, 0, time.time()
+    while time.time() - t0 < budget_s and not o.state(0)["done"]:
+        out, lg, _ = o.round_one(0)
+        tokens += len(out)
+        rounds += 1
+        log(f"cpu oracle round {rounds}: {len(out)} tokens, {time.time() - t0:.1f}s")
+    dt = time.time() - t0
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"sequence 0 only, first {prefix} prompt tokens prefilled (untimed), then {rounds} rounds "
+                      f"({tokens} tokens) timed; float64 C oracle, OpenMP over output rows"}
+
+
+def main():
+    import sd2_inputs as si
+
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=si.LLAMA8B.name, choices=list(si.BY_NAME))
+    ap.add_argument("--prof-rounds", type=int, default=3)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2511_09844_amd import binding as B
+
+    B.load()
+    wl = si.BY_NAME[args.workload]
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    keep_host = not args.no_cpu_baseline
+    host = {0: {"layers": []}, 1: {"layers": []}}
+    models = []
+    for which in (0, 1):
+        items = []
+        for key, arr in si.iter_model_tensors(wl, which):
+            items.append((key, arr))
+        if keep_host:
+            h = host[which]
+            for key, arr in items:
+                if key[0] == "layers":
+                    while len(h["layers"]) <= key[1]:
+                        h["layers"].append([])
+                    h["layers"][key[1]].append(arr)
+                else:
+                    h[key[0]] = arr
+        models.append(B.DeviceModel(items, dev))
+        del items
+        log(f"model {which} generated and uploaded ({time.time() - t0:.1f}s)")
+    ws = si.steer_weights(wl)
+    ws_dev = B.to_device(ws, dev)
+    toks, lens = si.prompts(wl)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        eng = B.Engine(B.config_of(wl), models[0], models[1], ws_dev, stream=stream, device=dev)
+        t_tok = torch.from_numpy(toks).to(dev)
+        t_len = torch.from_numpy(lens).to(dev)
+        torch.cuda.synchronize()
+        tp = time.time()
+        eng.prefill(t_tok, t_len, wl.max_prompt)
+        torch.cuda.synchronize()
+        log(f"prefill done in {time.time() - tp:.2f}s")
+        for _ in range(args.warmup):
+            eng.round()
+        torch.cuda.synchronize()
+        st0 = eng.state()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(args.steps):
+            eng.round()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1)
+        st1 = eng.state()
+        log(f"timed {args.steps} rounds: {ms:.2f} ms")
+        # kernel-level timing: HIP events around every launch of the same rounds, recorded into the graph
+        prof = {c: [0, 0.0, 0.0] for c in (B.PROF_GEMV, B.PROF_ATTN, B.PROF_SAMPLER, B.PROF_OTHER)}
+        if args.prof_rounds > 0:
+            eng.profile(True)
+            for _ in range(args.prof_rounds):
+                eng.round()
+                for c in prof:
+                    n, pms, pby = eng.profile_read(c)
+                    prof[c][0] += n
+                    prof[c][1] += pms
+                    prof[c][2] += pby
+            eng.profile(False)
+        torch.cuda.synchronize()
+
+    active = [b for b in range(wl.batch) if not st0[b]["done"]]
+    tokens = sum(st1[b]["produced"] - st0[b]["produced"] for b in range(wl.batch))
+    sec = ms / 1e3
+    tau = tokens / (args.steps * max(1, len(active)))
+    w_b, kvv_b, kvd_b = 0.0, 0.0, 0.0
+    for b in active:
+        t_avg = st0[b]["t"] + (st1[b]["t"] - st0[b]["t"]) * (args.steps - 1) / (2 * args.steps)
+        w, kvv, kvd = round_bytes(wl, t_avg)
+        w_b = w
+        kvv_b += kvv
+        kvd_b += kvd
+    bytes_round = w_b + kvv_b + kvd_b
+    ms_round = ms / args.steps
+    g_n, g_ms, g_by = prof[B.PROF_GEMV]
+    gemv_gbs = g_by / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
+    log(f"round: {ms_round:.3f} ms, {bytes_round / 1e9:.3f} GB algorithmic -> "
+        f"{bytes_round / (ms_round / 1e3) / 1e9:.0f} GB/s ({bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS:.1%} of HBM)")
+    for c, name in ((B.PROF_GEMV, "gemv"), (B.PROF_ATTN, "attn"), (B.PROF_SAMPLER, "sampler"), (B.PROF_OTHER, "other")):
+        n, pms, pby = prof[c]
+        log(f"  {name}: {n / max(1, args.prof_rounds):.0f} launches/round, {pms / max(1, args.prof_rounds):.3f} ms/round"
+            + (f", {pby / (pms / 1e3) / 1e9:.0f} GB/s" if pby and pms else ""))
+
+    result = {
+        "metric": "generated tokens/s at 1 GPU (one SD2 round per step)",
+        "value": tokens / sec,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_round,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 weights, f32 activations/KV" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic: seeded N(0,0.02) weights, uniform-random prompt ids",
+        "config": {"workload": wl.name, "batch": wl.batch, "k": wl.k, "prompt": list(wl.prompt),
+                   "new_tokens": wl.new_tokens, "temperature": wl.temperature,
+                   "verifier": f"L{wl.verifier.n_layers} d{wl.verifier.d_model} H{wl.verifier.n_heads}/"
+                               f"{wl.verifier.n_kv_heads} F{wl.verifier.d_ff} V{wl.verifier.vocab}",
+                   "drafter": f"L{wl.drafter.n_layers} d{wl.drafter.d_model} H{wl.drafter.n_heads}/"
+                              f"{wl.drafter.n_kv_heads} F{wl.drafter.d_ff}"},
+        "block_efficiency": tau,
+        "round_bytes": bytes_round,
+        "round_hbm_frac": bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS,
+        "roofline": {"bound": "hbm", "kernel": "k_gemv (all weight-streaming projections + LM heads)",
+                     "achieved": gemv_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gemv_gbs / PEAK_HBM_GBS,
+                     "traffic": None, "launches_per_round": g_n / max(1, args.prof_rounds),
+                     "avg_launch_us": g_ms / max(1, g_n) * 1e3,
+                     "bytes_per_launch": g_by / max(1, g_n)},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, host[0], host[1], ws, toks, lens, args.cpu_budget)
+    eng.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

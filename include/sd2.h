@@ -153,6 +153,26 @@ const char* sd2_last_error(sd2_handle_t h);
 /* Copy a debug buffer of the last round into host memory dst (bytes must match). */
 sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes);
 
+/* Kernel classes for sd2_profile_read. */
+#define SD2_PROF_GEMV 1      /* weight-streaming projections and LM heads */
+#define SD2_PROF_ATTN 2      /* attention over the KV cache */
+#define SD2_PROF_SAMPLER 3   /* draft picks, accept test, final draw, commit */
+#define SD2_PROF_OTHER 4     /* embedding/planning, RoPE and cache append */
+
+/*
+ * Measurement hook.  enable != 0: following rounds record a HIP event pair on the handle's
+ * stream around every kernel launch (the recorded round graph then carries the event nodes);
+ * enable == 0 turns this off.  Rounds stay functionally identical.
+ */
+sd2_status sd2_profile(sd2_handle_t h, int32_t enable);
+
+/*
+ * For the last profiled round (synchronises the stream): number of launches of class cls,
+ * the sum of their event-to-event durations in milliseconds, and the sum of their algorithmic
+ * bytes (for SD2_PROF_GEMV: weights + input rows + output rows; 0 for other classes).
+ */
+sd2_status sd2_profile_read(sd2_handle_t h, int32_t cls, int32_t* launches, double* total_ms, double* bytes);
+
 #ifdef __cplusplus
 }
 #endif

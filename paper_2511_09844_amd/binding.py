@@ -18,7 +18,8 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "capacity", -3: "state", -4: "hip
 DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V = range(1, 10)
 
 EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
-           "sd2_status_string", "sd2_last_error", "sd2_debug_read"]
+           "sd2_status_string", "sd2_last_error", "sd2_debug_read", "sd2_profile", "sd2_profile_read"]
+PROF_GEMV, PROF_ATTN, PROF_SAMPLER, PROF_OTHER = 1, 2, 3, 4
 
 
 class Dims(ctypes.Structure):
@@ -66,6 +67,11 @@ def load():
         lib.sd2_last_error.restype = ctypes.c_char_p
         lib.sd2_debug_read.argtypes = [P, ctypes.c_int32, P, ctypes.c_size_t]
         lib.sd2_debug_read.restype = ctypes.c_int32
+        lib.sd2_profile.argtypes = [P, ctypes.c_int32]
+        lib.sd2_profile.restype = ctypes.c_int32
+        lib.sd2_profile_read.argtypes = [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+        lib.sd2_profile_read.restype = ctypes.c_int32
         _lib = lib
     return _lib
 
@@ -195,6 +201,16 @@ class Engine:
         out = np.zeros(shp, dtype=dt)
         check(self.lib.sd2_debug_read(self.h, what, out.ctypes.data, out.nbytes), self.h, "sd2_debug_read")
         return out
+
+    def profile(self, enable: bool):
+        check(self.lib.sd2_profile(self.h, 1 if enable else 0), self.h, "sd2_profile")
+
+    def profile_read(self, cls: int):
+        """(launches, total ms, algorithmic bytes) of kernel class cls in the last profiled round."""
+        n, ms, by = ctypes.c_int32(), ctypes.c_double(), ctypes.c_double()
+        check(self.lib.sd2_profile_read(self.h, cls, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(by)),
+              self.h, "sd2_profile_read")
+        return n.value, ms.value, by.value
 
     def state(self):
         s = self.debug(DBG_STATE)

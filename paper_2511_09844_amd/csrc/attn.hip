@@ -1,0 +1,273 @@
+// Grouped-query causal attention over the fp32 KV cache for a block of query rows.
+//
+// Split over cache positions (flash-decoding): one workgroup owns up to 32 query vectors of one
+// sequence -- either one query head for a tile of rows (small batches: more workgroups, the KV
+// head shared through L2) or all query heads of one KV head (large batches: each cached K/V
+// row read once) -- and one span of kSplit cache positions.  It walks its span in chunks of 64
+// positions with an online softmax (running max, running sum, rescaled output), keeping the
+// next chunk's K/V in flight in registers while the current chunk is scored from LDS, and
+// writes an un-normalised partial (output, max, sum).  A second kernel merges the spans of
+// each (row, head) in span order (a kernel boundary, rather than an in-kernel hand-off, makes
+// the partials visible: on this part a device-scope release fence writes back the whole L2).  The causal mask is key position <= query position; rows
+// with position -1 are inactive and produce zeros.  Workgroups of one KV head are placed on
+// the same XCD (workgroup ids are dealt round-robin over the 8 XCDs), so a KV head is fetched
+// into one L2 only.
+#include <math.h>
+
+#include "device_common.h"
+#include "engine.h"
+
+namespace sd2 {
+
+constexpr int kAttnCL = 64;   // cache positions per chunk
+constexpr int kSplit = 128;   // cache positions per workgroup
+constexpr int kAttnQT = 32;   // query vectors per workgroup
+constexpr int kAttnT = 256;
+constexpr int kXcds = 8;
+
+typedef float f4_t __attribute__((ext_vector_type(4)));
+
+struct AttnArgs {
+    const float* q;
+    int q_stride;
+    const float *kc, *vc;
+    float* out;
+    const int32_t* row_pos;
+    int rps, H, Hkv, hd, cap, max_batch, layer;
+    int hp;     // query heads per workgroup: 1 or H/Hkv
+    int nrt;    // row tiles per (sequence, head group)
+    int ngrp;   // number of (sequence, KV head, row tile) groups
+    int nsplit; // position spans per group
+    float scale;
+    float* part;     // [row][head][nsplit][HD + 2]
+};
+
+// Request chunk c of K and V (positions past maxpos re-read the last valid row; they are masked).
+template <int HD, int F4>
+__device__ __forceinline__ void fetch_chunk(f4_t (&pk)[F4], f4_t (&pv)[F4], const float* kg, const float* vg,
+                                            int c, int maxpos, int tid) {
+#pragma unroll
+    for (int i = 0; i < F4; ++i) {
+        int e4 = tid + i * kAttnT;  // float4 index within the chunk
+        int pos = c * kAttnCL + (e4 * 4) / HD;
+        int pp = pos <= maxpos ? pos : maxpos;
+        pk[i] = *(const f4_t*)(kg + (size_t)pp * HD + (e4 * 4) % HD);
+        pv[i] = *(const f4_t*)(vg + (size_t)pp * HD + (e4 * 4) % HD);
+    }
+}
+
+template <int HD>
+__global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
+    extern __shared__ __attribute__((aligned(16))) float sm[];
+    __shared__ int qpos[kAttnQT];
+    __shared__ int qrow[kAttnQT];
+    __shared__ int qhead[kAttnQT];
+    __shared__ float mrun[kAttnQT], lrun[kAttnQT], rescale[kAttnQT];
+    __shared__ int maxpos_s;
+    const int tid = threadIdx.x;
+    const int G = a.H / a.Hkv;
+    const int members = G / a.hp;  // workgroups per group
+    // XCD-aware decode: the `members` workgroups of a group share wg % 8
+    const int wg = blockIdx.x / a.nsplit;
+    const int sp = blockIdx.x % a.nsplit;
+    const int gi = (wg / (kXcds * members)) * kXcds + wg % kXcds;
+    const int mi = (wg / kXcds) % members;
+    if (gi >= a.ngrp) return;
+    const int rt = gi % a.nrt;
+    const int kvh = (gi / a.nrt) % a.Hkv;
+    const int b = gi / (a.nrt * a.Hkv);
+    const int hbase = kvh * G + mi * a.hp;
+    const int rows_per_tile = kAttnQT / a.hp;
+    const int r0 = rt * rows_per_tile;
+    const int nrows = min(rows_per_tile, a.rps - r0);
+    const int nq = nrows * a.hp;
+
+    float* qs = sm;                          // [QT][HD]   (pre-scaled queries)
+    float* ks = qs + kAttnQT * HD;           // [CL][HD+1]
+    float* vs = ks + kAttnCL * (HD + 1);     // [CL][HD]
+    float* ps = vs + kAttnCL * HD;           // [QT][CL]
+
+    if (tid == 0) maxpos_s = -1;
+    __syncthreads();
+    if (tid < kAttnQT) {
+        int p = -1, row = 0, h = 0;
+        if (tid < nq) {
+            row = b * a.rps + r0 + tid / a.hp;
+            h = hbase + tid % a.hp;
+            p = a.row_pos[row];
+        }
+        qpos[tid] = p;
+        qrow[tid] = row;
+        qhead[tid] = h;
+        mrun[tid] = -INFINITY;
+        lrun[tid] = 0.f;
+        if (p >= 0) atomicMax(&maxpos_s, p);
+    }
+    __syncthreads();
+    const int p_lo = sp * kSplit;
+    const int maxpos = min(maxpos_s, p_lo + kSplit - 1);  // last position this span scores
+    for (int idx = tid; idx < nq * HD; idx += kAttnT) {
+        int qi = idx / HD, d = idx % HD;
+        qs[idx] = a.q[(size_t)qrow[qi] * a.q_stride + qhead[qi] * HD + d] * a.scale;
+    }
+    const size_t head_base = (((size_t)a.layer * a.max_batch + b) * a.Hkv + kvh) * a.cap * HD;
+    const float* kg = a.kc + head_base;
+    const float* vg = a.vc + head_base;
+
+    // output accumulators: thread owns dims d = tid % HD of query vectors qi = tid / HD + j * (T / HD)
+    constexpr int QSTEP = kAttnT / HD;
+    constexpr int NACC = kAttnQT / QSTEP;
+    float acc[NACC];
+#pragma unroll
+    for (int j = 0; j < NACC; ++j) acc[j] = 0.f;
+    const int od = tid % HD, oq0 = tid / HD;
+
+    // K/V chunk prefetch: each thread moves CL*HD/T float4 pairs per chunk
+    constexpr int F4 = kAttnCL * HD / 4 / kAttnT;
+    f4_t pk[F4], pv[F4];
+    const int nchunks = maxpos >= p_lo ? (maxpos - p_lo) / kAttnCL + 1 : 0;
+    const float* kgs = kg + (size_t)p_lo * HD;
+    const float* vgs = vg + (size_t)p_lo * HD;
+    if (nchunks > 0) fetch_chunk<HD, F4>(pk, pv, kgs, vgs, 0, maxpos - p_lo, tid);
+    for (int c = 0; c < nchunks; ++c) {
+        __syncthreads();  // previous chunk fully consumed
+#pragma unroll
+        for (int i = 0; i < F4; ++i) {
+            int e4 = tid + i * kAttnT;
+            int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
+            float* kd = ks + j * (HD + 1) + d;
+            kd[0] = pk[i][0]; kd[1] = pk[i][1]; kd[2] = pk[i][2]; kd[3] = pk[i][3];
+            *(f4_t*)(vs + j * HD + d) = pv[i];
+        }
+        __syncthreads();
+        if (c + 1 < nchunks) fetch_chunk<HD, F4>(pk, pv, kgs, vgs, c + 1, maxpos - p_lo, tid);
+        const int j0 = p_lo + c * kAttnCL;
+        // scores of every (query, key) pair of the chunk; 64 threads per query vector
+        for (int idx = tid; idx < nq * kAttnCL; idx += kAttnT) {
+            int qi = idx / kAttnCL, j = idx % kAttnCL;
+            float s = -INFINITY;
+            if (j0 + j <= qpos[qi]) {
+                const float* qr = qs + qi * HD;
+                const float* kr = ks + j * (HD + 1);
+                float d0 = 0.f;
+#pragma unroll 8
+                for (int d = 0; d < HD; ++d) d0 += qr[d] * kr[d];
+                s = d0;
+            }
+            // row max and sum over the 64 keys held by this wave's 64 lanes
+            float mx = wave_max(s);
+            float mnew = fmaxf(mrun[qi], mx);
+            float p = (s == -INFINITY) ? 0.f : expf(s - mnew);
+            float sum = wave_sum(p);
+            ps[qi * kAttnCL + j] = p;
+            if (j == 0) {
+                float sc = mrun[qi] == -INFINITY ? 0.f : expf(mrun[qi] - mnew);
+                rescale[qi] = sc;
+                lrun[qi] = lrun[qi] * sc + sum;
+                mrun[qi] = mnew;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int jj = 0; jj < NACC; ++jj) {
+            int qi = oq0 + jj * QSTEP;
+            if (qi < nq) {
+                float o = acc[jj] * rescale[qi];
+                const float* pr = ps + qi * kAttnCL;
+#pragma unroll 8
+                for (int j = 0; j < kAttnCL; ++j) o += pr[j] * vs[j * HD + od];
+                acc[jj] = o;
+            }
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int jj = 0; jj < NACC; ++jj) {
+        int qi = oq0 + jj * QSTEP;
+        if (qi < nq) {
+            float* pp = a.part + (((size_t)qrow[qi] * a.H + qhead[qi]) * a.nsplit + sp) * (HD + 2);
+            pp[od] = acc[jj];
+            if (od == 0) {
+                pp[HD] = mrun[qi];
+                pp[HD + 1] = lrun[qi];
+            }
+        }
+    }
+}
+
+// Merge the position spans of every (row, head) in span order: out = sum_s e^(m_s - M) O_s /
+// sum_s e^(m_s - M) l_s.  One thread per output element.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_merge(const float* __restrict__ part, const int32_t* __restrict__ row_pos,
+                                                    float* __restrict__ out, int rows, int H, int nsplit) {
+    size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (size_t)rows * H * HD) return;
+    int d = idx % HD;
+    size_t rh = idx / HD;
+    int row = (int)(rh / H);
+    int pos = row_pos[row];
+    float res = 0.f;
+    if (pos >= 0) {
+        const float* pp = part + rh * nsplit * (HD + 2);
+        int live = min(nsplit, pos / kSplit + 1);
+        float M = -INFINITY;
+        for (int s = 0; s < live; ++s) M = fmaxf(M, pp[(size_t)s * (HD + 2) + HD]);
+        float L = 0.f, O = 0.f;
+        for (int s = 0; s < live; ++s) {
+            const float* e = pp + (size_t)s * (HD + 2);
+            if (e[HD] == -INFINITY) continue;
+            float w = expf(e[HD] - M);
+            L += w * e[HD + 1];
+            O += w * e[d];
+        }
+        res = L > 0.f ? O / L : 0.f;
+    }
+    out[idx] = res;
+}
+
+static size_t attn_lds(int hd) {
+    return sizeof(float) * ((size_t)kAttnQT * hd + (size_t)kAttnCL * (hd + 1) + (size_t)kAttnCL * hd +
+                            (size_t)kAttnQT * kAttnCL);
+}
+
+void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride) {
+    const sd2_dims& dm = m.dm;
+    AttnArgs a;
+    a.q = q; a.q_stride = q_stride; a.kc = m.kc; a.vc = m.vc; a.out = e.ws.attn; a.row_pos = e.ws.row_pos;
+    a.rps = rps; a.H = dm.n_heads; a.Hkv = dm.n_kv_heads; a.hd = m.hd; a.cap = e.cap; a.max_batch = e.cfg.max_batch;
+    a.layer = layer;
+    int nseq = rows / rps;
+    int G = dm.n_heads / dm.n_kv_heads;
+    // all heads of a group per workgroup once the groups alone fill the chip and fit a tile
+    a.hp = (nseq * dm.n_kv_heads >= 128 && G <= kAttnQT && rps * G <= kAttnQT) ? G : 1;  // as attn_groups
+    int rows_per_tile = kAttnQT / a.hp;
+    a.nrt = (rps + rows_per_tile - 1) / rows_per_tile;
+    a.ngrp = nseq * dm.n_kv_heads * a.nrt;
+    a.scale = 1.0f / sqrtf((float)m.hd);
+    int members = G / a.hp;
+    a.nsplit = attn_nsplit(e.cap);
+    a.part = e.ws.attn_part;
+    int nblk = (a.ngrp + kXcds - 1) / kXcds * kXcds * members * a.nsplit;
+    int nmerge = (int)(((size_t)rows * dm.n_heads * m.hd + 255) / 256);
+    prof_begin(&e, kProfAttn, 0.0);
+    switch (m.hd) {
+        case 32:
+            k_attn<32><<<nblk, kAttnT, attn_lds(32), s>>>(a);
+            k_attn_merge<32><<<nmerge, 256, 0, s>>>(a.part, a.row_pos, a.out, rows, dm.n_heads, a.nsplit);
+            break;
+        case 64:
+            k_attn<64><<<nblk, kAttnT, attn_lds(64), s>>>(a);
+            k_attn_merge<64><<<nmerge, 256, 0, s>>>(a.part, a.row_pos, a.out, rows, dm.n_heads, a.nsplit);
+            break;
+        case 128:
+            k_attn<128><<<nblk, kAttnT, attn_lds(128), s>>>(a);
+            k_attn_merge<128><<<nmerge, 256, 0, s>>>(a.part, a.row_pos, a.out, rows, dm.n_heads, a.nsplit);
+            break;
+        default: e.bad_launch = true; break;
+    }
+    prof_end(&e);
+}
+
+int attn_nsplit(int cap) { return (cap + kSplit - 1) / kSplit; }
+
+}  // namespace sd2

@@ -24,6 +24,7 @@ struct ModelDev {
     float* rope_cos;                  // [cap][hd/2]
     float* rope_sin;
     float* x;                         // residual stream [maxm][d]
+    float* ss;                        // [maxm][d/16] sums of squares of 16-column slices of x
 };
 
 enum WIdx { kAttnNorm = 0, kWq, kWk, kWv, kWo, kFfnNorm, kWg, kWu, kWd };
@@ -46,6 +47,7 @@ struct Workspace {
     int32_t* hist;          // [max_batch][cap]
     float* steer;           // [max_batch][d_D]
     float* hcap;            // [max_batch][d_V] verifier residual captured at prefill
+    float* hcap_ss;         // [max_batch][d_V/16] its slice sums of squares
     // row plans
     int32_t* row_pos;       // [maxm]
     int32_t* row_seq;       // [maxm]
@@ -71,6 +73,18 @@ struct Workspace {
     int32_t* own_y;
     int32_t* forced;        // [max_batch][k+2]
     int32_t* forced_on;     // [1]
+    // split-K partial tiles of the projection kernel; attention partials per position span
+    float* ws_part;
+    float* attn_part;
+};
+
+// Per-launch timing entries (HIP events recorded on the engine's stream).
+enum ProfClass { kProfGemv = 1, kProfAttn = 2, kProfSampler = 3, kProfOther = 4 };
+constexpr int kProfMax = 4096;
+struct ProfEntry {
+    int cls;
+    double bytes;
+    hipEvent_t a, b;
 };
 
 struct Engine {
@@ -89,7 +103,15 @@ struct Engine {
     int graph_batch;
     int32_t* graph_out_tokens;
     int32_t* graph_out_counts;
+    bool bad_launch;  // a projection shape had no kernel instance (reported as SD2_ERR_UNSUPPORTED)
+    bool prof_on;
+    int prof_n;
+    ProfEntry* prof;
 };
+
+// Bracket one launch with timing events when profiling is enabled (no-op otherwise).
+void prof_begin(Engine* e, int cls, double bytes);
+void prof_end(Engine* e);
 
 size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm);
 
@@ -99,11 +121,46 @@ void launch_init_maps(hipStream_t s, Engine& e);
 enum PlanKind { kPlanDraft1 = 0, kPlanDraftJ = 1, kPlanVerify = 2, kPlanPrefill = 3 };
 void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
                        const int32_t* prompt_len, int max_prompt, int chunk);
-void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows);
-enum Epi { kEpiStore = 0, kEpiAdd = 1, kEpiSwiglu = 2 };
-void launch_gemv(hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K, const void* gamma,
-                 float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y, int ldy,
-                 const int32_t* out_map);
+void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps);
+// Final-norm LM head of `rows` residual rows into Y[out_map[r]] (bf16 path via the projection kernel).
+void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map);
+void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows);
+enum Epi { kEpiStore = 0, kEpiAdd = 1, kEpiSwiglu = 2, kEpiQkv = 3 };
+
+// One bf16 weight-streaming projection (see wsgemv.hip).
+struct WsCall {
+    const float* X;
+    const int32_t* in_map;
+    int M, K;
+    const void* gamma;  // RMSNorm gain (bf16) or null
+    float eps;
+    const float* ss;    // [rows][nss] slice sums of squares of the X rows (norm input)
+    int nss;
+    const void* W[3];
+    int seg_rows[3];
+    int nseg, mode;
+    float* Y;
+    int ldy;
+    const int32_t* out_map;
+    float* ss_out;
+    float* part;
+    int H, Hkv, hd;
+    const int32_t *row_pos, *row_seq;
+    const float *rcos, *rsin;
+    float *qout, *kc, *vc;
+    int cap, max_batch, layer;
+};
+struct WsPlan {
+    int KR, S, tiles, NW, steps, Gt;
+    size_t lds;
+};
+WsPlan ws_plan(int M, int N, int K, int mode);
+void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c);
+void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride);
+int attn_nsplit(int cap);
+void launch_gemv(Engine* e, hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K,
+                 const void* gamma, float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y,
+                 int ldy, const int32_t* out_map);
 void launch_draft_pick(hipStream_t s, Engine& e, int j);
 void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t* out_counts);
 void launch_prefill_capture(hipStream_t s, Engine& e, int rows, const int32_t* prompt_len, int max_prompt);

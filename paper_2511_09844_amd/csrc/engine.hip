@@ -35,7 +35,7 @@ bool dims_ok(const sd2_dims& d) {
         return false;
     if (d.d_model % d.n_heads || d.n_heads % d.n_kv_heads) return false;
     int hd = d.d_model / d.n_heads;
-    if (hd % 2 || hd > 128 || hd % 4) return false;
+    if (hd != 32 && hd != 64 && hd != 128) return false;
     if (d.d_model % 64 || (d.n_heads * hd) % 64 || d.d_ff % 64) return false;
     // every GEMV input row must fit the 64 KiB of LDS a workgroup stages it in
     if (d.d_model > 16384 || d.d_ff > 16384) return false;
@@ -43,9 +43,18 @@ bool dims_ok(const sd2_dims& d) {
     return true;
 }
 
+bool bf16_dims_ok(const sd2_dims& d) {
+    // the bf16 projection kernel splits K into multiples of 256 and N into 16-row tiles;
+    // attention kernels exist for head dims 32, 64 and 128
+    int hd = d.d_model / d.n_heads;
+    return d.d_model % 256 == 0 && (d.n_heads * hd) % 256 == 0 && d.d_ff % 256 == 0 && d.vocab % 16 == 0 &&
+           (hd == 32 || hd == 64 || hd == 128);
+}
+
 bool config_ok(const sd2_config* c) {
     if (!c) return false;
     if (!dims_ok(c->verifier) || !dims_ok(c->drafter)) return false;
+    if (c->dtype == SD2_BF16 && (!bf16_dims_ok(c->verifier) || !bf16_dims_ok(c->drafter))) return false;
     if (c->verifier.vocab != c->drafter.vocab) return false;
     if (c->dtype != SD2_F32 && c->dtype != SD2_BF16) return false;
     if (c->k < 1 || c->k > kMaxK) return false;
@@ -91,6 +100,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
     w.hist = cv.take<int32_t>((size_t)B * cap);
     w.steer = cv.take<float>((size_t)B * c.drafter.d_model);
     w.hcap = cv.take<float>((size_t)B * c.verifier.d_model);
+    w.hcap_ss = cv.take<float>((size_t)B * (c.verifier.d_model / 16));
     w.row_pos = cv.take<int32_t>(maxm);
     w.row_seq = cv.take<int32_t>(maxm);
     w.lm_map_d = cv.take<int32_t>((size_t)k * 2 * B);
@@ -116,6 +126,38 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
     w.own_y = cv.take<int32_t>(B);
     w.forced = cv.take<int32_t>((size_t)B * (k + 2));
     w.forced_on = cv.take<int32_t>(1);
+    // projection split-K partials: the largest tiles*S*256*subs over every projection shape
+    {
+        size_t pmax = 0;
+        const sd2_dims* dd[2] = {&c.verifier, &c.drafter};
+        int mmax = std::min(maxm, 16);
+        for (int i = 0; i < 2; ++i) {
+            const sd2_dims& d = *dd[i];
+            int hd = d.d_model / d.n_heads;
+            int shapes[6][3] = {{(d.n_heads + 2 * d.n_kv_heads) * hd, d.d_model, kEpiQkv},
+                                {d.d_model, d.n_heads * hd, kEpiAdd},
+                                {d.d_ff, d.d_model, kEpiSwiglu},
+                                {d.d_model, d.d_ff, kEpiAdd},
+                                {d.vocab, d.d_model, kEpiStore},
+                                {c.drafter.d_model, c.verifier.d_model, kEpiStore}};
+            for (int mm = 1; mm <= mmax; ++mm)
+                for (auto& sh : shapes) {
+                    WsPlan p = ws_plan(mm, sh[0], sh[1], sh[2]);
+                    size_t subs = sh[2] == kEpiSwiglu ? 2 : 1;
+                    if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256 * subs);
+                }
+        }
+        w.ws_part = cv.take<float>(std::max<size_t>(pmax, 1));
+    }
+    {
+        size_t amax = 0;
+        const sd2_dims* dd[2] = {&c.verifier, &c.drafter};
+        for (int i = 0; i < 2; ++i) {
+            int hd = dd[i]->d_model / dd[i]->n_heads;
+            amax = std::max(amax, (size_t)maxm * dd[i]->n_heads * attn_nsplit(cap) * (hd + 2));
+        }
+        w.attn_part = cv.take<float>(amax);
+    }
     for (int i = 0; i < 2; ++i) {
         ModelDev* m = ms[i];
         const sd2_dims& d = m->dm;
@@ -125,9 +167,31 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         m->rope_cos = cv.take<float>((size_t)cap * (m->hd / 2));
         m->rope_sin = cv.take<float>((size_t)cap * (m->hd / 2));
         m->x = cv.take<float>((size_t)maxm * d.d_model);
+        m->ss = cv.take<float>((size_t)maxm * (d.d_model / 16));
     }
     if (ws) *ws = w;
     return align_up(cv.off);
+}
+
+}  // namespace sd2
+
+namespace sd2 {
+
+void prof_begin(Engine* e, int cls, double bytes) {
+    if (!e || !e->prof_on || e->prof_n >= kProfMax) return;
+    ProfEntry& p = e->prof[e->prof_n];
+    if (!p.a) return;
+    p.cls = cls;
+    p.bytes = bytes;
+    (void)hipEventRecord(p.a, e->stream);
+}
+
+void prof_end(Engine* e) {
+    if (!e || !e->prof_on || e->prof_n >= kProfMax) return;
+    ProfEntry& p = e->prof[e->prof_n];
+    if (!p.a) return;
+    (void)hipEventRecord(p.b, e->stream);
+    ++e->prof_n;
 }
 
 }  // namespace sd2
@@ -140,42 +204,33 @@ sd2_status hip_fail(Engine* e, hipError_t err, const char* where) {
 }
 
 sd2_status check_launch(Engine* e, const char* where) {
+    if (e->bad_launch) {
+        snprintf(e->err, sizeof(e->err), "%s: no projection kernel instance for a shape", where);
+        return SD2_ERR_UNSUPPORTED;
+    }
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return hip_fail(e, err, where);
     return SD2_OK;
 }
 
-void lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map) {
-    const void* ws[1] = {m.lm_head};
-    int rws[1] = {m.dm.vocab};
-    launch_gemv(e.stream, e.bf16, m.x, nullptr, rows, m.dm.d_model, m.final_norm, m.dm.rms_eps, ws, rws, 1,
-                kEpiStore, Y, m.dm.vocab, out_map);
-}
-
-void steer_gemv(Engine& e, const float* X, const int32_t* in_map, int rows) {
-    const void* ws[1] = {e.w_steer};
-    int rws[1] = {e.md.dm.d_model};
-    launch_gemv(e.stream, e.bf16, X, in_map, rows, e.mv.dm.d_model, e.mv.final_norm, e.mv.dm.rms_eps, ws, rws, 1,
-                kEpiStore, e.ws.steer, e.md.dm.d_model, nullptr);
-}
-
 // The whole round, as a fixed sequence of kernels (no host decisions).
 void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
     hipStream_t s = e.stream;
+    e.prof_n = 0;
     int B = e.batch, k = e.cfg.k;
     for (int j = 1; j <= k; ++j) {
         int rows = j == 1 ? 2 * B : B;
         launch_plan_embed(s, e, e.md, j == 1 ? kPlanDraft1 : kPlanDraftJ, j, rows, nullptr, nullptr, 0, 1);
-        for (int l = 0; l < e.md.dm.n_layers; ++l) launch_layer(s, e, e.md, l, rows);
-        lm_head(e, e.md, rows, e.ws.logits_d, e.ws.lm_map_d + (size_t)(j - 1) * 2 * e.cfg.max_batch);
+        for (int l = 0; l < e.md.dm.n_layers; ++l) launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1);
+        launch_lm_head(e, e.md, rows, e.ws.logits_d, e.ws.lm_map_d + (size_t)(j - 1) * 2 * e.cfg.max_batch);
         launch_draft_pick(s, e, j);
     }
     int rows = B * (k + 1);
     launch_plan_embed(s, e, e.mv, kPlanVerify, 0, rows, nullptr, nullptr, 0, 1);
-    for (int l = 0; l < e.mv.dm.n_layers; ++l) launch_layer(s, e, e.mv, l, rows);
-    lm_head(e, e.mv, rows, e.ws.logits_v, nullptr);
+    for (int l = 0; l < e.mv.dm.n_layers; ++l) launch_layer(s, e, e.mv, l, rows, k + 1);
+    launch_lm_head(e, e.mv, rows, e.ws.logits_v, nullptr);
     launch_verify_decide(s, e, out_tokens, out_counts);
-    steer_gemv(e, e.mv.x, e.ws.steer_map, B);
+    launch_steer(e, e.mv.x, e.mv.ss, e.ws.steer_map, B);
 }
 
 void drop_graph(Engine& e) {
@@ -307,13 +362,13 @@ sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, con
     if (err != hipSuccess) return hip_fail(e, err, "hipMemsetAsync");
     for (int c = 0; c < nchunks; ++c) {
         launch_plan_embed(s, *e, e->mv, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
-        for (int l = 0; l < e->mv.dm.n_layers; ++l) launch_layer(s, *e, e->mv, l, rows);
+        for (int l = 0; l < e->mv.dm.n_layers; ++l) launch_layer(s, *e, e->mv, l, rows, chunk);
         launch_prefill_capture(s, *e, rows, lens, max_prompt);
     }
-    steer_gemv(*e, e->ws.hcap, nullptr, batch);
+    launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, nullptr, batch);
     for (int c = 0; c < nchunks; ++c) {
         launch_plan_embed(s, *e, e->md, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
-        for (int l = 0; l < e->md.dm.n_layers; ++l) launch_layer(s, *e, e->md, l, rows);
+        for (int l = 0; l < e->md.dm.n_layers; ++l) launch_layer(s, *e, e->md, l, rows, chunk);
     }
     launch_prefill_finish(s, *e, batch, tokens, lens, max_prompt);
     sd2_status st = check_launch(e, "prefill");
@@ -349,7 +404,59 @@ sd2_status sd2_destroy(sd2_handle_t h) {
     if (!h) return SD2_OK;
     Engine* e = reinterpret_cast<Engine*>(h);
     drop_graph(*e);
+    if (e->prof) {
+        for (int i = 0; i < kProfMax; ++i) {
+            if (e->prof[i].a) (void)hipEventDestroy(e->prof[i].a);
+            if (e->prof[i].b) (void)hipEventDestroy(e->prof[i].b);
+        }
+        delete[] e->prof;
+    }
     delete e;
+    return SD2_OK;
+}
+
+sd2_status sd2_profile(sd2_handle_t h, int32_t enable) {
+    if (!h) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    if (enable && !e->prof) {
+        // all timing events are created here, outside any stream capture
+        e->prof = new (std::nothrow) ProfEntry[kProfMax]();
+        if (!e->prof) return SD2_ERR_INVALID_ARG;
+        for (int i = 0; i < kProfMax; ++i) {
+            hipError_t err = hipEventCreateWithFlags(&e->prof[i].a, hipEventDefault);
+            if (err == hipSuccess) err = hipEventCreateWithFlags(&e->prof[i].b, hipEventDefault);
+            if (err != hipSuccess) return hip_fail(e, err, "hipEventCreate");
+        }
+    }
+    if ((bool)enable != e->prof_on) {
+        drop_graph(*e);  // the next round is recorded again, with or without timing events
+        e->prof_on = enable != 0;
+        e->prof_n = 0;
+    }
+    return SD2_OK;
+}
+
+sd2_status sd2_profile_read(sd2_handle_t h, int32_t cls, int32_t* launches, double* total_ms, double* bytes) {
+    if (!h || !launches || !total_ms || !bytes) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    if (!e->prof_on) return SD2_ERR_STATE;
+    hipError_t err = hipStreamSynchronize(e->stream);
+    if (err != hipSuccess) return hip_fail(e, err, "hipStreamSynchronize");
+    int n = 0;
+    double ms = 0.0, by = 0.0;
+    for (int i = 0; i < e->prof_n; ++i) {
+        const ProfEntry& p = e->prof[i];
+        if (p.cls != cls) continue;
+        float t = 0.f;
+        err = hipEventElapsedTime(&t, p.a, p.b);
+        if (err != hipSuccess) return hip_fail(e, err, "hipEventElapsedTime");
+        ++n;
+        ms += t;
+        by += p.bytes;
+    }
+    *launches = n;
+    *total_ms = ms;
+    *bytes = by;
     return SD2_OK;
 }
 

@@ -56,6 +56,7 @@ struct PlanArgs {
     int add_steer;
     int32_t *row_pos, *row_seq;
     float* x;
+    float* ss;   // [rows][d/16]
     const void* embed;
 };
 
@@ -107,13 +108,20 @@ __global__ __launch_bounds__(256) void k_plan_embed(PlanArgs a) {
     float* xr = a.x + (size_t)r * a.d;
     const TW* er = (const TW*)a.embed + (size_t)tok * a.d;
     const float* sr = a.steer + (size_t)b * a.d;
-    for (int i = threadIdx.x; i < a.d; i += blockDim.x) {
-        float v = 0.0f;
-        if (active) {
-            v = load_scalar<TW>(er, i);
-            if (a.add_steer) v += sr[i];
+    const int nsl = a.d / 16;
+    for (int sl = threadIdx.x; sl < nsl; sl += blockDim.x) {
+        float acc = 0.0f;
+        for (int c = 0; c < 16; ++c) {
+            int i = sl * 16 + c;
+            float v = 0.0f;
+            if (active) {
+                v = load_scalar<TW>(er, i);
+                if (a.add_steer) v += sr[i];
+            }
+            xr[i] = v;
+            acc += v * v;
         }
-        xr[i] = v;
+        a.ss[(size_t)r * nsl + sl] = acc;
     }
 }
 
@@ -126,9 +134,11 @@ void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, i
     a.prompt_tok = prompt_tok; a.prompt_len = prompt_len;
     a.steer = e.ws.steer;
     a.add_steer = (&m == &e.md) && (kind == kPlanDraft1 || kind == kPlanDraftJ);
-    a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq; a.x = m.x; a.embed = m.embed;
+    a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq; a.x = m.x; a.ss = m.ss; a.embed = m.embed;
+    prof_begin(&e, kProfOther, 0.0);
     if (e.bf16) k_plan_embed<uint16_t><<<rows, 256, 0, s>>>(a);
     else k_plan_embed<float><<<rows, 256, 0, s>>>(a);
+    prof_end(&e);
 }
 
 // ===========================================================================
@@ -210,39 +220,49 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_vec(GemvArgs a) {
     __syncthreads();
 
     constexpr int VN = Vec16<TW>::N;
-    const int nsub = a.epi == kEpiSwiglu ? 2 : 1;
     for (int rr = 0; rr < kGemvRowsPerWave; ++rr) {
         const int n = blockIdx.x * kGemvRowsPerBlock + wave * kGemvRowsPerWave + rr;
         if (n >= a.N) break;
-        float acc[2][MT];
+        float acc0[MT], acc1[MT];
 #pragma unroll
-        for (int m = 0; m < MT; ++m) { acc[0][m] = 0.0f; acc[1][m] = 0.0f; }
-        for (int sub = 0; sub < nsub; ++sub) {
-            const TW* wr;
-            if (a.epi == kEpiSwiglu) {
-                wr = (const TW*)a.W[sub] + (size_t)n * K;
-            } else {
-                int sgi = 0;
-                while (sgi + 1 < a.nseg && n >= a.seg_off[sgi + 1]) ++sgi;
-                wr = (const TW*)a.W[sgi] + (size_t)(n - a.seg_off[sgi]) * K;
+        for (int m = 0; m < MT; ++m) { acc0[m] = 0.0f; acc1[m] = 0.0f; }
+        const TW* wr0;
+        const TW* wr1 = nullptr;
+        if (a.epi == kEpiSwiglu) {
+            wr0 = (const TW*)a.W[0] + (size_t)n * K;
+            wr1 = (const TW*)a.W[1] + (size_t)n * K;
+        } else {
+            int sgi = 0;
+            while (sgi + 1 < a.nseg && n >= a.seg_off[sgi + 1]) ++sgi;
+            wr0 = (const TW*)a.W[sgi] + (size_t)(n - a.seg_off[sgi]) * K;
+        }
+        for (int k = lane * VN; k < K; k += kWave * VN) {
+            float w[VN];
+            Vec16<TW>::load(wr0 + k, w);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const float* xv = xs + (size_t)m * K + k;
+                float sacc = 0.0f;
+#pragma unroll
+                for (int e2 = 0; e2 < VN; ++e2) sacc += w[e2] * xv[e2];
+                acc0[m] += sacc;
             }
-            for (int k = lane * VN; k < K; k += kWave * VN) {
-                float w[VN];
-                Vec16<TW>::load(wr + k, w);
+            if (wr1) {
+                Vec16<TW>::load(wr1 + k, w);
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const float* xv = xs + (size_t)m * K + k;
-                    float s = 0.0f;
+                    float sacc = 0.0f;
 #pragma unroll
-                    for (int e2 = 0; e2 < VN; ++e2) s += w[e2] * xv[e2];
-                    acc[sub][m] += s;
+                    for (int e2 = 0; e2 < VN; ++e2) sacc += w[e2] * xv[e2];
+                    acc1[m] += sacc;
                 }
             }
         }
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
-            acc[0][m] = wave_sum(acc[0][m]);
-            if (nsub == 2) acc[1][m] = wave_sum(acc[1][m]);
+            acc0[m] = wave_sum(acc0[m]);
+            if (wr1) acc1[m] = wave_sum(acc1[m]);
         }
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
@@ -250,18 +270,18 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_vec(GemvArgs a) {
                 int orow = a.out_map ? a.out_map[m0 + m] : m0 + m;
                 if (orow >= 0) {
                     float* yp = a.Y + (size_t)orow * a.ldy + n;
-                    if (a.epi == kEpiStore) *yp = acc[0][m];
-                    else if (a.epi == kEpiAdd) *yp += acc[0][m];
-                    else *yp = silu(acc[0][m]) * acc[1][m];
+                    if (a.epi == kEpiStore) *yp = acc0[m];
+                    else if (a.epi == kEpiAdd) *yp += acc0[m];
+                    else *yp = silu(acc0[m]) * acc1[m];
                 }
             }
         }
     }
 }
 
-void launch_gemv(hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K, const void* gamma,
-                 float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y, int ldy,
-                 const int32_t* out_map) {
+void launch_gemv(Engine* e, hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K,
+                 const void* gamma, float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y,
+                 int ldy, const int32_t* out_map) {
     GemvArgs a;
     a.X = X; a.in_map = in_map; a.M = M; a.K = K; a.gamma = gamma; a.eps = eps;
     int off = 0;
@@ -279,6 +299,10 @@ void launch_gemv(hipStream_t s, bool bf16, const float* X, const int32_t* in_map
     while (mt > 1 && (mt / 2 >= M || (size_t)mt * K * 4 > 65536)) mt >>= 1;
     dim3 grid((a.N + kGemvRowsPerBlock - 1) / kGemvRowsPerBlock, (M + mt - 1) / mt);
     size_t sh = (size_t)mt * K * 4;
+    // algorithmic bytes: every weight once, the input rows once, the output rows once
+    double wrows = (double)(epi == kEpiSwiglu ? 2 * a.N : a.N);
+    double nout = (double)a.N;
+    prof_begin(e, kProfGemv, wrows * K * (bf16 ? 2.0 : 4.0) + (double)M * K * 4.0 + (double)M * nout * 4.0);
 #define SD2_GEMV_CASE(MTV)                                                                  \
     case MTV:                                                                               \
         if (bf16) k_gemv_vec<uint16_t, MTV><<<grid, kGemvThreads, sh, s>>>(a);             \
@@ -291,6 +315,7 @@ void launch_gemv(hipStream_t s, bool bf16, const float* X, const int32_t* in_map
         SD2_GEMV_CASE(8)
     }
 #undef SD2_GEMV_CASE
+    prof_end(e);
 }
 
 // ===========================================================================
@@ -338,88 +363,55 @@ __global__ __launch_bounds__(128) void k_rope_append(RopeArgs a) {
 }
 
 // ===========================================================================
-// Attention: one block per (row, query head); causal over cache positions 0..pos.
-// ===========================================================================
-struct AttnArgs {
-    const float* qkv;
-    int qkv_dim, H, Hkv, hd, cap, max_batch, layer;
-    const int32_t *row_pos, *row_seq;
-    const float *kc, *vc;
-    float* out;
-    float scale;
-};
-
-constexpr int kAttnThreads = 128;
-
-__global__ __launch_bounds__(kAttnThreads) void k_attention(AttnArgs a) {
-    extern __shared__ float sc[];  // [cap]
-    __shared__ float qs[128];
-    __shared__ float red[kAttnThreads / kWave];
-    int r = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
-    int lane = tid & (kWave - 1), wave = tid / kWave;
-    float* o = a.out + (size_t)r * a.H * a.hd + h * a.hd;
-    int pos = a.row_pos[r];
-    if (pos < 0) {
-        for (int i = tid; i < a.hd; i += kAttnThreads) o[i] = 0.0f;
-        return;
-    }
-    int b = a.row_seq[r];
-    int g = h / (a.H / a.Hkv);
-    const float* q = a.qkv + (size_t)r * a.qkv_dim + h * a.hd;
-    for (int i = tid; i < a.hd; i += kAttnThreads) qs[i] = q[i];
-    __syncthreads();
-    size_t base = (((size_t)a.layer * a.max_batch + b) * a.Hkv + g) * a.cap * a.hd;
-    const float* K = a.kc + base;
-    const float* Vv = a.vc + base;
-    float mx = -INFINITY;
-    for (int j = tid; j <= pos; j += kAttnThreads) {
-        const float* kj = K + (size_t)j * a.hd;
-        float d = 0.0f;
-        for (int i = 0; i < a.hd; i += 4) {
-            float4 kv = *(const float4*)(kj + i);
-            d += qs[i] * kv.x + qs[i + 1] * kv.y + qs[i + 2] * kv.z + qs[i + 3] * kv.w;
-        }
-        d *= a.scale;
-        sc[j] = d;
-        mx = fmaxf(mx, d);
-    }
-    mx = wave_max(mx);
-    if (lane == 0) red[wave] = mx;
-    __syncthreads();
-    mx = red[0];
-    for (int w = 1; w < kAttnThreads / kWave; ++w) mx = fmaxf(mx, red[w]);
-    __syncthreads();
-    float sum = 0.0f;
-    for (int j = tid; j <= pos; j += kAttnThreads) {
-        float e = expf(sc[j] - mx);
-        sc[j] = e;
-        sum += e;
-    }
-    sum = wave_sum(sum);
-    if (lane == 0) red[wave] = sum;
-    __syncthreads();
-    float tot = 0.0f;
-    for (int w = 0; w < kAttnThreads / kWave; ++w) tot += red[w];
-    float inv = 1.0f / tot;
-    for (int i = tid; i < a.hd; i += kAttnThreads) {
-        float acc = 0.0f;
-        for (int j = 0; j <= pos; ++j) acc += sc[j] * Vv[(size_t)j * a.hd + i];
-        o[i] = acc * inv;
-    }
-}
-
-// ===========================================================================
 // One decoder layer on `rows` planned rows.
 // ===========================================================================
-void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows) {
+static WsCall ws_base(Engine& e, ModelDev& m) {
+    WsCall c{};
+    c.part = e.ws.ws_part;
+    c.eps = m.dm.rms_eps;
+    c.nss = m.dm.d_model / 16;
+    return c;
+}
+
+void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps) {
     const sd2_dims& dm = m.dm;
     const void* const* W = m.layer + (size_t)layer * 9;
     int hd = m.hd, H = dm.n_heads, Hkv = dm.n_kv_heads;
-    // QKV with the attention RMSNorm as prologue
+    if (e.bf16) {
+        // Q|K|V with the attention RMSNorm as prologue, RoPE and the cache append as epilogue
+        WsCall c = ws_base(e, m);
+        c.X = m.x; c.M = rows; c.K = dm.d_model; c.gamma = W[kAttnNorm]; c.ss = m.ss;
+        c.W[0] = W[kWq]; c.W[1] = W[kWk]; c.W[2] = W[kWv];
+        c.seg_rows[0] = H * hd; c.seg_rows[1] = Hkv * hd; c.seg_rows[2] = Hkv * hd;
+        c.nseg = 3; c.mode = kEpiQkv;
+        c.H = H; c.Hkv = Hkv; c.hd = hd; c.row_pos = e.ws.row_pos; c.row_seq = e.ws.row_seq;
+        c.rcos = m.rope_cos; c.rsin = m.rope_sin; c.qout = e.ws.qkv; c.kc = m.kc; c.vc = m.vc;
+        c.cap = e.cap; c.max_batch = e.cfg.max_batch; c.layer = layer;
+        launch_wsgemv(&e, s, c);
+        launch_attn(e, s, m, layer, rows, rps, e.ws.qkv, H * hd);
+        // O projection + residual (+ slice sums of squares for the FFN norm)
+        WsCall o = ws_base(e, m);
+        o.X = e.ws.attn; o.M = rows; o.K = H * hd; o.W[0] = W[kWo]; o.seg_rows[0] = dm.d_model; o.nseg = 1;
+        o.mode = kEpiAdd; o.Y = m.x; o.ldy = dm.d_model; o.ss_out = m.ss;
+        launch_wsgemv(&e, s, o);
+        // gate|up with the FFN RMSNorm prologue and SwiGLU epilogue
+        WsCall g = ws_base(e, m);
+        g.X = m.x; g.M = rows; g.K = dm.d_model; g.gamma = W[kFfnNorm]; g.ss = m.ss;
+        g.W[0] = W[kWg]; g.W[1] = W[kWu]; g.seg_rows[0] = dm.d_ff; g.seg_rows[1] = dm.d_ff; g.nseg = 2;
+        g.mode = kEpiSwiglu; g.Y = e.ws.ffh; g.ldy = dm.d_ff;
+        launch_wsgemv(&e, s, g);
+        // down projection + residual
+        WsCall d = ws_base(e, m);
+        d.X = e.ws.ffh; d.M = rows; d.K = dm.d_ff; d.W[0] = W[kWd]; d.seg_rows[0] = dm.d_model; d.nseg = 1;
+        d.mode = kEpiAdd; d.Y = m.x; d.ldy = dm.d_model; d.ss_out = m.ss;
+        launch_wsgemv(&e, s, d);
+        return;
+    }
+    // fp32 weights: vector projections, separate RoPE/append
     {
         const void* ws[3] = {W[kWq], W[kWk], W[kWv]};
         int rws[3] = {H * hd, Hkv * hd, Hkv * hd};
-        launch_gemv(s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kAttnNorm], dm.rms_eps, ws, rws, 3, kEpiStore,
+        launch_gemv(&e, s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kAttnNorm], dm.rms_eps, ws, rws, 3, kEpiStore,
                     e.ws.qkv, m.qkv_dim, nullptr);
     }
     {
@@ -427,33 +419,59 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows) {
         a.qkv = e.ws.qkv; a.qkv_dim = m.qkv_dim; a.H = H; a.Hkv = Hkv; a.hd = hd; a.cap = e.cap;
         a.max_batch = e.cfg.max_batch; a.layer = layer; a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq;
         a.cosv = m.rope_cos; a.sinv = m.rope_sin; a.kc = m.kc; a.vc = m.vc;
+        prof_begin(&e, kProfOther, 0.0);
         k_rope_append<<<rows, 128, 0, s>>>(a);
+        prof_end(&e);
     }
-    {
-        AttnArgs a;
-        a.qkv = e.ws.qkv; a.qkv_dim = m.qkv_dim; a.H = H; a.Hkv = Hkv; a.hd = hd; a.cap = e.cap;
-        a.max_batch = e.cfg.max_batch; a.layer = layer; a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq;
-        a.kc = m.kc; a.vc = m.vc; a.out = e.ws.attn; a.scale = 1.0f / sqrtf((float)hd);
-        k_attention<<<dim3(rows, H), kAttnThreads, (size_t)e.cap * 4, s>>>(a);
-    }
+    launch_attn(e, s, m, layer, rows, rps, e.ws.qkv, m.qkv_dim);
     {
         const void* ws[1] = {W[kWo]};
         int rws[1] = {dm.d_model};
-        launch_gemv(s, e.bf16, e.ws.attn, nullptr, rows, H * hd, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x,
+        launch_gemv(&e, s, e.bf16, e.ws.attn, nullptr, rows, H * hd, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x,
                     dm.d_model, nullptr);
     }
     {
         const void* ws[2] = {W[kWg], W[kWu]};
         int rws[2] = {dm.d_ff, dm.d_ff};
-        launch_gemv(s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kFfnNorm], dm.rms_eps, ws, rws, 2, kEpiSwiglu,
+        launch_gemv(&e, s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kFfnNorm], dm.rms_eps, ws, rws, 2, kEpiSwiglu,
                     e.ws.ffh, dm.d_ff, nullptr);
     }
     {
         const void* ws[1] = {W[kWd]};
         int rws[1] = {dm.d_model};
-        launch_gemv(s, e.bf16, e.ws.ffh, nullptr, rows, dm.d_ff, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x, dm.d_model,
-                    nullptr);
+        launch_gemv(&e, s, e.bf16, e.ws.ffh, nullptr, rows, dm.d_ff, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x,
+                    dm.d_model, nullptr);
     }
+}
+
+void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map) {
+    if (e.bf16) {
+        WsCall c = ws_base(e, m);
+        c.X = m.x; c.M = rows; c.K = m.dm.d_model; c.gamma = m.final_norm; c.ss = m.ss;
+        c.W[0] = m.lm_head; c.seg_rows[0] = m.dm.vocab; c.nseg = 1; c.mode = kEpiStore;
+        c.Y = Y; c.ldy = m.dm.vocab; c.out_map = out_map;
+        launch_wsgemv(&e, e.stream, c);
+        return;
+    }
+    const void* ws[1] = {m.lm_head};
+    int rws[1] = {m.dm.vocab};
+    launch_gemv(&e, e.stream, e.bf16, m.x, nullptr, rows, m.dm.d_model, m.final_norm, m.dm.rms_eps, ws, rws, 1,
+                kEpiStore, Y, m.dm.vocab, out_map);
+}
+
+void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows) {
+    if (e.bf16) {
+        WsCall c = ws_base(e, e.mv);
+        c.X = X; c.in_map = in_map; c.M = rows; c.K = e.mv.dm.d_model; c.gamma = e.mv.final_norm; c.ss = ss;
+        c.W[0] = e.w_steer; c.seg_rows[0] = e.md.dm.d_model; c.nseg = 1; c.mode = kEpiStore;
+        c.Y = e.ws.steer; c.ldy = e.md.dm.d_model;
+        launch_wsgemv(&e, e.stream, c);
+        return;
+    }
+    const void* ws[1] = {e.w_steer};
+    int rws[1] = {e.md.dm.d_model};
+    launch_gemv(&e, e.stream, e.bf16, X, in_map, rows, e.mv.dm.d_model, e.mv.final_norm, e.mv.dm.rms_eps, ws, rws,
+                1, kEpiStore, e.ws.steer, e.md.dm.d_model, nullptr);
 }
 
 // ===========================================================================
@@ -727,8 +745,10 @@ static SampArgs samp_args(Engine& e) {
 void launch_draft_pick(hipStream_t s, Engine& e, int j) {
     SampArgs a = samp_args(e);
     a.j = j;
+    prof_begin(&e, kProfSampler, 0.0);
     k_pick_partial<<<dim3(kVocabChunks, e.batch), 256, 0, s>>>(a);
     k_pick_final<<<e.batch, 64, 0, s>>>(a);
+    prof_end(&e);
 }
 
 void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t* out_counts) {
@@ -736,10 +756,12 @@ void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t
     a.out_tokens = out_tokens;
     a.out_counts = out_counts;
     int per = 2 * e.cfg.k + 1;
+    prof_begin(&e, kProfSampler, 0.0);
     k_row_partial<<<dim3(kVocabChunks, e.batch * per), 256, 0, s>>>(a);
     k_accept<<<e.batch, 64, 0, s>>>(a);
     if (e.cfg.temperature > 0.0f) k_final_partial<<<dim3(kVocabChunks, e.batch), 256, 0, s>>>(a);
     k_commit<<<e.batch, 64, 0, s>>>(a);
+    prof_end(&e);
 }
 
 // ===========================================================================
@@ -747,18 +769,20 @@ void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t
 // ===========================================================================
 // Keep the verifier residual of the row at position len-2 (the steering tap of the first round).
 __global__ void k_prefill_capture(const int32_t* row_pos, const int32_t* row_seq, const int32_t* prompt_len,
-                                  int max_prompt, const float* x, float* hcap, int d, int batch) {
+                                  int max_prompt, const float* x, const float* ss, float* hcap, float* hcap_ss,
+                                  int d, int batch) {
     int r = blockIdx.x;
     int pos = row_pos[r];
     if (pos < 0) return;
     int b = row_seq[r];
     if (b >= batch || pos != min(prompt_len[b], max_prompt) - 2) return;
     for (int i = threadIdx.x; i < d; i += blockDim.x) hcap[(size_t)b * d + i] = x[(size_t)r * d + i];
+    for (int i = threadIdx.x; i < d / 16; i += blockDim.x) hcap_ss[(size_t)b * (d / 16) + i] = ss[(size_t)r * (d / 16) + i];
 }
 
 void launch_prefill_capture(hipStream_t s, Engine& e, int rows, const int32_t* prompt_len, int max_prompt) {
-    k_prefill_capture<<<rows, 256, 0, s>>>(e.ws.row_pos, e.ws.row_seq, prompt_len, max_prompt, e.mv.x, e.ws.hcap,
-                                           e.mv.dm.d_model, e.batch);
+    k_prefill_capture<<<rows, 256, 0, s>>>(e.ws.row_pos, e.ws.row_seq, prompt_len, max_prompt, e.mv.x, e.mv.ss,
+                                           e.ws.hcap, e.ws.hcap_ss, e.mv.dm.d_model, e.batch);
 }
 
 __global__ void k_prefill_finish(int batch, const int32_t* prompt_tok, const int32_t* prompt_len, int max_prompt,

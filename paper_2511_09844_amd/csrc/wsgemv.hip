@@ -1,0 +1,404 @@
+// Weight-streaming projection for bf16 weights and up to 16 activation rows per launch.
+//
+//   Y[m][n] (op)= sum_k W[n][k] * xn[m][k],   xn = x (optionally RMS-normalised and scaled by gamma)
+//
+// Workgroups are persistent: each stages the activation slice xn[:, k0:k0+KR) in LDS once,
+// as a bf16 hi/lo pair (xn ~= hi + lo to ~16 significant bits), then walks a strided list of
+// 16-row weight tiles.  Its NW waves split the K-range; every lane streams 16-byte fragments
+// so that the four lanes sharing a weight row read one contiguous 128-byte segment, and the
+// next tile's fragments are requested before the current tile is multiplied, so HBM traffic
+// never waits on the MFMA/LDS work.  The contraction runs on v_mfma_f32_16x16x32_bf16 twice
+// per fragment (hi and lo), i.e. fp32 activations against bf16 weights.  The NW partial tiles
+// are summed in LDS.  Weights are read exactly once.
+//
+// When the activation slice of the whole K does not fit in LDS, K is cut into S ranges; each
+// range writes a partial tile and a separate reduction kernel adds the S partials in order and
+// applies the epilogue (a kernel boundary makes the partials visible: on this part an in-kernel
+// device-scope release fence writes back the whole L2 and costs far more than a launch).
+//
+// Epilogues: plain store (optional output-row map), residual add (+ per-16-column sums of
+// squares of the new residual, consumed by the next RMSNorm), SwiGLU on paired gate/up
+// tiles, and Q|K|V with rotate-half RoPE and the append of K and V to the cache.
+#include "device_common.h"
+#include "engine.h"
+
+namespace sd2 {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+struct WsArgs {
+    const float* X;
+    int ldx;
+    const int32_t* in_map;
+    int M;     // rows in this launch (<= 16)
+    int row0;  // first row (of X / Y / row plans) handled by this launch
+    int K;
+    const uint16_t* gamma;
+    float eps;
+    const float* ss;  // [rows][nss] partial sums of squares of X rows (norm input)
+    int nss;
+    const uint16_t* W[3];
+    int seg_tiles[3];
+    int nseg;
+    int mode;
+    int tiles;
+    float* Y;
+    int ldy;
+    const int32_t* out_map;
+    float* ss_out;
+    int KR, S, Gt;  // K-range per workgroup, number of K ranges, workgroups per K range
+    float* part;    // S > 1: [tiles][S][SUBS][256]
+    // Q|K|V mode
+    int H, Hkv, hd;
+    const int32_t *row_pos, *row_seq;
+    const float *rcos, *rsin;
+    float *qout, *kc, *vc;
+    int cap, max_batch, layer;
+};
+
+// Weight row streamed by lane column n of a tile (segment resolution and the Q|K|V pairing
+// of rotate-half partners i and i + hd/2 inside one tile).
+__device__ __forceinline__ const uint16_t* tile_row(const WsArgs& a, int tile, int sub, int n) {
+    if (a.mode == kEpiSwiglu) return a.W[sub] + (size_t)(tile * 16 + n) * a.K;
+    int seg = 0, lt = tile;
+    while (seg + 1 < a.nseg && lt >= a.seg_tiles[seg]) { lt -= a.seg_tiles[seg]; ++seg; }
+    int wrow;
+    if (a.mode == kEpiQkv) {
+        int per_head = a.hd / 16;
+        int h = lt / per_head, j = lt % per_head;
+        wrow = h * a.hd + (n < 8 ? 8 * j + n : a.hd / 2 + 8 * j + (n - 8));
+    } else {
+        wrow = lt * 16 + n;
+    }
+    return a.W[seg] + (size_t)wrow * a.K;
+}
+
+// Epilogue of one finished 16x16 tile; element (m, c) is held by thread t = 16m + c of the
+// first 256 threads.  `v` holds the value per sub-tile.
+template <int SUBS>
+__device__ __forceinline__ void tile_epilogue(const WsArgs& a, int tile, const float* v) {
+    const int tid = threadIdx.x;
+    const int em = tid >> 4, ec = tid & 15;
+    const bool valid = em < a.M;
+    const int row = a.row0 + em;
+    if (a.mode == kEpiStore) {
+        if (valid) {
+            int orow = a.out_map ? a.out_map[row] : row;
+            if (orow >= 0) a.Y[(size_t)orow * a.ldy + tile * 16 + ec] = v[0];
+        }
+    } else if (a.mode == kEpiAdd) {
+        float nv = 0.0f;
+        if (valid) {
+            float* yp = a.Y + (size_t)row * a.ldy + tile * 16 + ec;
+            nv = *yp + v[0];
+            *yp = nv;
+        }
+        float sq = nv * nv;
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 16);
+        if (valid && ec == 0) a.ss_out[(size_t)row * a.tiles + tile] = sq;
+    } else if (a.mode == kEpiSwiglu) {
+        if (valid) a.Y[(size_t)row * a.ldy + tile * 16 + ec] = silu(v[0]) * v[SUBS - 1];
+    } else {
+        float partner = __shfl_xor(v[0], 8, 16);
+        if (!valid) return;
+        int seg = 0, lt = tile;
+        while (seg + 1 < a.nseg && lt >= a.seg_tiles[seg]) { lt -= a.seg_tiles[seg]; ++seg; }
+        int per_head = a.hd / 16;
+        int h = lt / per_head, j = lt % per_head;
+        int half = a.hd / 2;
+        int i = 8 * j + (ec & 7);
+        int dim = ec < 8 ? i : half + i;
+        int pos = a.row_pos[row];
+        float out = v[0];
+        if (seg < 2) {
+            int pp = pos < 0 ? 0 : pos;
+            float c = a.rcos[(size_t)pp * half + i], sn = a.rsin[(size_t)pp * half + i];
+            out = ec < 8 ? v[0] * c - partner * sn : v[0] * c + partner * sn;
+        }
+        if (seg == 0) {
+            a.qout[(size_t)row * a.H * a.hd + h * a.hd + dim] = out;
+        } else if (pos >= 0) {
+            int b = a.row_seq[row];
+            size_t idx = ((((size_t)a.layer * a.max_batch + b) * a.Hkv + h) * a.cap + pos) * a.hd + dim;
+            if (seg == 1) a.kc[idx] = out;
+            else a.vc[idx] = out;
+        }
+    }
+}
+
+template <int NW, int STEPS, int SUBS>
+__global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ float inv_rms[16];
+    __shared__ int src_row[16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int M = a.M;
+    const int KR = a.KR;
+    const int ldk = KR + 8;  // padded row stride (bf16 elements) of the LDS slices
+    const int s = blockIdx.x % a.S;
+    const int g = blockIdx.x / a.S;
+    const int k0 = s * KR;
+    uint16_t* xh = (uint16_t*)smem;
+    uint16_t* xl = xh + (size_t)M * ldk;
+    float* red = (float*)(xl + (size_t)M * ldk);  // [NW][256]
+
+    const int n = lane & 15, q = lane >> 4;
+    const int kw0 = wave * (KR / NW);
+
+    // The workgroup's work is a sequence of sub-tiles u = 0, 1, ...: tile g + (u / SUBS) * Gt,
+    // sub-tile u % SUBS (SwiGLU: gate then up).  Fragments of sub-tile u+1 are requested
+    // before sub-tile u is multiplied; the two register buffers alternate.
+    const int ntile_mine = a.tiles > g ? (a.tiles - g + a.Gt - 1) / a.Gt : 0;
+    const int nsub_mine = ntile_mine * SUBS;
+    u32x4_t wa[STEPS][2], wb[STEPS][2];
+    auto issue = [&](u32x4_t (&buf)[STEPS][2], int u) {
+        const int tile = g + (u / SUBS) * a.Gt;
+        const uint16_t* wp = tile_row(a, tile, u % SUBS, n) + k0 + kw0 + 16 * q;
+#pragma unroll
+        for (int st = 0; st < STEPS; ++st)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                buf[st][h] = *(const u32x4_t*)(wp + st * 64 + 8 * h);
+    };
+
+    if (nsub_mine > 0) issue(wa, 0);
+
+    // ---- prologue: normalisation scale per row (one wave per row, the slice sums of squares
+    //      read in parallel), then the hi/lo activation slice with its loads batched ----
+    if (tid < 16) {
+        int src = -1;
+        if (tid < M) src = a.in_map ? a.in_map[a.row0 + tid] : a.row0 + tid;
+        src_row[tid] = src;
+        inv_rms[tid] = 1.0f;
+    }
+    __syncthreads();
+    if (a.gamma) {
+        for (int m = wave; m < M; m += NW) {
+            const int src = src_row[m];
+            float sum = 0.0f;
+            if (src >= 0) {
+                const float* sp = a.ss + (size_t)src * a.nss;
+                for (int t = lane; t < a.nss; t += 64) sum += sp[t];
+            }
+            sum = wave_sum(sum);
+            if (lane == 0) inv_rms[m] = rsqrtf(sum / (float)a.K + a.eps);
+        }
+        __syncthreads();
+    }
+    {
+        constexpr int B4 = 4;  // float4 loads in flight per thread
+        const int n4 = KR / 4;
+        const int total = M * n4;
+        for (int base = tid; base < total; base += NW * 64 * B4) {
+            float4 v[B4];
+#pragma unroll
+            for (int u = 0; u < B4; ++u) {
+                int idx = base + u * NW * 64;
+                v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (idx < total) {
+                    int m = idx / n4, kk = (idx % n4) * 4;
+                    int src = src_row[m];
+                    if (src >= 0) v[u] = *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < B4; ++u) {
+                int idx = base + u * NW * 64;
+                if (idx >= total) break;
+                int m = idx / n4, kk = (idx % n4) * 4;
+                float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+                uint16_t hi[4], lo[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float x = vv[e];
+                    if (a.gamma) x *= inv_rms[m] * bf16_to_f32(a.gamma[k0 + kk + e]);
+                    hi[e] = f32_to_bf16_rne(x);
+                    lo[e] = f32_to_bf16_rne(x - bf16_to_f32(hi[e]));
+                }
+                *(uint2*)(xh + (size_t)m * ldk + kk) =
+                    make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+                *(uint2*)(xl + (size_t)m * ldk + kk) =
+                    make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+            }
+        }
+    }
+    __syncthreads();
+
+    const bool arow = n < M;
+    float stash = 0.0f;  // gate value of the current SwiGLU tile (threads < 256)
+    auto compute = [&](u32x4_t (&buf)[STEPS][2], int u) {
+        floatx4_t acc = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < STEPS; ++st) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int kk = kw0 + st * 64 + 16 * q + 8 * h;
+                bf16x8_t ah = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0}, al = ah;
+                if (arow) {
+                    ah = *(const bf16x8_t*)(xh + (size_t)n * ldk + kk);
+                    al = *(const bf16x8_t*)(xl + (size_t)n * ldk + kk);
+                }
+                bf16x8_t b = __builtin_bit_cast(bf16x8_t, buf[st][h]);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc, 0, 0, 0);
+            }
+        }
+        // sum the NW waves' tiles: element (m, c) = (t / 16, t % 16)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red[wave * 256 + (4 * q + i) * 16 + n] = acc[i];
+        __syncthreads();
+        const int tile = g + (u / SUBS) * a.Gt;
+        const int sub = u % SUBS;
+        float x = 0.0f;
+        if (tid < 256) {
+#pragma unroll
+            for (int w = 0; w < NW; ++w) x += red[w * 256 + tid];
+        }
+        if (SUBS == 2 && sub == 0) {
+            stash = x;
+        } else if (a.S == 1) {
+            float v[2] = {SUBS == 2 ? stash : x, x};
+            if (tid < 256) tile_epilogue<SUBS>(a, tile, v);
+        } else if (tid < 256) {
+            // K split over S workgroups: store this range's partial tile for k_wsreduce
+            float* pt = a.part + ((size_t)tile * a.S + s) * SUBS * 256;
+            pt[tid] = SUBS == 2 ? stash : x;
+            if (SUBS == 2) pt[256 + tid] = x;
+        }
+        __syncthreads();
+    };
+
+    // ---- sub-tile loop, two per iteration so the fragment buffers are addressed statically ----
+    for (int u = 0; u < nsub_mine; u += 2) {
+        if (u + 1 < nsub_mine) issue(wb, u + 1);
+        compute(wa, u);
+        if (u + 1 >= nsub_mine) break;
+        if (u + 2 < nsub_mine) issue(wa, u + 2);
+        compute(wb, u + 1);
+    }
+}
+
+// Split-K finish: add the S partial tiles in order and apply the epilogue.
+template <int SUBS>
+__global__ __launch_bounds__(256) void k_wsreduce(WsArgs a) {
+    const int tile = blockIdx.x, tid = threadIdx.x;
+    const float* pt = a.part + (size_t)tile * a.S * SUBS * 256;
+    float v[2] = {0.f, 0.f};
+    for (int s = 0; s < a.S; ++s) {
+        v[0] += pt[((size_t)s * SUBS) * 256 + tid];
+        if (SUBS == 2) v[1] += pt[((size_t)s * SUBS + 1) * 256 + tid];
+    }
+    if (SUBS == 1) v[1] = v[0];
+    tile_epilogue<SUBS>(a, tile, v);
+}
+
+constexpr int kLdsBudget = 160 * 1024 - 2048;
+
+static size_t lds_bytes(int rows, int KR, int NW) {
+    return (size_t)rows * (KR + 8) * 2 * 2 + (size_t)NW * 256 * 4;
+}
+
+// Plan: number of K ranges S (1 when the whole activation row fits in LDS), K-range KR,
+// waves NW and fragment steps per lane, and how many workgroups walk the tiles.
+WsPlan ws_plan(int M, int N, int K, int mode) {
+    WsPlan p{};
+    int rows = M < 16 ? M : 16;
+    (void)mode;
+    p.tiles = N / 16;
+    for (int S = 1; S <= K / 256; ++S) {
+        if (K % S) continue;
+        int KR = K / S;
+        if (KR % 256) continue;
+        // waves: each a multiple of 64 columns; two fragment buffers of 8*steps VGPRs each must
+        // leave room in the 512-entry register file (8 steps with <= 8 waves, 4 with 16 waves)
+        int NW = 0, steps = 0;
+        for (int nw = 4; nw <= 16; nw *= 2) {
+            if (KR % (nw * 64)) continue;
+            int st = KR / (nw * 64);
+            if (st > (nw == 16 ? 4 : 8)) continue;
+            NW = nw;
+            steps = st;
+            break;
+        }
+        if (!NW) continue;
+        if (lds_bytes(rows, KR, NW) > (size_t)kLdsBudget) continue;
+        p.S = S;
+        p.KR = KR;
+        p.NW = NW;
+        p.steps = steps;
+        break;
+    }
+    if (!p.S) return p;
+    size_t lds = lds_bytes(rows, p.KR, p.NW);
+    int per_cu = (int)((160 * 1024) / (lds + 1024));
+    if (per_cu < 1) per_cu = 1;
+    if (per_cu > 2) per_cu = 2;
+    int want = 256 * per_cu;
+    int gt = want / p.S;
+    if (gt < 1) gt = 1;
+    if (gt > p.tiles) gt = p.tiles;
+    p.Gt = gt;
+    p.lds = lds;
+    return p;
+}
+
+void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
+    for (int r0 = 0; r0 < c.M; r0 += 16) {
+        int M = c.M - r0 < 16 ? c.M - r0 : 16;
+        WsArgs a{};
+        a.X = c.X; a.ldx = c.K; a.in_map = c.in_map; a.M = M; a.row0 = r0; a.K = c.K;
+        a.gamma = (const uint16_t*)c.gamma; a.eps = c.eps; a.ss = c.ss; a.nss = c.nss;
+        int tiles = 0;
+        for (int i = 0; i < 3; ++i) {
+            a.W[i] = i < c.nseg ? (const uint16_t*)c.W[i] : nullptr;
+            a.seg_tiles[i] = i < c.nseg ? c.seg_rows[i] / 16 : 0;
+            if (c.mode != kEpiSwiglu) tiles += a.seg_tiles[i];
+        }
+        if (c.mode == kEpiSwiglu) tiles = c.seg_rows[0] / 16;
+        a.nseg = c.nseg; a.mode = c.mode; a.tiles = tiles;
+        a.Y = c.Y; a.ldy = c.ldy; a.out_map = c.out_map; a.ss_out = c.ss_out;
+        WsPlan p = ws_plan(M, tiles * 16, c.K, c.mode);
+        a.KR = p.KR; a.S = p.S; a.Gt = p.Gt;
+        a.part = c.part;
+        a.H = c.H; a.Hkv = c.Hkv; a.hd = c.hd; a.row_pos = c.row_pos; a.row_seq = c.row_seq;
+        a.rcos = c.rcos; a.rsin = c.rsin; a.qout = c.qout; a.kc = c.kc; a.vc = c.vc;
+        a.cap = c.cap; a.max_batch = c.max_batch; a.layer = c.layer;
+        int subs = c.mode == kEpiSwiglu ? 2 : 1;
+        bool launched = false;
+        if (p.S) {
+            dim3 grid(p.S * p.Gt);
+            double wbytes = (double)tiles * 16 * subs * c.K * 2.0;
+            prof_begin(e, kProfGemv, wbytes + (double)M * c.K * 4.0 + (double)M * tiles * 16 * 4.0);
+#define SD2_WS_CASE(NWV, ST, SB)                                                   \
+    if (!launched && p.NW == NWV && p.steps == ST && subs == SB) {                  \
+        k_wsgemv<NWV, ST, SB><<<grid, NWV * 64, p.lds, s>>>(a);                     \
+        launched = true;                                                            \
+    }
+#define SD2_WS_STEPS8(NWV, SB)                                                    \
+    SD2_WS_CASE(NWV, 1, SB) SD2_WS_CASE(NWV, 2, SB) SD2_WS_CASE(NWV, 3, SB) SD2_WS_CASE(NWV, 4, SB) \
+    SD2_WS_CASE(NWV, 5, SB) SD2_WS_CASE(NWV, 6, SB) SD2_WS_CASE(NWV, 7, SB) SD2_WS_CASE(NWV, 8, SB)
+            SD2_WS_STEPS8(4, 1) SD2_WS_STEPS8(8, 1) SD2_WS_STEPS8(4, 2) SD2_WS_STEPS8(8, 2)
+            SD2_WS_CASE(16, 1, 1) SD2_WS_CASE(16, 2, 1) SD2_WS_CASE(16, 3, 1) SD2_WS_CASE(16, 4, 1)
+            SD2_WS_CASE(16, 1, 2) SD2_WS_CASE(16, 2, 2) SD2_WS_CASE(16, 3, 2) SD2_WS_CASE(16, 4, 2)
+#undef SD2_WS_STEPS8
+#undef SD2_WS_CASE
+            if (launched && p.S > 1) {
+                if (subs == 1) k_wsreduce<1><<<tiles, 256, 0, s>>>(a);
+                else k_wsreduce<2><<<tiles, 256, 0, s>>>(a);
+            }
+            prof_end(e);
+        }
+        if (!launched && e) e->bad_launch = true;
+    }
+}
+
+}  // namespace sd2

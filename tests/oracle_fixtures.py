@@ -4,9 +4,9 @@ import numpy as np
 import sd2_inputs as si
 from sd2_inputs.configs import Dims, Workload
 
-# Grouped-query shapes (H/Hkv = 4) at a size the float64 oracle runs in milliseconds.
+# Grouped-query shapes (H/Hkv = 4 and 2) at a size the float64 oracle runs in milliseconds.
 GQA = Workload(
-    name="gqa-tiny", verifier=Dims(3, 128, 8, 2, 256, 512, 5e5), drafter=Dims(2, 64, 4, 2, 192, 512, 5e5),
+    name="gqa-tiny", verifier=Dims(3, 256, 8, 2, 512, 512, 5e5), drafter=Dims(2, 256, 4, 2, 768, 512, 5e5),
     dtype="bf16", k=3, batch=2, prompt=(5, 9), new_tokens=24, temperature=1.0, seed=7)
 
 # Vocabulary of 8 for exact enumeration of one round's output law.
