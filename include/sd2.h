@@ -160,9 +160,9 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
 #define SD2_PROF_OTHER 4     /* embedding/planning, RoPE and cache append */
 
 /*
- * Measurement hook.  enable != 0: following rounds record a HIP event pair on the handle's
- * stream around every kernel launch (the recorded round graph then carries the event nodes);
- * enable == 0 turns this off.  Rounds stay functionally identical.
+ * Measurement hook.  enable != 0: following rounds are launched one kernel at a time (not from
+ * the recorded graph) with a HIP event pair recorded on the handle's stream around every
+ * launch; enable == 0 returns to graph replay.  Rounds stay functionally identical.
  */
 sd2_status sd2_profile(sd2_handle_t h, int32_t enable);
 

@@ -6,9 +6,8 @@
 // row read once) -- and one span of kSplit cache positions.  It walks its span in chunks of 64
 // positions with an online softmax (running max, running sum, rescaled output), keeping the
 // next chunk's K/V in flight in registers while the current chunk is scored from LDS, and
-// writes an un-normalised partial (output, max, sum).  A second kernel merges the spans of
-// each (row, head) in span order (a kernel boundary, rather than an in-kernel hand-off, makes
-// the partials visible: on this part a device-scope release fence writes back the whole L2).  The causal mask is key position <= query position; rows
+// writes an un-normalised partial (output, max, sum); the last span to finish for a set of
+// query vectors merges all spans in span order (see arrive_last).  The causal mask is key position <= query position; rows
 // with position -1 are inactive and produce zeros.  Workgroups of one KV head are placed on
 // the same XCD (workgroup ids are dealt round-robin over the 8 XCDs), so a KV head is fetched
 // into one L2 only.
@@ -21,6 +20,7 @@ namespace sd2 {
 
 constexpr int kAttnCL = 64;   // cache positions per chunk
 constexpr int kSplit = 128;   // cache positions per workgroup
+constexpr int kMaxSplit = 64; // spans per query vector (cache capacity up to 8192 positions)
 constexpr int kAttnQT = 32;   // query vectors per workgroup
 constexpr int kAttnT = 256;
 constexpr int kXcds = 8;
@@ -40,6 +40,7 @@ struct AttnArgs {
     int nsplit; // position spans per group
     float scale;
     float* part;     // [row][head][nsplit][HD + 2]
+    int32_t* cnt;    // one arrival counter per workgroup of the split-free grid
 };
 
 // Request chunk c of K and V (positions past maxpos re-read the last valid row; they are masked).
@@ -64,6 +65,7 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
     __shared__ int qhead[kAttnQT];
     __shared__ float mrun[kAttnQT], lrun[kAttnQT], rescale[kAttnQT];
     __shared__ int maxpos_s;
+    __shared__ int last_flag;
     const int tid = threadIdx.x;
     const int G = a.H / a.Hkv;
     const int members = G / a.hp;  // workgroups per group
@@ -186,43 +188,49 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
         int qi = oq0 + jj * QSTEP;
         if (qi < nq) {
             float* pp = a.part + (((size_t)qrow[qi] * a.H + qhead[qi]) * a.nsplit + sp) * (HD + 2);
-            pp[od] = acc[jj];
+            store_through(pp + od, acc[jj]);
             if (od == 0) {
-                pp[HD] = mrun[qi];
-                pp[HD + 1] = lrun[qi];
+                store_through(pp + HD, mrun[qi]);
+                store_through(pp + HD + 1, lrun[qi]);
             }
         }
     }
-}
-
-// Merge the position spans of every (row, head) in span order: out = sum_s e^(m_s - M) O_s /
-// sum_s e^(m_s - M) l_s.  One thread per output element.
-template <int HD>
-__global__ __launch_bounds__(256) void k_attn_merge(const float* __restrict__ part, const int32_t* __restrict__ row_pos,
-                                                    float* __restrict__ out, int rows, int H, int nsplit) {
-    size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= (size_t)rows * H * HD) return;
-    int d = idx % HD;
-    size_t rh = idx / HD;
-    int row = (int)(rh / H);
-    int pos = row_pos[row];
-    float res = 0.f;
-    if (pos >= 0) {
-        const float* pp = part + rh * nsplit * (HD + 2);
-        int live = min(nsplit, pos / kSplit + 1);
-        float M = -INFINITY;
-        for (int s = 0; s < live; ++s) M = fmaxf(M, pp[(size_t)s * (HD + 2) + HD]);
-        float L = 0.f, O = 0.f;
-        for (int s = 0; s < live; ++s) {
-            const float* e = pp + (size_t)s * (HD + 2);
-            if (e[HD] == -INFINITY) continue;
-            float w = expf(e[HD] - M);
-            L += w * e[HD + 1];
-            O += w * e[d];
+    // the last span of these query vectors to finish merges all spans in span order
+    if (!arrive_last(a.cnt + wg, a.nsplit, &last_flag)) return;
+    const int nlive = maxpos_s >= 0 ? min(a.nsplit, maxpos_s / kSplit + 1) : 0;
+    for (int idx = tid; idx < nq * HD; idx += kAttnT) {
+        int qi = idx / HD, d = idx % HD;
+        int pos = qpos[qi];
+        float res = 0.f;
+        if (pos >= 0) {
+            const float* pp = a.part + ((size_t)qrow[qi] * a.H + qhead[qi]) * a.nsplit * (HD + 2);
+            float mv[kMaxSplit], lv[kMaxSplit], ov[kMaxSplit];
+#pragma unroll
+            for (int s2 = 0; s2 < kMaxSplit; ++s2) {
+                if (s2 < nlive) {
+                    const float* e = pp + (size_t)s2 * (HD + 2);
+                    mv[s2] = e[HD];
+                    lv[s2] = e[HD + 1];
+                    ov[s2] = e[d];
+                }
+            }
+            float M = -INFINITY;
+#pragma unroll
+            for (int s2 = 0; s2 < kMaxSplit; ++s2)
+                if (s2 < nlive) M = fmaxf(M, mv[s2]);
+            float L = 0.f, O = 0.f;
+#pragma unroll
+            for (int s2 = 0; s2 < kMaxSplit; ++s2) {
+                if (s2 < nlive && mv[s2] != -INFINITY) {
+                    float w = expf(mv[s2] - M);
+                    L += w * lv[s2];
+                    O += w * ov[s2];
+                }
+            }
+            res = L > 0.f ? O / L : 0.f;
         }
-        res = L > 0.f ? O / L : 0.f;
+        a.out[(size_t)qrow[qi] * a.H * HD + qhead[qi] * HD + d] = res;
     }
-    out[idx] = res;
 }
 
 static size_t attn_lds(int hd) {
@@ -247,25 +255,26 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
     int members = G / a.hp;
     a.nsplit = attn_nsplit(e.cap);
     a.part = e.ws.attn_part;
+    a.cnt = e.ws.attn_cnt;
     int nblk = (a.ngrp + kXcds - 1) / kXcds * kXcds * members * a.nsplit;
-    int nmerge = (int)(((size_t)rows * dm.n_heads * m.hd + 255) / 256);
     prof_begin(&e, kProfAttn, 0.0);
     switch (m.hd) {
-        case 32:
-            k_attn<32><<<nblk, kAttnT, attn_lds(32), s>>>(a);
-            k_attn_merge<32><<<nmerge, 256, 0, s>>>(a.part, a.row_pos, a.out, rows, dm.n_heads, a.nsplit);
-            break;
-        case 64:
-            k_attn<64><<<nblk, kAttnT, attn_lds(64), s>>>(a);
-            k_attn_merge<64><<<nmerge, 256, 0, s>>>(a.part, a.row_pos, a.out, rows, dm.n_heads, a.nsplit);
-            break;
-        case 128:
-            k_attn<128><<<nblk, kAttnT, attn_lds(128), s>>>(a);
-            k_attn_merge<128><<<nmerge, 256, 0, s>>>(a.part, a.row_pos, a.out, rows, dm.n_heads, a.nsplit);
-            break;
+        case 32: k_attn<32><<<nblk, kAttnT, attn_lds(32), s>>>(a); break;
+        case 64: k_attn<64><<<nblk, kAttnT, attn_lds(64), s>>>(a); break;
+        case 128: k_attn<128><<<nblk, kAttnT, attn_lds(128), s>>>(a); break;
         default: e.bad_launch = true; break;
     }
     prof_end(&e);
+}
+
+// Workgroups of the split-free attention grid for a launch shape (arrival counters needed).
+size_t attn_groups(int rows, int rps, int H, int Hkv) {
+    int nseq = rows / rps, G = H / Hkv;
+    int hp = (nseq * Hkv >= 128 && G <= kAttnQT && rps * G <= kAttnQT) ? G : 1;
+    int rows_per_tile = kAttnQT / hp;
+    int nrt = (rps + rows_per_tile - 1) / rows_per_tile;
+    int ngrp = nseq * Hkv * nrt;
+    return (size_t)(ngrp + kXcds - 1) / kXcds * kXcds * (G / hp);
 }
 
 int attn_nsplit(int cap) { return (cap + kSplit - 1) / kSplit; }

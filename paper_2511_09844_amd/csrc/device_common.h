@@ -100,4 +100,30 @@ __device__ __forceinline__ float gumbel(uint32_t w) { return -logf(-logf(u01(w))
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
+// ---------------------------------------------------------------------------
+// Last-arriving workgroup hand-off inside one kernel, without a device-scope fence (on this
+// part a release fence writes back the whole L2, which costs more than a kernel launch):
+//   - every workgroup stores its partial with device-scope (write-through) stores and waits
+//     until they have completed, then counts itself in with a device-scope atomic;
+//   - the workgroup that counts in last reads all partials with ordinary loads.  Those lines
+//     are read by nobody else during the kernel, so no stale copy of them can sit in the
+//     reader's caches; the caches are invalidated at every kernel start.
+// The last workgroup also resets the counter for the next launch.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void store_through(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Returns true in the last workgroup (uniform across the block).
+__device__ __forceinline__ bool arrive_last(int32_t* cnt, int expected, int* flag_smem) {
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int prev = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag_smem = prev == expected - 1;
+        if (prev == expected - 1) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    return *flag_smem != 0;
+}
+
 }  // namespace sd2

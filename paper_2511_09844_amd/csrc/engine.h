@@ -75,7 +75,9 @@ struct Workspace {
     int32_t* forced_on;     // [1]
     // split-K partial tiles of the projection kernel; attention partials per position span
     float* ws_part;
+    int32_t* ws_cnt;
     float* attn_part;
+    int32_t* attn_cnt;
 };
 
 // Per-launch timing entries (HIP events recorded on the engine's stream).
@@ -144,6 +146,7 @@ struct WsCall {
     const int32_t* out_map;
     float* ss_out;
     float* part;
+    int32_t* cnt;
     int H, Hkv, hd;
     const int32_t *row_pos, *row_seq;
     const float *rcos, *rsin;
@@ -158,6 +161,7 @@ WsPlan ws_plan(int M, int N, int K, int mode);
 void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c);
 void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride);
 int attn_nsplit(int cap);
+size_t attn_groups(int rows, int rps, int H, int Hkv);
 void launch_gemv(Engine* e, hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K,
                  const void* gamma, float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y,
                  int ldy, const int32_t* out_map);

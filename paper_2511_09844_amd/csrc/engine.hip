@@ -60,7 +60,7 @@ bool config_ok(const sd2_config* c) {
     if (c->k < 1 || c->k > kMaxK) return false;
     if (c->max_batch < 1 || c->max_batch > 256) return false;
     if (c->max_new_tokens < 1) return false;
-    if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;
+    if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // 8192 = 64 spans of 128
     if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
     return true;
 }
@@ -148,6 +148,10 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                 }
         }
         w.ws_part = cv.take<float>(std::max<size_t>(pmax, 1));
+        size_t tmax = (size_t)std::max(c.verifier.vocab, c.drafter.vocab) / 16 + 1;
+        for (int i = 0; i < 2; ++i)
+            tmax = std::max(tmax, (size_t)std::max(dd[i]->d_ff, dd[i]->d_model) / 16 + 1);
+        w.ws_cnt = cv.take<int32_t>(tmax);
     }
     {
         size_t amax = 0;
@@ -157,6 +161,19 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
             amax = std::max(amax, (size_t)maxm * dd[i]->n_heads * attn_nsplit(cap) * (hd + 2));
         }
         w.attn_part = cv.take<float>(amax);
+        // arrival counters: the largest split-free grid of any launch shape
+        size_t gmax = 1;
+        for (int i = 0; i < 2; ++i) {
+            const sd2_dims& d = *dd[i];
+            gmax = std::max(gmax, attn_groups(2 * B, 2, d.n_heads, d.n_kv_heads));
+            gmax = std::max(gmax, attn_groups(B, 1, d.n_heads, d.n_kv_heads));
+            gmax = std::max(gmax, attn_groups(B * (c.k + 1), c.k + 1, d.n_heads, d.n_kv_heads));
+            for (int nseq = 1; nseq <= B; ++nseq) {
+                int rps = std::max(1, kPrefillRows / nseq);
+                gmax = std::max(gmax, attn_groups(nseq * rps, rps, d.n_heads, d.n_kv_heads));
+            }
+        }
+        w.attn_cnt = cv.take<int32_t>(gmax);
     }
     for (int i = 0; i < 2; ++i) {
         ModelDev* m = ms[i];
@@ -241,8 +258,9 @@ void drop_graph(Engine& e) {
 }
 
 sd2_status run_round(Engine* e, int32_t* out_tokens, int32_t* out_counts) {
-    // Replay the recorded round when the shape and output buffers are unchanged.
-    if (!e->use_graph) {
+    // Replay the recorded round when the shape and output buffers are unchanged.  Profiled rounds
+    // are launched eagerly: HIP events recorded inside a captured graph cannot be timed.
+    if (!e->use_graph || e->prof_on) {
         enqueue_round(*e, out_tokens, out_counts);
         return check_launch(e, "round");
     }

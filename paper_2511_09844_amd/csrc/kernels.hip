@@ -368,6 +368,7 @@ __global__ __launch_bounds__(128) void k_rope_append(RopeArgs a) {
 static WsCall ws_base(Engine& e, ModelDev& m) {
     WsCall c{};
     c.part = e.ws.ws_part;
+    c.cnt = e.ws.ws_cnt;
     c.eps = m.dm.rms_eps;
     c.nss = m.dm.d_model / 16;
     return c;

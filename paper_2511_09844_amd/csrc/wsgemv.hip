@@ -12,9 +12,8 @@
 // are summed in LDS.  Weights are read exactly once.
 //
 // When the activation slice of the whole K does not fit in LDS, K is cut into S ranges; each
-// range writes a partial tile and a separate reduction kernel adds the S partials in order and
-// applies the epilogue (a kernel boundary makes the partials visible: on this part an in-kernel
-// device-scope release fence writes back the whole L2 and costs far more than a launch).
+// range writes a partial tile (write-through), and the last workgroup to finish a tile adds the
+// S partials in range order and applies the epilogue (see arrive_last).
 //
 // Epilogues: plain store (optional output-row map), residual add (+ per-16-column sums of
 // squares of the new residual, consumed by the next RMSNorm), SwiGLU on paired gate/up
@@ -56,6 +55,7 @@ struct WsArgs {
     float* ss_out;
     int KR, S, Gt;  // K-range per workgroup, number of K ranges, workgroups per K range
     float* part;    // S > 1: [tiles][S][SUBS][256]
+    int32_t* cnt;   // S > 1: arrival counter per tile
     // Q|K|V mode
     int H, Hkv, hd;
     const int32_t *row_pos, *row_seq;
@@ -140,6 +140,7 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ float inv_rms[16];
     __shared__ int src_row[16];
+    __shared__ int last_flag;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int M = a.M;
     const int KR = a.KR;
@@ -155,8 +156,8 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
     const int kw0 = wave * (KR / NW);
 
     // The workgroup's work is a sequence of sub-tiles u = 0, 1, ...: tile g + (u / SUBS) * Gt,
-    // sub-tile u % SUBS (SwiGLU: gate then up).  Fragments of sub-tile u+1 are requested
-    // before sub-tile u is multiplied; the two register buffers alternate.
+    // sub-tile u % SUBS (SwiGLU: gate then up).  Two sub-tiles of weight fragments are kept in
+    // flight in two register buffers.
     const int ntile_mine = a.tiles > g ? (a.tiles - g + a.Gt - 1) / a.Gt : 0;
     const int nsub_mine = ntile_mine * SUBS;
     u32x4_t wa[STEPS][2], wb[STEPS][2];
@@ -166,14 +167,12 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
 #pragma unroll
         for (int st = 0; st < STEPS; ++st)
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
-                buf[st][h] = *(const u32x4_t*)(wp + st * 64 + 8 * h);
+            for (int h = 0; h < 2; ++h) buf[st][h] = *(const u32x4_t*)(wp + st * 64 + 8 * h);
     };
 
-    if (nsub_mine > 0) issue(wa, 0);
-
-    // ---- prologue: normalisation scale per row (one wave per row, the slice sums of squares
-    //      read in parallel), then the hi/lo activation slice with its loads batched ----
+    // ---- prologue.  Loads return in issue order, so the small activation loads go first, then
+    //      the first weight sub-tile, then the RMSNorm statistics (needed only by the epilogue:
+    //      the row scale 1/rms is applied to the outputs, the gain to the staged activations) ----
     if (tid < 16) {
         int src = -1;
         if (tid < M) src = a.in_map ? a.in_map[a.row0 + tid] : a.row0 + tid;
@@ -181,54 +180,65 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
         inv_rms[tid] = 1.0f;
     }
     __syncthreads();
-    if (a.gamma) {
-        for (int m = wave; m < M; m += NW) {
+    constexpr int XB = 16;  // activation float4 loads per thread issued ahead of the weights
+    const int n4 = KR / 4;
+    const int nx = M * n4;  // float4 groups of the slice, row-major
+    float4 xv[XB];
+#pragma unroll
+    for (int i = 0; i < XB; ++i) {
+        const int idx = tid + i * NW * 64;
+        if (idx < nx) {
+            const int m = idx / n4, kk = (idx % n4) * 4;
             const int src = src_row[m];
-            float sum = 0.0f;
-            if (src >= 0) {
-                const float* sp = a.ss + (size_t)src * a.nss;
-                for (int t = lane; t < a.nss; t += 64) sum += sp[t];
-            }
-            sum = wave_sum(sum);
-            if (lane == 0) inv_rms[m] = rsqrtf(sum / (float)a.K + a.eps);
+            xv[i] = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        __syncthreads();
     }
-    {
-        constexpr int B4 = 4;  // float4 loads in flight per thread
-        const int n4 = KR / 4;
-        const int total = M * n4;
-        for (int base = tid; base < total; base += NW * 64 * B4) {
-            float4 v[B4];
+    if (nsub_mine > 0) issue(wa, 0);
+    float ssum = 0.0f;
+    const int ss_row = wave < M ? src_row[wave] : -1;
+    if (a.gamma && ss_row >= 0)
+        for (int t = lane; t < a.nss; t += 64) ssum += a.ss[(size_t)ss_row * a.nss + t];
+    auto stage = [&](const float4& v, int idx) {
+        const int m = idx / n4, kk = (idx % n4) * 4;
+        float gm[4] = {1.f, 1.f, 1.f, 1.f};
+        if (a.gamma) {
+            uint2 gw = *(const uint2*)(a.gamma + k0 + kk);
+            gm[0] = bf16_lo(gw.x); gm[1] = bf16_hi(gw.x); gm[2] = bf16_lo(gw.y); gm[3] = bf16_hi(gw.y);
+        }
+        float vv[4] = {v.x * gm[0], v.y * gm[1], v.z * gm[2], v.w * gm[3]};
+        uint16_t hi[4], lo[4];
 #pragma unroll
-            for (int u = 0; u < B4; ++u) {
-                int idx = base + u * NW * 64;
-                v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (idx < total) {
-                    int m = idx / n4, kk = (idx % n4) * 4;
-                    int src = src_row[m];
-                    if (src >= 0) v[u] = *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk);
-                }
-            }
+        for (int e = 0; e < 4; ++e) {
+            hi[e] = f32_to_bf16_rne(vv[e]);
+            lo[e] = f32_to_bf16_rne(vv[e] - bf16_to_f32(hi[e]));
+        }
+        *(uint2*)(xh + (size_t)m * ldk + kk) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+        *(uint2*)(xl + (size_t)m * ldk + kk) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+    };
 #pragma unroll
-            for (int u = 0; u < B4; ++u) {
-                int idx = base + u * NW * 64;
-                if (idx >= total) break;
-                int m = idx / n4, kk = (idx % n4) * 4;
-                float vv[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-                uint16_t hi[4], lo[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float x = vv[e];
-                    if (a.gamma) x *= inv_rms[m] * bf16_to_f32(a.gamma[k0 + kk + e]);
-                    hi[e] = f32_to_bf16_rne(x);
-                    lo[e] = f32_to_bf16_rne(x - bf16_to_f32(hi[e]));
-                }
-                *(uint2*)(xh + (size_t)m * ldk + kk) =
-                    make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-                *(uint2*)(xl + (size_t)m * ldk + kk) =
-                    make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
-            }
+    for (int i = 0; i < XB; ++i) {
+        const int idx = tid + i * NW * 64;
+        if (idx < nx) stage(xv[i], idx);
+    }
+    // slices larger than XB float4 per thread (not used by the planned shapes) stage the rest here
+    for (int idx = tid + XB * NW * 64; idx < nx; idx += NW * 64) {
+        const int m = idx / n4, kk = (idx % n4) * 4;
+        const int src = src_row[m];
+        float4 v = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+        stage(v, idx);
+    }
+    if (nsub_mine > 1) issue(wb, 1);
+    if (a.gamma) {
+        ssum = wave_sum(ssum);
+        if (lane == 0 && wave < M) inv_rms[wave] = rsqrtf(ssum / (float)a.K + a.eps);
+        // rows beyond the number of waves (M > NW)
+        for (int m = NW + wave; m < M; m += NW) {
+            const int src = src_row[m];
+            float sm = 0.0f;
+            if (src >= 0)
+                for (int t = lane; t < a.nss; t += 64) sm += a.ss[(size_t)src * a.nss + t];
+            sm = wave_sum(sm);
+            if (lane == 0) inv_rms[m] = rsqrtf(sm / (float)a.K + a.eps);
         }
     }
     __syncthreads();
@@ -252,7 +262,7 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
                 acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc, 0, 0, 0);
             }
         }
-        // sum the NW waves' tiles: element (m, c) = (t / 16, t % 16)
+        // sum the NW waves' tiles: element (m, c) = (t / 16, t % 16); scale by the row's 1/rms
 #pragma unroll
         for (int i = 0; i < 4; ++i) red[wave * 256 + (4 * q + i) * 16 + n] = acc[i];
         __syncthreads();
@@ -262,43 +272,55 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
         if (tid < 256) {
 #pragma unroll
             for (int w = 0; w < NW; ++w) x += red[w * 256 + tid];
+            x *= inv_rms[tid >> 4];
         }
         if (SUBS == 2 && sub == 0) {
             stash = x;
         } else if (a.S == 1) {
             float v[2] = {SUBS == 2 ? stash : x, x};
             if (tid < 256) tile_epilogue<SUBS>(a, tile, v);
-        } else if (tid < 256) {
-            // K split over S workgroups: store this range's partial tile for k_wsreduce
-            float* pt = a.part + ((size_t)tile * a.S + s) * SUBS * 256;
-            pt[tid] = SUBS == 2 ? stash : x;
-            if (SUBS == 2) pt[256 + tid] = x;
+        } else {
+            // K split over S workgroups: the last to finish this tile adds the partials in order
+            float* pt = a.part + (size_t)tile * a.S * SUBS * 256;
+            if (tid < 256) {
+                store_through(pt + (size_t)s * SUBS * 256 + tid, SUBS == 2 ? stash : x);
+                if (SUBS == 2) store_through(pt + (size_t)s * SUBS * 256 + 256 + tid, x);
+            }
+            if (arrive_last(a.cnt + tile, a.S, &last_flag) && tid < 256) {
+                float p0[8], p1[8];
+                float v[2] = {0.f, 0.f};
+                for (int s0 = 0; s0 < a.S; s0 += 8) {
+                    const int ns = min(8, a.S - s0);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        if (i < ns) {
+                            p0[i] = pt[(size_t)(s0 + i) * SUBS * 256 + tid];
+                            if (SUBS == 2) p1[i] = pt[(size_t)(s0 + i) * SUBS * 256 + 256 + tid];
+                        }
+                    }
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        if (i < ns) {
+                            v[0] += p0[i];
+                            if (SUBS == 2) v[1] += p1[i];
+                        }
+                    }
+                }
+                if (SUBS == 1) v[1] = v[0];
+                tile_epilogue<SUBS>(a, tile, v);
+            }
         }
         __syncthreads();
     };
 
-    // ---- sub-tile loop, two per iteration so the fragment buffers are addressed statically ----
+    // ---- sub-tile loop: after a buffer is consumed it is refilled two sub-tiles ahead ----
     for (int u = 0; u < nsub_mine; u += 2) {
-        if (u + 1 < nsub_mine) issue(wb, u + 1);
         compute(wa, u);
-        if (u + 1 >= nsub_mine) break;
         if (u + 2 < nsub_mine) issue(wa, u + 2);
+        if (u + 1 >= nsub_mine) break;
         compute(wb, u + 1);
+        if (u + 3 < nsub_mine) issue(wb, u + 3);
     }
-}
-
-// Split-K finish: add the S partial tiles in order and apply the epilogue.
-template <int SUBS>
-__global__ __launch_bounds__(256) void k_wsreduce(WsArgs a) {
-    const int tile = blockIdx.x, tid = threadIdx.x;
-    const float* pt = a.part + (size_t)tile * a.S * SUBS * 256;
-    float v[2] = {0.f, 0.f};
-    for (int s = 0; s < a.S; ++s) {
-        v[0] += pt[((size_t)s * SUBS) * 256 + tid];
-        if (SUBS == 2) v[1] += pt[((size_t)s * SUBS + 1) * 256 + tid];
-    }
-    if (SUBS == 1) v[1] = v[0];
-    tile_epilogue<SUBS>(a, tile, v);
 }
 
 constexpr int kLdsBudget = 160 * 1024 - 2048;
@@ -369,6 +391,7 @@ void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
         WsPlan p = ws_plan(M, tiles * 16, c.K, c.mode);
         a.KR = p.KR; a.S = p.S; a.Gt = p.Gt;
         a.part = c.part;
+        a.cnt = c.cnt;
         a.H = c.H; a.Hkv = c.Hkv; a.hd = c.hd; a.row_pos = c.row_pos; a.row_seq = c.row_seq;
         a.rcos = c.rcos; a.rsin = c.rsin; a.qout = c.qout; a.kc = c.kc; a.vc = c.vc;
         a.cap = c.cap; a.max_batch = c.max_batch; a.layer = c.layer;
@@ -391,10 +414,6 @@ void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
             SD2_WS_CASE(16, 1, 2) SD2_WS_CASE(16, 2, 2) SD2_WS_CASE(16, 3, 2) SD2_WS_CASE(16, 4, 2)
 #undef SD2_WS_STEPS8
 #undef SD2_WS_CASE
-            if (launched && p.S > 1) {
-                if (subs == 1) k_wsreduce<1><<<tiles, 256, 0, s>>>(a);
-                else k_wsreduce<2><<<tiles, 256, 0, s>>>(a);
-            }
             prof_end(e);
         }
         if (!launched && e) e->bad_launch = true;

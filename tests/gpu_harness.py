@@ -134,5 +134,7 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
     for b in seqs:
         assert o.state(b)["done"] == 1
     eng.close()
+    del eng, dv, dd, ws_dev
+    torch.cuda.empty_cache()
     log(f"[parity] {wl.name}: {st}")
     return st

@@ -31,3 +31,26 @@ def test_parity_gqa_greedy():
 def test_parity_small_bf16_greedy():
     """12-layer d=768 verifier / 4-layer d=512 drafter, vocab 32000, greedy, 128 new tokens."""
     _run(si.SMALL)
+
+
+@pytest.fixture(scope="module")
+def host_8b():
+    """Host weights of the 8B-shaped verifier / 1B-shaped drafter (generated once, ~19 GB)."""
+    wl = si.LLAMA8B
+    return si.model_weights(wl, 0), si.model_weights(wl, 1), si.steer_weights(wl)
+
+
+def test_parity_8b_shapes_short_prompt(host_8b):
+    """Full 8B/1B model dimensions (32 x d4096 GQA verifier, 16 x d2048 drafter, 128256 vocab),
+    sampling at T=1, k=5, batch 1; a 16-token prompt keeps the float64 oracle within seconds."""
+    wl = si.LLAMA8B.with_(prompt=(16, 16), new_tokens=10)
+    wv, wd, ws = host_8b
+    _run(wl, wv=wv, wd=wd, ws=ws)
+
+
+def test_parity_8b_batched_ragged_sampled_sequences(host_8b):
+    """Batched configuration (16 sequences, ragged prompts, k=7, T=0.7): the GPU runs all 16
+    sequences; the oracle follows two of them, which must match exactly as if run alone."""
+    wl = si.LLAMA8B_BATCHED.with_(prompt=(6, 30), new_tokens=5)
+    wv, wd, ws = host_8b
+    _run(wl, wv=wv, wd=wd, ws=ws, seqs=[0, 11])
