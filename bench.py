@@ -70,6 +70,105 @@ def cpu_baseline(wl, wv, wd, ws, toks, lens, budget_s):
                       f"({tokens} tokens) timed; float64 C oracle, OpenMP over output rows"}
 
 
+# ---------------------------------------------------------------------------------------------
+# rocprofv3 post-processing (host-only; no GPU).  Rounds are delimited by k_set_flag, the one
+# single-thread kernel every sd2_round launches first.
+# ---------------------------------------------------------------------------------------------
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_wsgemv_8b-bf16-b1_traffic.json")
+TRAFFIC_SOURCES = ("paper_2511_09844_amd/csrc/wsgemv.hip", "paper_2511_09844_amd/csrc/device_common.h")
+
+
+def _kclass(name):
+    return "k_wsgemv" if "k_wsgemv" in name else "k_attn" if "k_attn" in name else "other"
+
+
+def _round_windows(names, skip_first):
+    marks = [i for i, n in enumerate(names) if "k_set_flag" in n]
+    return list(zip(marks[:-1], marks[1:]))[skip_first:]
+
+
+def summarize_trace(path, last_eager):
+    """Per-round kernel time by class from a kernel_trace.csv: the graph-launched rounds and the
+    last `last_eager` (eagerly launched, event-timed) rounds separately."""
+    import csv
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
+    rows.sort()
+    wins = _round_windows([r[2] for r in rows], 0)
+    groups = (("graph-launched rounds", wins[:len(wins) - last_eager]), ("eager (event-timed) rounds", wins[-last_eager:]))
+    for title, ws in groups:
+        if not ws:
+            continue
+        per, span = {}, 0
+        for a, b in ws:
+            span += rows[b][0] - rows[a][0]
+            for st, en, n in rows[a:b]:
+                c = per.setdefault(_kclass(n), [0, 0])
+                c[0] += 1
+                c[1] += en - st
+        print(f"{title}: {len(ws)} rounds, {span / len(ws) / 1e3:.1f} us per round (first kernel to first kernel)")
+        for c, (n, ns) in sorted(per.items(), key=lambda x: -x[1][1]):
+            print(f"  {c:9s} {n / len(ws):6.0f} launches/round  {ns / len(ws) / 1e3:9.1f} us/round  "
+                  f"avg {ns / n / 1e3:7.2f} us/launch")
+
+
+def _source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for p in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def summarize_pmc(fetch_csv, write_csv, write_json):
+    """HBM traffic per k_wsgemv launch from FETCH_SIZE and WRITE_SIZE runs (KiB per dispatch), each
+    scaled by what the same counter reads for the 1 GiB calibration copy."""
+    import csv
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = []
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+        rows.sort()
+        wins = _round_windows([r[1] for r in rows], 1)
+        n, kib = 0, 0.0
+        for a, b in wins:
+            for _, name, v in rows[a:b]:
+                if "k_wsgemv" in name:
+                    n += 1
+                    kib += v
+        copy = max((v for _, name, v in rows if "copyBuffer" in name), default=0.0)
+        factor = (1 << 20) / copy if copy else float("nan")
+        out[counter] = {"launches": n, "kib_per_launch_raw": kib / max(1, n), "copy_kib_raw": copy,
+                        "scale": factor, "bytes_per_launch": kib / max(1, n) * factor * 1024}
+        print(f"{counter}: {n} k_wsgemv launches in {len(wins)} rounds, {kib / max(1, n):.1f} KiB/launch raw; "
+              f"1 GiB copy reads {copy:.0f} KiB -> scale {factor:.4f}; {out[counter]['bytes_per_launch'] / 1e6:.3f} MB/launch")
+    total = out["FETCH_SIZE"]["bytes_per_launch"] + out["WRITE_SIZE"]["bytes_per_launch"]
+    print(f"traffic per k_wsgemv launch: {total / 1e6:.3f} MB")
+    if write_json:
+        rec = {"kernel": "k_wsgemv", "workload": "8b-bf16-b1", "source_sha256": _source_hash(),
+               "traffic_bytes_per_launch": total, "counters": out}
+        with open(write_json, "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+
+
+def stored_traffic(workload):
+    """Counter-measured bytes per k_wsgemv launch, if taken on the current kernel source and workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("workload") != workload or rec.get("source_sha256") != _source_hash():
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
 def main():
     import sd2_inputs as si
 
@@ -81,7 +180,22 @@ def main():
     ap.add_argument("--prof-rounds", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="after the rounds, copy one 1 GiB buffer (a plain copy of known size, the reference "
+                         "point for scaling hardware traffic counters)")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print the per-round breakdown of a rocprofv3 kernel trace of this script and exit")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print k_wsgemv HBM traffic from two rocprofv3 --pmc runs of this script with "
+                         "--calib-copy and exit")
+    ap.add_argument("--write-traffic", action="store_true", help="with --summarize-pmc: store the result")
     args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.prof_rounds)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, TRAFFIC_FILE if args.write_traffic else None)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build", file=sys.stderr)
         sys.exit(2)
@@ -152,6 +266,13 @@ def main():
                     prof[c][2] += pby
             eng.profile(False)
         torch.cuda.synchronize()
+        if args.calib_copy:
+            src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+            dst = torch.empty_like(src)
+            torch.cuda.synchronize()
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            del src, dst
 
     active = [b for b in range(wl.batch) if not st0[b]["done"]]
     tokens = sum(st1[b]["produced"] - st0[b]["produced"] for b in range(wl.batch))
@@ -197,9 +318,9 @@ def main():
         "block_efficiency": tau,
         "round_bytes": bytes_round,
         "round_hbm_frac": bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS,
-        "roofline": {"bound": "hbm", "kernel": "k_gemv (all weight-streaming projections + LM heads)",
+        "roofline": {"bound": "hbm", "kernel": "k_wsgemv (every weight-streaming projection: QKV, O, gate|up, down, LM heads, W_s)",
                      "achieved": gemv_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gemv_gbs / PEAK_HBM_GBS,
-                     "traffic": None, "launches_per_round": g_n / max(1, args.prof_rounds),
+                     "traffic": stored_traffic(wl.name), "launches_per_round": g_n / max(1, args.prof_rounds),
                      "avg_launch_us": g_ms / max(1, g_n) * 1e3,
                      "bytes_per_launch": g_by / max(1, g_n)},
         "cpu_baseline": None,

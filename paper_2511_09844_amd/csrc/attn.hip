@@ -13,6 +13,8 @@
 // into one L2 only.
 #include <math.h>
 
+#include <hip/hip_ext.h>
+
 #include "device_common.h"
 #include "engine.h"
 
@@ -257,14 +259,15 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
     a.part = e.ws.attn_part;
     a.cnt = e.ws.attn_cnt;
     int nblk = (a.ngrp + kXcds - 1) / kXcds * kXcds * members * a.nsplit;
-    prof_begin(&e, kProfAttn, 0.0);
+    ProfEntry* pe = prof_slot(&e, kProfAttn, 0.0);
+    hipEvent_t ea = pe ? pe->a : nullptr, eb = pe ? pe->b : nullptr;
     switch (m.hd) {
-        case 32: k_attn<32><<<nblk, kAttnT, attn_lds(32), s>>>(a); break;
-        case 64: k_attn<64><<<nblk, kAttnT, attn_lds(64), s>>>(a); break;
-        case 128: k_attn<128><<<nblk, kAttnT, attn_lds(128), s>>>(a); break;
-        default: e.bad_launch = true; break;
+        case 32: hipExtLaunchKernelGGL(k_attn<32>, dim3(nblk), dim3(kAttnT), attn_lds(32), s, ea, eb, 0, a); break;
+        case 64: hipExtLaunchKernelGGL(k_attn<64>, dim3(nblk), dim3(kAttnT), attn_lds(64), s, ea, eb, 0, a); break;
+        case 128: hipExtLaunchKernelGGL(k_attn<128>, dim3(nblk), dim3(kAttnT), attn_lds(128), s, ea, eb, 0, a); break;
+        default: e.bad_launch = true; pe = nullptr; break;
     }
-    prof_end(&e);
+    if (pe) prof_commit(&e);
 }
 
 // Workgroups of the split-free attention grid for a launch shape (arrival counters needed).

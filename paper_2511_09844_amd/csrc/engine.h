@@ -114,6 +114,10 @@ struct Engine {
 // Bracket one launch with timing events when profiling is enabled (no-op otherwise).
 void prof_begin(Engine* e, int cls, double bytes);
 void prof_end(Engine* e);
+// For launches through hipExtLaunchKernelGGL: the next free entry (nullptr when not profiling);
+// its events are handed to the dispatch itself, so their span is the kernel's own execution.
+ProfEntry* prof_slot(Engine* e, int cls, double bytes);
+void prof_commit(Engine* e);
 
 size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm);
 

@@ -203,6 +203,19 @@ void prof_begin(Engine* e, int cls, double bytes) {
     (void)hipEventRecord(p.a, e->stream);
 }
 
+ProfEntry* prof_slot(Engine* e, int cls, double bytes) {
+    if (!e || !e->prof_on || e->prof_n >= kProfMax) return nullptr;
+    ProfEntry& p = e->prof[e->prof_n];
+    if (!p.a) return nullptr;
+    p.cls = cls;
+    p.bytes = bytes;
+    return &p;
+}
+
+void prof_commit(Engine* e) {
+    if (e && e->prof_on && e->prof_n < kProfMax) ++e->prof_n;
+}
+
 void prof_end(Engine* e) {
     if (!e || !e->prof_on || e->prof_n >= kProfMax) return;
     ProfEntry& p = e->prof[e->prof_n];

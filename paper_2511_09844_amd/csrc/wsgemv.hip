@@ -18,6 +18,8 @@
 // Epilogues: plain store (optional output-row map), residual add (+ per-16-column sums of
 // squares of the new residual, consumed by the next RMSNorm), SwiGLU on paired gate/up
 // tiles, and Q|K|V with rotate-half RoPE and the append of K and V to the cache.
+#include <hip/hip_ext.h>
+
 #include "device_common.h"
 #include "engine.h"
 
@@ -400,11 +402,14 @@ void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
         if (p.S) {
             dim3 grid(p.S * p.Gt);
             double wbytes = (double)tiles * 16 * subs * c.K * 2.0;
-            prof_begin(e, kProfGemv, wbytes + (double)M * c.K * 4.0 + (double)M * tiles * 16 * 4.0);
-#define SD2_WS_CASE(NWV, ST, SB)                                                   \
-    if (!launched && p.NW == NWV && p.steps == ST && subs == SB) {                  \
-        k_wsgemv<NWV, ST, SB><<<grid, NWV * 64, p.lds, s>>>(a);                     \
-        launched = true;                                                            \
+            ProfEntry* pe = prof_slot(e, kProfGemv, wbytes + (double)M * c.K * 4.0 + (double)M * tiles * 16 * 4.0);
+#define SD2_WS_CASE(NWV, ST, SB)                                                                     \
+    if (!launched && p.NW == NWV && p.steps == ST && subs == SB) {                                    \
+        if (pe)                                                                                       \
+            hipExtLaunchKernelGGL((k_wsgemv<NWV, ST, SB>), grid, dim3(NWV * 64), p.lds, s, pe->a, pe->b, 0, a); \
+        else                                                                                          \
+            k_wsgemv<NWV, ST, SB><<<grid, NWV * 64, p.lds, s>>>(a);                                   \
+        launched = true;                                                                              \
     }
 #define SD2_WS_STEPS8(NWV, SB)                                                    \
     SD2_WS_CASE(NWV, 1, SB) SD2_WS_CASE(NWV, 2, SB) SD2_WS_CASE(NWV, 3, SB) SD2_WS_CASE(NWV, 4, SB) \
@@ -414,7 +419,7 @@ void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
             SD2_WS_CASE(16, 1, 2) SD2_WS_CASE(16, 2, 2) SD2_WS_CASE(16, 3, 2) SD2_WS_CASE(16, 4, 2)
 #undef SD2_WS_STEPS8
 #undef SD2_WS_CASE
-            prof_end(e);
+            if (pe && launched) prof_commit(e);
         }
         if (!launched && e) e->bad_launch = true;
     }
