@@ -149,6 +149,13 @@ const char* sd2_last_error(sd2_handle_t h);
 #define SD2_DBG_STATE 7       /* int32 [batch][5]: t, len_verifier, len_drafter, produced, done */
 #define SD2_DBG_HIST 8        /* int32 [batch][max_seq_len]: committed tokens */
 #define SD2_DBG_HIDDEN_V 9    /* float [batch][k+1][d_verifier]: last verify pass's final-norm hidden states */
+#define SD2_DBG_PATH 10       /* int32 [2]: round execution path (0: one kernel per operation, 1: one persistent
+                                 launch per drafter step and per verify pass), and 1 if one of those launches
+                                 ever timed out at a grid barrier (its results are then invalid) */
+#define SD2_DBG_TRACE 11      /* int64 [33][1024]: persistent path, last profiled round, device clock
+                                 (100 MHz): entry 0 = start of launch j (0: verify pass, 1..k: drafter
+                                 steps), entry p+1 = end of its phase p; SD2_ERR_STATE when that path
+                                 is unavailable */
 
 /* Copy a debug buffer of the last round into host memory dst (bytes must match). */
 sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes);

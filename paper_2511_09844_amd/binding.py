@@ -15,7 +15,8 @@ P = ctypes.c_void_p
 
 SD2_OK = 0
 STATUS = {0: "ok", -1: "invalid argument", -2: "capacity", -3: "state", -4: "hip error", -5: "unsupported"}
-DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V = range(1, 10)
+DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V, DBG_PATH, \
+    DBG_TRACE = range(1, 12)
 
 EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
            "sd2_status_string", "sd2_last_error", "sd2_debug_read", "sd2_profile", "sd2_profile_read"]
@@ -196,6 +197,7 @@ class Engine:
             DBG_STEER: ((B, dD), np.float32), DBG_OWN_DRAFTS: ((B, k), np.int32), DBG_OWN_N: ((B,), np.int32),
             DBG_OWN_Y: ((B,), np.int32), DBG_STATE: ((B, 5), np.int32),
             DBG_HIST: ((B, self.cfg.max_seq_len), np.int32), DBG_HIDDEN_V: ((B, k + 1, dV), np.float32),
+            DBG_PATH: ((2,), np.int32), DBG_TRACE: ((33, 1024), np.int64),
         }
         shp, dt = shapes[what]
         out = np.zeros(shp, dtype=dt)

@@ -5,7 +5,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SO = os.path.join(HERE, "libsd2.so")
-SOURCES = ["csrc/kernels.hip", "csrc/wsgemv.hip", "csrc/attn.hip", "csrc/engine.hip"]
+SOURCES = ["csrc/kernels.hip", "csrc/wsgemv.hip", "csrc/attn.hip", "csrc/mk.hip", "csrc/engine.hip"]
 ARCH = "gfx950"
 
 

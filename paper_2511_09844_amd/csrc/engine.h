@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include "../../include/sd2.h"
+#include "mk.h"
 
 namespace sd2 {
 
@@ -106,9 +107,11 @@ struct Engine {
     int32_t* graph_out_tokens;
     int32_t* graph_out_counts;
     bool bad_launch;  // a projection shape had no kernel instance (reported as SD2_ERR_UNSUPPORTED)
+    hipError_t launch_err;  // failure of a launch call that returns an error (round-program path)
     bool prof_on;
     int prof_n;
     ProfEntry* prof;
+    MkState mk;  // persistent round-program path (used when active)
 };
 
 // Bracket one launch with timing events when profiling is enabled (no-op otherwise).
@@ -119,7 +122,8 @@ void prof_end(Engine* e);
 ProfEntry* prof_slot(Engine* e, int cls, double bytes);
 void prof_commit(Engine* e);
 
-size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm);
+size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm,
+             MkState* mk = nullptr);
 
 // ---- launchers (kernels.hip) ----
 void launch_rope_table(hipStream_t s, ModelDev& m, int cap);

@@ -80,7 +80,8 @@ void model_dims(ModelDev* m, const sd2_dims& d) {
 
 namespace sd2 {
 
-size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm_out) {
+size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, ModelDev* md, int* maxm_out,
+             MkState* mk) {
     Carver cv{base};
     int B = c.max_batch, k = c.k, cap = c.max_seq_len, V = c.verifier.vocab;
     int maxm = max_rows(c);
@@ -186,6 +187,23 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         m->x = cv.take<float>((size_t)maxm * d.d_model);
         m->ss = cv.take<float>((size_t)maxm * (d.d_model / 16));
     }
+    // persistent round-program path: phase lists, activation arena, barrier and hand-off state
+    {
+        MkState st{};
+        st.max_batch = mk_max_batch(c);
+        if (st.max_batch > 0) {
+            st.prog_cap = mk_phase_count(c);
+            st.prog = cv.take<MkPhase>((size_t)st.prog_cap);
+            st.arena = cv.take<char>(mk_arena_bytes(c, st.max_batch));
+            st.bar = cv.take<int32_t>(kMkBarInts);
+            st.err = cv.take<int32_t>(64);
+            st.cnt = cv.take<int32_t>(mk_counter_ints(c));
+            st.dummy = cv.take<uint16_t>(512);
+            st.ones = cv.take<uint16_t>(kMkMaxKR);
+            st.trace = cv.take<int64_t>((size_t)kMkMaxLaunch * kMkTracePhases);
+        }
+        if (mk) *mk = st;
+    }
     if (ws) *ws = w;
     return align_up(cv.off);
 }
@@ -234,6 +252,11 @@ sd2_status hip_fail(Engine* e, hipError_t err, const char* where) {
 }
 
 sd2_status check_launch(Engine* e, const char* where) {
+    if (e->launch_err != hipSuccess) {
+        hipError_t err = e->launch_err;
+        e->launch_err = hipSuccess;
+        return hip_fail(e, err, where);
+    }
     if (e->bad_launch) {
         snprintf(e->err, sizeof(e->err), "%s: no projection kernel instance for a shape", where);
         return SD2_ERR_UNSUPPORTED;
@@ -248,6 +271,19 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
     hipStream_t s = e.stream;
     e.prof_n = 0;
     int B = e.batch, k = e.cfg.k;
+    if (e.mk.active) {
+        // one persistent launch per drafter step and one for the verifier block
+        for (int j = 1; j <= k; ++j) {
+            hipError_t err = mk_launch(e, j);
+            if (err != hipSuccess) { e.launch_err = err; return; }
+            launch_draft_pick(s, e, j);
+        }
+        hipError_t err = mk_launch(e, 0);
+        if (err != hipSuccess) { e.launch_err = err; return; }
+        launch_verify_decide(s, e, out_tokens, out_counts);
+        launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
+        return;
+    }
     for (int j = 1; j <= k; ++j) {
         int rows = j == 1 ? 2 * B : B;
         launch_plan_embed(s, e, e.md, j == 1 ? kPlanDraft1 : kPlanDraftJ, j, rows, nullptr, nullptr, 0, 1);
@@ -273,7 +309,7 @@ void drop_graph(Engine& e) {
 sd2_status run_round(Engine* e, int32_t* out_tokens, int32_t* out_counts) {
     // Replay the recorded round when the shape and output buffers are unchanged.  Profiled rounds
     // are launched eagerly: HIP events recorded inside a captured graph cannot be timed.
-    if (!e->use_graph || e->prof_on) {
+    if (!e->use_graph || e->prof_on || e->mk.active) {
         enqueue_round(*e, out_tokens, out_counts);
         return check_launch(e, "round");
     }
@@ -351,7 +387,7 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
     e->w_steer = w_steer;
     // Graph replay needs a capturable (non-null) stream; SD2_NO_GRAPH=1 forces eager launches.
     e->use_graph = hip_stream != nullptr && getenv("SD2_NO_GRAPH") == nullptr;
-    carve(*cfg, (char*)workspace, &e->ws, &e->mv, &e->md, &e->maxm);
+    carve(*cfg, (char*)workspace, &e->ws, &e->mv, &e->md, &e->maxm, &e->mk);
     const sd2_weights* src[2] = {verifier, drafter};
     ModelDev* dst[2] = {&e->mv, &e->md};
     for (int i = 0; i < 2; ++i) {
@@ -369,6 +405,7 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
     launch_rope_table(e->stream, e->mv, e->cap);
     launch_rope_table(e->stream, e->md, e->cap);
     launch_init_maps(e->stream, *e);
+    mk_init_buffers(*e);
     sd2_status st = check_launch(e, "create");
     if (st != SD2_OK) {
         delete e;
@@ -404,6 +441,8 @@ sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, con
     launch_prefill_finish(s, *e, batch, tokens, lens, max_prompt);
     sd2_status st = check_launch(e, "prefill");
     if (st != SD2_OK) return st;
+    // rounds run as persistent launches when the shapes allow it (else as separate kernels)
+    mk_build(*e, batch);
     e->prefilled = true;
     return SD2_OK;
 }
@@ -508,12 +547,29 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
         case SD2_DBG_HIST: src = e->ws.hist; want = sizeof(int32_t) * (size_t)B * e->cap; break;
         case SD2_DBG_STATE: want = sizeof(int32_t) * (size_t)B * 5; break;
         case SD2_DBG_HIDDEN_V: src = e->ws.hidden_dbg; want = sizeof(float) * (size_t)B * (k + 1) * e->mv.dm.d_model; break;
+        case SD2_DBG_PATH: want = sizeof(int32_t) * 2; break;
+        case SD2_DBG_TRACE:
+            if (!e->mk.trace) return SD2_ERR_STATE;
+            src = e->mk.trace;
+            want = sizeof(int64_t) * (size_t)kMkMaxLaunch * kMkTracePhases;
+            break;
         default: return SD2_ERR_INVALID_ARG;
     }
     if (bytes != want) return SD2_ERR_INVALID_ARG;
+    if (what == SD2_DBG_PATH) {
+        int32_t* out = (int32_t*)dst_host;
+        out[0] = e->mk.active ? 1 : 0;
+        out[1] = 0;
+        if (e->mk.err) {
+            hipError_t err = hipStreamSynchronize(e->stream);
+            if (err == hipSuccess) err = hipMemcpy(&out[1], e->mk.err, sizeof(int32_t), hipMemcpyDeviceToHost);
+            if (err != hipSuccess) return hip_fail(e, err, "hipMemcpy");
+        }
+        return SD2_OK;
+    }
     if (what == SD2_DBG_HIDDEN_V) {
-        launch_rmsnorm_rows(e->stream, e->mv.x, B * (k + 1), e->mv.dm.d_model, e->mv.final_norm, e->bf16,
-                            e->mv.dm.rms_eps, e->ws.hidden_dbg);
+        launch_rmsnorm_rows(e->stream, e->mk.active ? e->mk.final_x : e->mv.x, B * (k + 1), e->mv.dm.d_model,
+                            e->mv.final_norm, e->bf16, e->mv.dm.rms_eps, e->ws.hidden_dbg);
         sd2_status st = check_launch(e, "debug_read");
         if (st != SD2_OK) return st;
     }

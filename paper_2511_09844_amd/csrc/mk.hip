@@ -1,0 +1,1006 @@
+// Persistent round-program kernel: one cooperative launch runs a whole drafter step (embedding
+// with the steering injection, every decoder layer, the LM head) or the verifier's (k+1)-row
+// block pass, as a fixed list of phases separated by grid barriers.
+//
+// Why: a decode step at batch 1 is a chain of ~80 dependent weight-streaming projections and
+// attention passes.  As separate kernels each pays the launch's own start/finish cost (several
+// microseconds on this part) plus a cold start of its loads; inside one persistent launch a
+// phase boundary is a grid barrier (about 2 us), descriptors are prefetched, and the weights of
+// a phase start streaming as soon as the barrier opens.
+//
+// Workgroups: one per compute unit, 8 waves; every weight load of a phase has returned before the
+// grid barrier, so the thread that runs it never waits behind weight traffic.
+//
+// Memory protocol (no device-scope fences: on this part a release fence writes back the whole
+// L2): every value one workgroup produces for another is written with device-scope
+// (write-through) stores and completed (s_waitcnt) before the producer counts in at a barrier
+// or a hand-off counter; consumers read it with ordinary loads.  That is safe because every
+// such buffer is written once per launch before anybody reads it (activations, residuals,
+// partials each get their own region per phase; cache rows are appended before they are read),
+// so no workgroup can hold a stale copy in its caches, which are invalidated at launch start.
+#include <hip/hip_ext.h>
+#include <math.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "device_common.h"
+#include "engine.h"
+#include "mk.h"
+
+namespace sd2 {
+
+typedef __bf16 mk_bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 mk_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float mk_f4 __attribute__((ext_vector_type(4)));
+typedef float mk_f2 __attribute__((ext_vector_type(2)));
+typedef unsigned int mk_u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int mk_u2 __attribute__((ext_vector_type(2)));
+// Global-address-space pointers: loads through generic pointers are "flat" and are also counted
+// by the LDS counter, which would make every LDS wait a wait on memory.
+typedef const __attribute__((address_space(1))) mk_u4* mk_gu4p;
+typedef const __attribute__((address_space(1))) mk_u2* mk_gu2p;
+typedef const __attribute__((address_space(1))) mk_f4* mk_gf4p;
+typedef const __attribute__((address_space(1))) float* mk_gfp;
+typedef const __attribute__((address_space(1))) int32_t* mk_gip;
+
+constexpr int kNW = kMkWaves;
+constexpr int kMkMinWG = 256;       // workgroups assumed by the LDS plans (one per compute unit)
+constexpr int kNT = kMkWaves * 64;  // streaming threads
+constexpr int kCtl = 0;             // thread that runs the grid barrier (no loads in flight there)
+constexpr long kMkSpin = 1L << 22;  // grid-barrier polls before a workgroup gives up (reports err)
+
+__device__ __forceinline__ int mk_ld(int32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ int mk_add(int32_t* p, int v) { return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ void mk_sti(int32_t* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ void mk_stf(float* p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ float mk_ldg(const float* p) { return *(mk_gfp)p; }
+__device__ __forceinline__ float4 mk_ldg4(const float* p) {
+    mk_f4 v = *(mk_gf4p)p;
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float mk_ldbf(const uint16_t* p) {
+    return bf16_to_f32(*(const __attribute__((address_space(1))) uint16_t*)p);
+}
+__device__ __forceinline__ int mk_ldi(const int32_t* p) { return *(mk_gip)p; }
+__device__ __forceinline__ uint32_t mk_ldu(const void* p) { return *(const __attribute__((address_space(1))) uint32_t*)p; }
+__device__ __forceinline__ void mk_vmwait() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+// Uniform copy of a value every lane holds identically (descriptor fields read from LDS): kept in
+// scalar registers instead of a stack copy of the whole descriptor.
+template <typename T>
+__device__ __forceinline__ T mk_uni(const T& v) {
+    static_assert(sizeof(T) % 4 == 0, "32-bit words");
+    uint32_t w[sizeof(T) / 4];
+    __builtin_memcpy(w, &v, sizeof(T));
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(T) / 4); ++i) w[i] = __builtin_amdgcn_readfirstlane(w[i]);
+    T r;
+    __builtin_memcpy(&r, w, sizeof(T));
+    return r;
+}
+
+// Row plan of the launch, one entry per activation row (position -1: inactive row).
+struct MkRows {
+    int pos[kMkMaxRows], seq[kMkMaxRows], tok[kMkMaxRows];
+};
+
+__device__ __forceinline__ void mk_plan(const MkArgs& a, MkRows& rp) {
+    const int r = threadIdx.x;
+    if (r >= kMkMaxRows) return;
+    int b = 0, pos = -1, tok = 0;
+    if (r < a.M) {
+        if (a.kind == 1) {
+            b = r / (a.k + 1);
+            const int i = r % (a.k + 1);
+            if (b < a.batch && !a.done[b]) {
+                const int t = a.t[b];
+                pos = t - 1 + i;
+                tok = i == 0 ? a.hist[(size_t)b * a.cap + t - 1] : a.drafts[b * a.k + i - 1];
+            }
+        } else if (a.j == 1) {
+            b = r >> 1;
+            const int i = r & 1;
+            if (b < a.batch && !a.done[b]) {
+                const int t = a.t[b], m = t - a.len_d[b];
+                if (i == 1) pos = t - 1;
+                else if (m == 2) pos = t - 2;
+                if (pos >= 0) tok = a.hist[(size_t)b * a.cap + pos];
+            }
+        } else {
+            b = r;
+            if (b < a.batch && !a.done[b]) {
+                pos = a.t[b] + a.j - 2;
+                tok = a.drafts[b * a.k + a.j - 2];
+            }
+        }
+    }
+    rp.pos[r] = pos;
+    rp.seq[r] = b < a.max_batch ? b : 0;
+    rp.tok[r] = tok < 0 ? 0 : (tok >= a.vocab ? a.vocab - 1 : tok);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Grid barrier.  Counters: one per XCD group (workgroup id mod 8), one global; the last arriver
+// of a group resets it and counts the group in; the last group resets the global counter and
+// publishes the next generation on 8 lines (one per group) that the control threads poll.  The
+// generation only grows, so no reset races with a poll.
+// ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ void mk_barrier(const MkArgs& a, int& gen, long& spins) {
+    __builtin_amdgcn_s_barrier();
+    if (threadIdx.x == kCtl) {
+        int32_t* base = a.bar;
+        const int x = blockIdx.x & 7;
+        const int ngroup = a.G < 8 ? a.G : 8;
+        const int per = a.G / 8 + (x < a.G % 8 ? 1 : 0);
+        const int prev = mk_add(base + (2 + x) * kMkLine, 1);
+        if (prev == per - 1) {
+            mk_sti(base + (2 + x) * kMkLine, 0);
+            mk_vmwait();
+            const int gp = mk_add(base + kMkLine, 1);
+            if (gp == ngroup - 1) {
+                mk_sti(base + kMkLine, 0);
+                mk_vmwait();
+                for (int i = 0; i < 8; ++i) mk_sti(base + (10 + i) * kMkLine, gen + 1);
+            }
+        }
+        gen += 1;
+        if (spins >= 0) {
+            while ((int)(mk_ld(base + (10 + x) * kMkLine) - gen) < 0) {
+                if (++spins > kMkSpin) {
+                    mk_sti(a.err, 1);
+                    spins = -1;  // give up waiting for the rest of the launch (results invalid)
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+    }
+    __builtin_amdgcn_s_barrier();
+}
+
+// ---------------------------------------------------------------------------------------------
+// Projection phase.
+// ---------------------------------------------------------------------------------------------
+struct MkBuf {
+    mk_u4 w[8][2];  // one weight unit per wave: 16 rows x 512 columns, MFMA B-operand layout
+};
+
+// Weight row streamed by lane row n of tile `tile` (Q|K|V tiles pair rotate-half partners
+// i and i + hd/2, 8 of each).
+struct MkW {
+    const uint16_t *w0, *w1, *w2;
+    int K, mode, nseg, st0, st1;
+};
+__device__ __forceinline__ const uint16_t* mk_row(const MkW& o, int hd, int tile, int sub, int n) {
+    if (o.mode == kEpiSwiglu) return (sub ? o.w1 : o.w0) + (size_t)(tile * 16 + n) * o.K;
+    int seg = 0, lt = tile;
+    if (o.nseg > 1 && lt >= o.st0) { lt -= o.st0; seg = 1; }
+    if (o.nseg > 2 && seg == 1 && lt >= o.st1) { lt -= o.st1; seg = 2; }
+    int wrow = lt * 16 + n;
+    if (o.mode == kEpiQkv) {
+        const int per_head = hd / 16;
+        const int h = lt / per_head, jj = lt % per_head;
+        wrow = h * hd + (n < 8 ? 8 * jj + n : hd / 2 + 8 * jj + (n - 8));
+    }
+    const uint16_t* base = seg == 0 ? o.w0 : (seg == 1 ? o.w1 : o.w2);
+    return base + (size_t)wrow * o.K;
+}
+
+__device__ __forceinline__ int mk_units(int tiles, int S, int subs, int G) {
+    const int gs = G / S, g = blockIdx.x / S;
+    const int nt = tiles > g ? (tiles - g + gs - 1) / gs : 0;
+    return nt * subs;
+}
+
+// stride 8 (16-byte words per 64 columns) for a real unit; 0 re-reads one word (absent unit)
+__device__ __forceinline__ void mk_issue(MkBuf& b, const uint16_t* wp, int stride) {
+    mk_gu4p p = (mk_gu4p)wp;
+#pragma unroll
+    for (int st = 0; st < 8; ++st) {
+        b.w[st][0] = p[st * stride];
+        b.w[st][1] = p[st * stride + (stride >> 3)];
+    }
+}
+
+// Embedding row value of activation row m, column c (+ steering for drafter launches).
+__device__ __forceinline__ float mk_embed_at(const MkArgs& a, const MkRows& rp, int m, int c) {
+    if (rp.pos[m] < 0) return 0.f;
+    float v = mk_ldbf(a.embed + (size_t)rp.tok[m] * a.d + c);
+    if (a.add_steer) v += mk_ldg(a.steer + (size_t)rp.seq[m] * a.d + c);
+    return v;
+}
+
+__device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, float* inv_rms,
+                        int* flags, int* last_flag) {
+    // descriptor fields (od lives in LDS), uniform
+    MkW ow;
+    ow.w0 = mk_uni(od.W[0]); ow.w1 = mk_uni(od.W[1]); ow.w2 = mk_uni(od.W[2]);
+    ow.K = mk_uni(od.K); ow.mode = mk_uni(od.mode); ow.nseg = mk_uni(od.nseg);
+    ow.st0 = mk_uni(od.seg_tiles[0]); ow.st1 = mk_uni(od.seg_tiles[1]);
+    const int oK = ow.K, omode = ow.mode, otiles = mk_uni(od.tiles), oS = mk_uni(od.S), oKR = mk_uni(od.KR);
+    const int owpu = mk_uni(od.wpu), osubs = mk_uni(od.subs), oxsrc = mk_uni(od.xsrc);
+    const float* oX = mk_uni(od.X);
+    const uint16_t* ogamma = mk_uni(od.gamma);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = a.G, M = a.M;
+    const int s = blockIdx.x % oS, g = blockIdx.x / oS, gs = G / oS;
+    const int k0 = s * oKR, KR = oKR, ldk = KR + 8;
+    const int nsub = mk_units(otiles, oS, osubs, G);
+    if (nsub == 0) return;
+    uint16_t* xh = (uint16_t*)smem;
+    uint16_t* xl = xh + (size_t)M * ldk;
+    float* red = (float*)(xl + (size_t)M * ldk);  // [2][8][256] wave partial tiles
+    float* res = red + 2 * kNW * 256;             // [nsub][256] reduced tiles
+    const int n = lane & 15, q = lane >> 4;
+    const int wpu = owpu, groups = kNW / wpu, gr = wave / wpu;
+    const bool streams = wave < kNW && gr < groups;
+    const int kw0 = (wave % wpu) * 512;
+    const int nround = (nsub + groups - 1) / groups;
+    auto uptr = [&](int r) -> const uint16_t* {
+        const int u = r * groups + gr;
+        if (!(streams && u < nsub)) return a.dummy + lane * 8;
+        const int tile = g + (osubs == 2 ? (u >> 1) : u) * gs;
+        return mk_row(ow, a.hd, tile, osubs == 2 ? (u & 1) : 0, n) + k0 + kw0 + 16 * q;
+    };
+    auto ustride = [&](int r) { const int u = r * groups + gr; return (streams && u < nsub) ? 8 : 0; };
+    MkBuf bf;
+    // The first weight unit is requested before anything else; activation rows follow.
+    if (wave < kNW) mk_issue(bf, uptr(0), ustride(0));
+    asm volatile("" ::: "memory");
+    // Norm gain slice (one 16-byte word per thread) into LDS, in the reduction area.
+    uint16_t* gl = (uint16_t*)red;
+    float* ssq = red + 2048;  // [kMkMaxRows][8] wave partials of the rows' sums of squares
+    // gain of this K-range (the ones vector, which covers one whole range, when there is no norm)
+    const uint16_t* gam = ogamma ? ogamma + k0 : a.ones;
+    mk_u4 gword = {0, 0, 0, 0};
+    if (tid * 8 < KR) gword = *(mk_gu4p)(gam + tid * 8);
+    if (tid * 8 < KR) *(mk_u4*)(gl + tid * 8) = gword;
+    __syncthreads();
+    // Stage rows in passes of four: x (times the gain) as a bf16 hi/lo pair in LDS.
+    const int n4 = KR / 4;
+    for (int m0 = 0; m0 < M; m0 += 4) {
+        float4 xv[4][2];
+#pragma unroll
+        for (int mm = 0; mm < 4; ++mm)
+#pragma unroll
+            for (int jc = 0; jc < 2; ++jc) {
+                const int m = m0 + mm, c = tid + 512 * jc;
+                xv[mm][jc] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (m < M && tid < kNT && c < n4) {
+                    if (oxsrc == kMkXEmbed) {
+                        const int cc = k0 + 4 * c;
+                        xv[mm][jc] = make_float4(mk_embed_at(a, rp, m, cc), mk_embed_at(a, rp, m, cc + 1),
+                                                 mk_embed_at(a, rp, m, cc + 2), mk_embed_at(a, rp, m, cc + 3));
+                    } else {
+                        xv[mm][jc] = mk_ldg4(oX + (size_t)m * oK + k0 + 4 * c);
+                    }
+                }
+            }
+#pragma unroll
+        for (int mm = 0; mm < 4; ++mm) {
+            const int m = m0 + mm;
+            if (m >= M) break;
+            float sq = 0.f;
+#pragma unroll
+            for (int jc = 0; jc < 2; ++jc) {
+                const int c = tid + 512 * jc;
+                if (tid < kNT && c < n4) {
+                    const float4 v = xv[mm][jc];
+                    const uint2 gw = *(const uint2*)(gl + 4 * c);
+                    const mk_f2 a0 = {v.x * __uint_as_float(gw.x << 16), v.y * __uint_as_float(gw.x & 0xffff0000u)};
+                    const mk_f2 a1 = {v.z * __uint_as_float(gw.y << 16), v.w * __uint_as_float(gw.y & 0xffff0000u)};
+                    const mk_bf16x2 h0 = __builtin_convertvector(a0, mk_bf16x2), h1 = __builtin_convertvector(a1, mk_bf16x2);
+                    const mk_bf16x2 l0 = __builtin_convertvector(a0 - __builtin_convertvector(h0, mk_f2), mk_bf16x2);
+                    const mk_bf16x2 l1 = __builtin_convertvector(a1 - __builtin_convertvector(h1, mk_f2), mk_bf16x2);
+                    *(uint2*)(xh + (size_t)m * ldk + 4 * c) =
+                        make_uint2(__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1));
+                    *(uint2*)(xl + (size_t)m * ldk + 4 * c) =
+                        make_uint2(__builtin_bit_cast(uint32_t, l0), __builtin_bit_cast(uint32_t, l1));
+                    sq += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+                }
+            }
+            sq = wave_sum(sq);
+            if (lane == 0 && wave < kNW) ssq[m * kNW + wave] = sq;
+        }
+    }
+    __syncthreads();
+    if (tid < M) {
+        float tsum = 0.f;
+        for (int ww = 0; ww < kNW; ++ww) tsum += ssq[tid * kNW + ww];
+        inv_rms[tid] = ogamma ? rsqrtf(tsum / (float)oK + a.eps) : 1.0f;
+    }
+    __syncthreads();
+
+    // ---- streaming loop: one unit per wave in flight, partial tiles summed every two rounds ----
+    const int arow = n < M ? n : M - 1;  // rows >= M repeat row M-1; their outputs are discarded
+    const uint16_t* ahp = xh + (size_t)arow * ldk + kw0 + 16 * q;
+    const uint16_t* alp = xl + (size_t)arow * ldk + kw0 + 16 * q;
+    auto mma = [&]() {
+        mk_f4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = acc;
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const mk_bf16x8 ah = *(const mk_bf16x8*)(ahp + st * 64 + 8 * h);
+                const mk_bf16x8 al = *(const mk_bf16x8*)(alp + st * 64 + 8 * h);
+                const mk_bf16x8 b = __builtin_bit_cast(mk_bf16x8, bf.w[st][h]);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc, 0, 0, 0);
+                acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc2, 0, 0, 0);
+            }
+        return acc + acc2;
+    };
+    auto put = [&](const mk_f4& v, int slot) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[(slot * kNW + wave) * 256 + (4 * q + r) * 16 + n] = v[r];
+    };
+    auto reduce = [&](int r0, int nr) {
+        __syncthreads();
+        for (int e = tid; e < nr * groups * 256 && tid < kNT; e += kNT) {
+            const int i = e / (groups * 256), gg = (e / 256) % groups, c = e & 255;
+            const int u = (r0 + i) * groups + gg;
+            if (u < nsub) {
+                float x = 0.f;
+                for (int ww = 0; ww < wpu; ++ww) x += red[(i * kNW + gg * wpu + ww) * 256 + c];
+                res[u * 256 + c] = x * inv_rms[c >> 4];
+            }
+        }
+        __syncthreads();
+    };
+    int r = 0;
+    for (; r + 1 < nround; ++r) {
+        mk_f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if (wave < kNW) acc = mma();
+        if (wave < kNW) mk_issue(bf, uptr(r + 1), ustride(r + 1));
+        if (wave < kNW) put(acc, r & 1);
+        if (r & 1) reduce(r - 1, 2);
+    }
+    {
+        mk_f4 acc = {0.f, 0.f, 0.f, 0.f};
+        if (wave < kNW) acc = mma();
+        if (wave < kNW) put(acc, r & 1);
+    }
+    if (r & 1) reduce(r - 1, 2);
+    else reduce(r, 1);
+
+    // ---- epilogue: element (m, c) of a tile is held by thread 16 m + c of the first 256 ----
+    const int em = tid >> 4, ec = tid & 15;
+    const int ntile = nsub / osubs;
+    const int oldy = mk_uni(od.ldy), ores_embed = mk_uni(od.res_embed), olayer = mk_uni(od.layer);
+    float* oY = mk_uni(od.Y);
+    float* oss_out = mk_uni(od.ss_out);
+    const float* oxres = mk_uni(od.xres);
+    const int32_t* oout_map = mk_uni(od.out_map);
+    float* oqout = mk_uni(od.qout);
+    auto epilogue = [&](int tile, float v0, float v1) {
+        // every thread of the first 256 calls this (sums of squares need whole 16-lane groups)
+        const bool valid = em < M;
+        if (omode == kEpiStore) {
+            if (valid) {
+                const int orow = oout_map ? mk_ldi(oout_map + em) : em;
+                if (orow >= 0) mk_stf(oY + (size_t)orow * oldy + tile * 16 + ec, v0);
+            }
+        } else if (omode == kEpiAdd) {
+            float nv = 0.f;
+            if (valid) {
+                const int col = tile * 16 + ec;
+                const float res0 = ores_embed ? mk_embed_at(a, rp, em, col) : mk_ldg(oxres + (size_t)em * oldy + col);
+                nv = res0 + v0;
+                mk_stf(oY + (size_t)em * oldy + col, nv);
+            }
+            if (oss_out) {
+                float sq = nv * nv;
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) sq += __shfl_xor(sq, off, 16);
+                if (valid && ec == 0) mk_stf(oss_out + (size_t)em * (oldy / 16) + tile, sq);
+            }
+        } else if (omode == kEpiSwiglu) {
+            if (valid) mk_stf(oY + (size_t)em * oldy + tile * 16 + ec, silu(v0) * v1);
+        } else {  // Q|K|V: rotate-half RoPE on Q and K, cache append of K and V
+            const float partner = __shfl_xor(v0, 8, 16);
+            if (!valid) return;
+            int seg = 0, lt = tile;
+            if (lt >= ow.st0) { lt -= ow.st0; seg = 1; }
+            if (seg == 1 && lt >= ow.st1) { lt -= ow.st1; seg = 2; }
+            const int per_head = a.hd / 16, half = a.hd / 2;
+            const int h = lt / per_head, jj = lt % per_head;
+            const int i = 8 * jj + (ec & 7);
+            const int dim = ec < 8 ? i : half + i;
+            const int pos = rp.pos[em];
+            float out = v0;
+            if (seg < 2) {
+                const int pp = pos < 0 ? 0 : pos;
+                const float c = mk_ldg(a.rcos + (size_t)pp * half + i), sn = mk_ldg(a.rsin + (size_t)pp * half + i);
+                out = ec < 8 ? v0 * c - partner * sn : v0 * c + partner * sn;
+            }
+            if (seg == 0) {
+                mk_stf(oqout + (size_t)em * a.H * a.hd + h * a.hd + dim, out);
+            } else if (pos >= 0) {
+                const size_t idx =
+                    ((((size_t)olayer * a.max_batch + rp.seq[em]) * a.Hkv + h) * a.cap + pos) * a.hd + dim;
+                mk_stf(seg == 1 ? a.kc + idx : a.vc + idx, out);
+            }
+        }
+    };
+    if (oS == 1) {
+        for (int jt = 0; jt < ntile; ++jt) {
+            const int tile = g + jt * gs;
+            if (tid < 256) {
+                const float v0 = res[(jt * osubs) * 256 + tid];
+                const float v1 = osubs == 2 ? res[(jt * 2 + 1) * 256 + tid] : v0;
+                epilogue(tile, v0, v1);
+            }
+        }
+        return;
+    }
+    // K split over S workgroups: partial tiles, one hand-off for all of this workgroup's tiles
+    float* opart = mk_uni(od.part);
+    int32_t* ocnt = mk_uni(od.cnt);
+    for (int jt = 0; jt < ntile; ++jt) {
+        const int tile = g + jt * gs;
+        float* pt = opart + ((size_t)tile * oS + s) * osubs * 256;
+        if (tid < 256)
+            for (int sb = 0; sb < osubs; ++sb) mk_stf(pt + sb * 256 + tid, res[(jt * osubs + sb) * 256 + tid]);
+    }
+    mk_vmwait();
+    __syncthreads();
+    if (tid < ntile) {
+        const int tile = g + tid * gs;
+        const int prev = mk_add(ocnt + tile, 1);
+        flags[tid] = prev == oS - 1;
+        if (prev == oS - 1) mk_sti(ocnt + tile, 0);
+    }
+    __syncthreads();
+    (void)last_flag;
+    for (int jt = 0; jt < ntile; ++jt) {
+        if (!flags[jt]) continue;
+        const int tile = g + jt * gs;
+        const float* pt = opart + (size_t)tile * oS * osubs * 256;
+        if (tid < 256) {
+            // all S partials are requested before any is added (one memory round trip)
+            float p0[8], p1[8];
+#pragma unroll
+            for (int s0 = 0; s0 < 8; ++s0) {
+                p0[s0] = s0 < oS ? mk_ldg(pt + (size_t)s0 * osubs * 256 + tid) : 0.f;
+                p1[s0] = (s0 < oS && osubs == 2) ? mk_ldg(pt + (size_t)s0 * osubs * 256 + 256 + tid) : 0.f;
+            }
+            float v0 = 0.f, v1 = 0.f;
+#pragma unroll
+            for (int s0 = 0; s0 < 8; ++s0) {
+                v0 += p0[s0];
+                v1 += p1[s0];
+            }
+            epilogue(tile, v0, osubs == 2 ? v1 : v0);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Attention phase: units (sequence, KV head, span of kMkSpan positions).  A unit scores all
+// query vectors of the sequence's rows for the KV head's query heads against its span (one wave
+// per query vector, one lane per position), writes an un-normalised partial (output, max, sum),
+// and the last span of a (sequence, KV head) to arrive merges all live spans in span order.
+// Positions beyond the longest query row of the sequence are never loaded.
+// ---------------------------------------------------------------------------------------------
+template <int HD>
+__device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, int* last_flag) {
+    struct {
+        int nsplit, layer;
+        const float* qout;
+        float *aout, *apart;
+        int32_t* cnt;
+    } o;
+    o.nsplit = mk_uni(od.nsplit);
+    o.layer = mk_uni(od.layer);
+    o.qout = mk_uni(od.qout);
+    o.aout = mk_uni(od.aout);
+    o.apart = mk_uni(od.apart);
+    o.cnt = mk_uni(od.cnt);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nwaves = kMkThreads / 64;
+    const int Gq = a.H / a.Hkv;
+    const int nq = a.rps * Gq;
+    const int nseq = a.M / a.rps;
+    const int nunit = nseq * a.Hkv * o.nsplit;
+    float* qs = (float*)smem;                 // [nq][HD]   pre-scaled queries
+    float* ks = qs + kMkMaxNq * HD;           // [64][HD+4]
+    float* vs = ks + kMkSpan * (HD + 4);      // [64][HD]
+    float* ps = vs + kMkSpan * HD;            // [nq][64]   probabilities
+    float* mq = ps + kMkMaxNq * kMkSpan;      // [nq] span max
+    float* lq = mq + kMkMaxNq;                // [nq] span sum
+    for (int u = blockIdx.x; u < nunit; u += a.G) {
+        const int sp = u % o.nsplit;
+        const int kvh = (u / o.nsplit) % a.Hkv;
+        const int sq = u / (o.nsplit * a.Hkv);
+        int maxq = -1;
+        for (int i = 0; i < a.rps; ++i) maxq = max(maxq, rp.pos[sq * a.rps + i]);
+        const int p0 = sp * kMkSpan;
+        const int nvalid = maxq >= p0 ? min(kMkSpan, maxq - p0 + 1) : 0;
+        if (nvalid > 0) {
+            const size_t head_base = (((size_t)o.layer * a.max_batch + rp.seq[sq * a.rps]) * a.Hkv + kvh) * a.cap * HD;
+            const float* kg = a.kc + head_base + (size_t)p0 * HD;
+            const float* vg = a.vc + head_base + (size_t)p0 * HD;
+            // K and V rows of the span (rows past the last valid one re-read it; masked below)
+            for (int e4 = tid; e4 < kMkSpan * HD / 4; e4 += kMkThreads) {
+                const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
+                const int jj = j < nvalid ? j : nvalid - 1;
+                const float4 kv = mk_ldg4(kg + (size_t)jj * HD + d);
+                const float4 vv = mk_ldg4(vg + (size_t)jj * HD + d);
+                *(float4*)(ks + j * (HD + 4) + d) = kv;
+                *(float4*)(vs + j * HD + d) = vv;
+            }
+            for (int e = tid; e < nq * HD; e += kMkThreads) {
+                const int qi = e / HD, d = e % HD;
+                const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
+                qs[e] = mk_ldg(o.qout + (size_t)row * a.H * HD + h * HD + d) * a.scale;
+            }
+            __syncthreads();
+            // scores: one wave per query vector, one lane per position
+            for (int qi = wave; qi < nq; qi += nwaves) {
+                const int row = sq * a.rps + qi / Gq;
+                const int qp = rp.pos[row];
+                float sc = -INFINITY;
+                if (lane < nvalid && p0 + lane <= qp) {
+                    const float4* qr = (const float4*)(qs + qi * HD);
+                    const float4* kr = (const float4*)(ks + lane * (HD + 4));
+                    float d0 = 0.f, d1 = 0.f;
+#pragma unroll 8
+                    for (int d4 = 0; d4 < HD / 4; ++d4) {
+                        const float4 qv = qr[d4], kv = kr[d4];
+                        d0 += qv.x * kv.x + qv.z * kv.z;
+                        d1 += qv.y * kv.y + qv.w * kv.w;
+                    }
+                    sc = d0 + d1;
+                }
+                const float mx = wave_max(sc);
+                const float p = sc == -INFINITY ? 0.f : expf(sc - mx);
+                const float sm = wave_sum(p);
+                ps[qi * kMkSpan + lane] = p;
+                if (lane == 0) { mq[qi] = mx; lq[qi] = sm; }
+            }
+            __syncthreads();
+            // un-normalised outputs of the span
+            for (int e = tid; e < nq * HD; e += kMkThreads) {
+                const int qi = e / HD, d = e % HD;
+                const float* pr = ps + qi * kMkSpan;
+                float acc = 0.f;
+#pragma unroll 8
+                for (int j = 0; j < kMkSpan; ++j) acc += pr[j] * vs[j * HD + d];
+                const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
+                float* pp = o.apart + (((size_t)row * a.H + h) * o.nsplit + sp) * (HD + 2);
+                mk_stf(pp + d, acc);
+                if (d == 0) {
+                    mk_stf(pp + HD, mq[qi]);
+                    mk_stf(pp + HD + 1, lq[qi]);
+                }
+            }
+        }
+        // count in; the last span of this (sequence, KV head) merges the live spans
+        mk_vmwait();
+        __syncthreads();
+        if (tid == 0) {
+            int32_t* c = o.cnt + sq * a.Hkv + kvh;
+            const int prev = mk_add(c, 1);
+            *last_flag = prev == o.nsplit - 1;
+            if (prev == o.nsplit - 1) mk_sti(c, 0);
+        }
+        __syncthreads();
+        if (*last_flag) {
+            const int nlive = maxq >= 0 ? min(o.nsplit, maxq / kMkSpan + 1) : 0;
+            for (int e = tid; e < nq * HD; e += kMkThreads) {
+                const int qi = e / HD, d = e % HD;
+                const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
+                float resv = 0.f;
+                if (rp.pos[row] >= 0) {
+                    const float* pp = o.apart + ((size_t)row * a.H + h) * o.nsplit * (HD + 2);
+                    // spans are merged 16 at a time: every partial of a group is requested before
+                    // any is used, and the running (max, sum, output) is rescaled per group
+                    float Mx = -INFINITY, L = 0.f, O = 0.f;
+                    for (int s0 = 0; s0 < nlive; s0 += 16) {
+                        float mv[16], lv[16], ov[16];
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const float* e2 = pp + (size_t)(s0 + i) * (HD + 2);
+                            const bool live = s0 + i < nlive;
+                            mv[i] = live ? mk_ldg(e2 + HD) : -INFINITY;
+                            lv[i] = live ? mk_ldg(e2 + HD + 1) : 0.f;
+                            ov[i] = live ? mk_ldg(e2 + d) : 0.f;
+                        }
+                        float cm = -INFINITY;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) cm = fmaxf(cm, mv[i]);
+                        if (cm == -INFINITY) continue;
+                        if (cm > Mx) {
+                            const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
+                            L *= sc;
+                            O *= sc;
+                            Mx = cm;
+                        }
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            if (mv[i] == -INFINITY) continue;
+                            const float w = expf(mv[i] - Mx);
+                            L += w * lv[i];
+                            O += w * ov[i];
+                        }
+                    }
+                    resv = L > 0.f ? O / L : 0.f;
+                }
+                mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, resv);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ MkPhase op_lds[2];
+    __shared__ MkRows rp;
+    __shared__ float inv_rms[kMkMaxRows];
+    __shared__ int flags[64];
+    __shared__ int last_flag;
+    __shared__ int gen0;
+    constexpr int kWords = (int)(sizeof(MkPhase) / 4);
+    static_assert(sizeof(MkPhase) % 4 == 0 && kWords <= 64, "phase descriptor larger than one wave");
+    mk_plan(a, rp);
+    if (threadIdx.x < kWords) ((uint32_t*)&op_lds[0])[threadIdx.x] = mk_ldu((const uint32_t*)&a.prog[0] + threadIdx.x);
+    if (threadIdx.x == kCtl) gen0 = mk_ld(a.bar + 10 * kMkLine + (blockIdx.x & 7) * kMkLine);
+    __syncthreads();
+    int gen = gen0;
+    long spins = 0;
+    if (a.trace && blockIdx.x == 0 && threadIdx.x == kCtl) a.trace[0] = wall_clock64();
+    for (int p = 0; p < a.nphase; ++p) {
+        // this phase's descriptor stays in LDS; the phase reads the fields it needs
+        const MkPhase& o = op_lds[p & 1];
+        const int op = mk_uni(o.op);
+        // the next descriptor is requested now and reaches LDS after the phase
+        uint32_t nw = 0;
+        if (threadIdx.x < kWords && p + 1 < a.nphase) nw = mk_ldu((const uint32_t*)&a.prog[p + 1] + threadIdx.x);
+        if (op == kMkGemv) {
+            mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag);
+        } else if (op == kMkAttn) {
+            if (a.hd == 64) mk_attn_t<64>(a, o, rp, smem, &last_flag);
+            else if (a.hd == 128) mk_attn_t<128>(a, o, rp, smem, &last_flag);
+            else mk_attn_t<32>(a, o, rp, smem, &last_flag);
+        }
+        mk_vmwait();  // this phase's stores are complete before the workgroup counts in
+        if (threadIdx.x < kWords && p + 1 < a.nphase) ((uint32_t*)&op_lds[(p + 1) & 1])[threadIdx.x] = nw;
+        if (p + 1 < a.nphase) mk_barrier(a, gen, spins);
+        if (a.trace && blockIdx.x == 0 && threadIdx.x == kCtl && p + 1 < kMkTracePhases) a.trace[p + 1] = wall_clock64();
+    }
+}
+
+// =============================================================================================
+// Host side: phase lists.
+// =============================================================================================
+namespace {
+
+size_t up256(size_t x) { return (x + 255) / 256 * 256; }
+
+struct MkPlanG {
+    int S, KR, wpu;
+    size_t lds;
+};
+
+// Split of K for a projection of M rows: smallest S with K-range KR a multiple of 512 up to
+// kMkMaxKR (8 waves x 512 columns), the staged rows in LDS, and no split for normed inputs
+// (their row statistics come from the whole staged row).
+MkPlanG mk_plan_gemv(int M, int N, int K, bool norm, int subs) {
+    MkPlanG p{0, 0, 0, 0};
+    for (int S = 1; S <= 8; S *= 2) {
+        if (norm && S > 1) break;
+        if (K % S) continue;
+        const int KR = K / S;
+        if (KR % 512 || KR > kMkMaxKR) continue;
+        const int tiles = N / 16;
+        const size_t units = (size_t)((tiles * S + kMkMinWG - 1) / kMkMinWG) * subs;  // per workgroup
+        const size_t lds = (size_t)M * (KR + 8) * 4 + 2 * kNW * 256 * 4 + units * 1024;
+        if (lds > (size_t)kMkLdsBudget) continue;
+        p.S = S;
+        p.KR = KR;
+        p.wpu = KR / 512;
+        p.lds = lds;
+        return p;
+    }
+    return p;
+}
+
+size_t mk_attn_lds(int hd) {
+    return sizeof(float) * ((size_t)kMkMaxNq * hd + (size_t)kMkSpan * (hd + 4) + (size_t)kMkSpan * hd +
+                            (size_t)kMkMaxNq * kMkSpan + 2 * kMkMaxNq);
+}
+
+struct Arena {
+    char* base;
+    size_t off;
+    template <typename T>
+    T* take(size_t n) {
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off += up256(n * sizeof(T));
+        return p;
+    }
+};
+
+int mk_nsplit(int cap) { return (cap + kMkSpan - 1) / kMkSpan; }
+
+// Phases of one launch of model m with M rows (rps per sequence); appends to `out` when given.
+// Returns false when a shape is not supported.  `lds` receives the largest dynamic LDS.
+bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int rps, int j, int G, Arena& ar,
+               const Workspace* ws, std::vector<MkPhase>* out, size_t* lds, int32_t* cnt, float** final_x,
+               float** final_ss, double* bytes_out = nullptr) {
+    double bytes = 0.0;
+    const sd2_dims& d = m.dm;
+    const int hd = d.d_model / d.n_heads;
+    const int L = d.n_layers, H = d.n_heads, Hkv = d.n_kv_heads, F = d.d_ff, dm = d.d_model;
+    if (M > kMkMaxRows || M < 1) return false;
+    if (rps * (H / Hkv) > kMkMaxNq) return false;
+    if (hd != 32 && hd != 64 && hd != 128) return false;
+    const int nsplit = mk_nsplit(c.max_seq_len);
+    size_t mx = mk_attn_lds(hd);
+    auto gemv = [&](int mode, int N, int K, const void* gamma, bool norm, int subs, MkPhase& ph) -> bool {
+        MkPlanG pl = mk_plan_gemv(M, N, K, norm, subs);
+        if (!pl.S || (G > 0 && G % pl.S)) return false;
+        ph.op = kMkGemv;
+        ph.mode = mode;
+        ph.K = K;
+        ph.tiles = N / 16;
+        ph.S = pl.S;
+        ph.KR = pl.KR;
+        ph.wpu = pl.wpu;
+        ph.subs = subs;
+        ph.gamma = (const uint16_t*)gamma;
+        ph.cnt = cnt;
+        if (pl.S > 1) ph.part = ar.take<float>((size_t)ph.tiles * pl.S * subs * 256);
+        mx = std::max(mx, pl.lds);
+        bytes += (double)ph.tiles * 16 * K * 2.0 * subs;
+        return N % 16 == 0;
+    };
+    const void* const* W = m.layer;
+    float* x_prev = nullptr;  // null: the embedding rows (+ steering)
+    for (int l = 0; l < L; ++l) {
+        const void* const* Wl = W + (size_t)l * 9;
+        float* q = ar.take<float>((size_t)M * H * hd);
+        float* att = ar.take<float>((size_t)M * H * hd);
+        float* xa = ar.take<float>((size_t)M * dm);
+        float* hbuf = ar.take<float>((size_t)M * F);
+        float* xf = ar.take<float>((size_t)M * dm);
+        float* apart = ar.take<float>((size_t)M * H * nsplit * (hd + 2));
+        float* ss = (l == L - 1) ? ar.take<float>((size_t)M * (dm / 16)) : nullptr;
+        MkPhase qkv{};
+        if (!gemv(kEpiQkv, (H + 2 * Hkv) * hd, dm, Wl[kAttnNorm], true, 1, qkv)) return false;
+        qkv.nseg = 3;
+        qkv.W[0] = (const uint16_t*)Wl[kWq];
+        qkv.W[1] = (const uint16_t*)Wl[kWk];
+        qkv.W[2] = (const uint16_t*)Wl[kWv];
+        qkv.seg_tiles[0] = H * hd / 16;
+        qkv.seg_tiles[1] = Hkv * hd / 16;
+        qkv.seg_tiles[2] = Hkv * hd / 16;
+        qkv.xsrc = x_prev ? kMkXBuf : kMkXEmbed;
+        qkv.X = x_prev;
+        qkv.qout = q;
+        qkv.layer = l;
+        MkPhase at{};
+        at.op = kMkAttn;
+        at.layer = l;
+        at.nsplit = nsplit;
+        at.qout = q;
+        at.aout = att;
+        at.apart = apart;
+        at.cnt = cnt;
+        MkPhase o{};
+        if (!gemv(kEpiAdd, dm, H * hd, nullptr, false, 1, o)) return false;
+        o.nseg = 1;
+        o.W[0] = (const uint16_t*)Wl[kWo];
+        o.X = att;
+        o.xres = x_prev;
+        o.res_embed = x_prev ? 0 : 1;
+        o.Y = xa;
+        o.ldy = dm;
+        MkPhase gu{};
+        if (!gemv(kEpiSwiglu, F, dm, Wl[kFfnNorm], true, 2, gu)) return false;
+        gu.nseg = 1;
+        gu.W[0] = (const uint16_t*)Wl[kWg];
+        gu.W[1] = (const uint16_t*)Wl[kWu];
+        gu.X = xa;
+        gu.Y = hbuf;
+        gu.ldy = F;
+        MkPhase dn{};
+        if (!gemv(kEpiAdd, dm, F, nullptr, false, 1, dn)) return false;
+        dn.nseg = 1;
+        dn.W[0] = (const uint16_t*)Wl[kWd];
+        dn.X = hbuf;
+        dn.xres = xa;
+        dn.Y = xf;
+        dn.ldy = dm;
+        dn.ss_out = ss;
+        if (out) {
+            out->push_back(qkv);
+            out->push_back(at);
+            out->push_back(o);
+            out->push_back(gu);
+            out->push_back(dn);
+        }
+        x_prev = xf;
+        if (l == L - 1) {
+            if (final_x) *final_x = xf;
+            if (final_ss) *final_ss = ss;
+        }
+    }
+    MkPhase lm{};
+    if (!gemv(kEpiStore, d.vocab, dm, m.final_norm, true, 1, lm)) return false;
+    lm.nseg = 1;
+    lm.W[0] = (const uint16_t*)m.lm_head;
+    lm.gamma = (const uint16_t*)m.final_norm;
+    lm.X = x_prev;
+    lm.ldy = d.vocab;
+    if (ws) {
+        lm.Y = verifier ? ws->logits_v : ws->logits_d;
+        lm.out_map = verifier ? nullptr : ws->lm_map_d + (size_t)(j - 1) * 2 * c.max_batch;
+    }
+    if (out) out->push_back(lm);
+    if (lds) *lds = std::max(*lds, mx);
+    if (bytes_out) *bytes_out = bytes;
+    return true;
+}
+
+}  // namespace
+
+// Largest batch for which both launch kinds are supported (0: none).
+int mk_max_batch(const sd2_config& c) {
+    if (c.dtype != SD2_BF16) return 0;
+    ModelDev mv{}, md{};
+    mv.dm = c.verifier;
+    md.dm = c.drafter;
+    for (int b = std::min(c.max_batch, kMkMaxRows); b >= 1; --b) {
+        Arena ar{nullptr, 0};
+        if (mk_record(c, md, false, 2 * b, 2, 1, 0, ar, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr) &&
+            mk_record(c, md, false, b, 1, 2, 0, ar, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr) &&
+            mk_record(c, mv, true, b * (c.k + 1), c.k + 1, 0, 0, ar, nullptr, nullptr, nullptr, nullptr, nullptr,
+                      nullptr))
+            return b;
+    }
+    return 0;
+}
+
+size_t mk_arena_bytes(const sd2_config& c, int batch) {
+    if (batch < 1) return 0;
+    ModelDev mv{}, md{};
+    mv.dm = c.verifier;
+    md.dm = c.drafter;
+    size_t mx = 0;
+    {
+        Arena ar{nullptr, 0};
+        mk_record(c, md, false, 2 * batch, 2, 1, 0, ar, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+        mx = std::max(mx, ar.off);
+    }
+    {
+        Arena ar{nullptr, 0};
+        mk_record(c, mv, true, batch * (c.k + 1), c.k + 1, 0, 0, ar, nullptr, nullptr, nullptr, nullptr, nullptr,
+                  nullptr);
+        mx = std::max(mx, ar.off);
+    }
+    return mx;
+}
+
+int mk_phase_count(const sd2_config& c) {
+    return c.k * (5 * c.drafter.n_layers + 1) + 5 * c.verifier.n_layers + 1;
+}
+
+size_t mk_counter_ints(const sd2_config& c) {
+    const int v = c.verifier.vocab / 16 + 1;
+    const int f = std::max(c.verifier.d_ff, c.drafter.d_ff) / 16 + 1;
+    const int kv = kMkMaxRows * std::max(c.verifier.n_kv_heads, c.drafter.n_kv_heads);
+    return (size_t)std::max(std::max(v, f), kv);
+}
+
+__global__ void k_mk_init(uint16_t* ones, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) ones[i] = 0x3f80;  // bf16 1.0
+}
+
+void mk_init_buffers(Engine& e) {
+    if (!e.mk.ones) return;
+    k_mk_init<<<(kMkMaxKR + 255) / 256, 256, 0, e.stream>>>(e.mk.ones, kMkMaxKR);
+}
+
+bool mk_build(Engine& e, int batch) {
+    MkState& s = e.mk;
+    s.active = false;
+    if (!s.prog || batch > s.max_batch || batch < 1 || getenv("SD2_NO_MK")) return false;
+    if (e.cfg.k + 1 > kMkMaxLaunch) return false;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    int cus = 0, coop = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop) return false;
+    if (cus < kMkMinWG || cus % 8) return false;  // LDS plans assume >= kMkMinWG workgroups
+    s.G = cus;
+    std::vector<MkPhase> prog;
+    size_t lds = 0;
+    const sd2_config& c = e.cfg;
+    for (int j = 1; j <= c.k; ++j) {
+        Arena ar{s.arena, 0};
+        s.off[j] = (int)prog.size();
+        if (!mk_record(c, e.md, false, j == 1 ? 2 * batch : batch, j == 1 ? 2 : 1, j, s.G, ar, &e.ws, &prog, &lds,
+                       s.cnt, nullptr, nullptr, &s.bytes[j]))
+            return false;
+        s.n[j] = (int)prog.size() - s.off[j];
+    }
+    {
+        Arena ar{s.arena, 0};
+        s.off[0] = (int)prog.size();
+        if (!mk_record(c, e.mv, true, batch * (c.k + 1), c.k + 1, 0, s.G, ar, &e.ws, &prog, &lds, s.cnt, &s.final_x,
+                       &s.final_ss, &s.bytes[0]))
+            return false;
+        s.n[0] = (int)prog.size() - s.off[0];
+    }
+    if ((int)prog.size() > s.prog_cap) return false;
+    s.lds = lds;
+    if (hipFuncSetAttribute((const void*)k_mk, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return false;
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, (const void*)k_mk, kMkThreads, lds) != hipSuccess || occ < 1)
+        return false;
+    if (hipMemcpyAsync(s.prog, prog.data(), sizeof(MkPhase) * prog.size(), hipMemcpyHostToDevice, e.stream) !=
+        hipSuccess)
+        return false;
+    if (hipStreamSynchronize(e.stream) != hipSuccess) return false;
+    s.batch = batch;
+    s.active = true;
+    return true;
+}
+
+hipError_t mk_launch(Engine& e, int j) {
+    MkState& s = e.mk;
+    const sd2_config& c = e.cfg;
+    const bool ver = j == 0;
+    ModelDev& m = ver ? e.mv : e.md;
+    MkArgs a{};
+    a.prog = s.prog + s.off[j];
+    a.nphase = s.n[j];
+    a.kind = ver ? 1 : 0;
+    a.j = j;
+    a.M = ver ? s.batch * (c.k + 1) : (j == 1 ? 2 * s.batch : s.batch);
+    a.rps = ver ? c.k + 1 : (j == 1 ? 2 : 1);
+    a.batch = e.batch;
+    a.k = c.k;
+    a.cap = e.cap;
+    a.max_batch = c.max_batch;
+    a.d = m.dm.d_model;
+    a.H = m.dm.n_heads;
+    a.Hkv = m.dm.n_kv_heads;
+    a.hd = m.hd;
+    a.eps = m.dm.rms_eps;
+    a.scale = 1.0f / sqrtf((float)m.hd);
+    a.t = e.ws.t;
+    a.len_d = e.ws.len_d;
+    a.done = e.ws.done;
+    a.hist = e.ws.hist;
+    a.drafts = e.ws.drafts;
+    a.steer = e.ws.steer;
+    a.embed = (const uint16_t*)m.embed;
+    a.vocab = m.dm.vocab;
+    a.add_steer = ver ? 0 : 1;
+    a.kc = m.kc;
+    a.vc = m.vc;
+    a.rcos = m.rope_cos;
+    a.rsin = m.rope_sin;
+    a.dummy = s.dummy;
+    a.ones = s.ones;
+    a.bar = s.bar;
+    a.err = s.err;
+    a.trace = (e.prof_on && s.trace) ? s.trace + (size_t)j * kMkTracePhases : nullptr;
+    a.G = s.G;
+    void* args[] = {&a};
+    ProfEntry* pe = prof_slot(&e, kProfGemv, s.bytes[j]);
+    if (pe) (void)hipEventRecord(pe->a, e.stream);
+    hipError_t err = hipLaunchCooperativeKernel((const void*)k_mk, dim3(s.G), dim3(kMkThreads), args, s.lds, e.stream);
+    if (pe) {
+        (void)hipEventRecord(pe->b, e.stream);
+        prof_commit(&e);
+    }
+    return err;
+}
+
+}  // namespace sd2

@@ -8,6 +8,8 @@ own decisions, and every comparison uses identical inputs:
   - logits and steering vectors must match within the dtype's tolerance;
   - emitted tokens, counts and cache lengths must match exactly.
 """
+import os
+
 import numpy as np
 import torch
 
@@ -47,8 +49,12 @@ class Stats:
                 f"err_steer={self.max_err_s:.3g}")
 
 
-def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check_logits=True, log=print):
-    """Run prefill + rounds on both sides; assert parity; return Stats."""
+def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check_logits=True, log=print,
+               expect_path=None, separate_kernels=False):
+    """Run prefill + rounds on both sides; assert parity; return Stats.
+
+    expect_path: 0 (one kernel per operation) or 1 (one persistent launch per drafter step and
+    verify pass) -- the execution path the library must have chosen; separate_kernels forces 0."""
     if wv is None:
         wv, wd, ws = si.model_weights(wl, 0), si.model_weights(wl, 1), si.steer_weights(wl)
     tol = TOL[wl.dtype]
@@ -59,7 +65,19 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
     dv, dd = device_model(wl, 0, wv), device_model(wl, 1, wd)
     ws_dev = B.to_device(ws)
     eng = B.Engine(B.config_of(wl), dv, dd, ws_dev)
-    eng.prefill(torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(), wl.max_prompt)
+    old = os.environ.pop("SD2_NO_MK", None)
+    if separate_kernels:
+        os.environ["SD2_NO_MK"] = "1"
+    try:
+        eng.prefill(torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(), wl.max_prompt)
+    finally:
+        os.environ.pop("SD2_NO_MK", None)
+        if old is not None:
+            os.environ["SD2_NO_MK"] = old
+    path = int(eng.debug(B.DBG_PATH)[0])
+    log(f"[parity] {wl.name}: execution path {path}")
+    if expect_path is not None:
+        assert path == expect_path, f"execution path {path}, expected {expect_path}"
     st = Stats()
     s_gpu = eng.debug(B.DBG_STEER)
     for b in seqs:
@@ -133,6 +151,7 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
         st.rounds += 1
     for b in seqs:
         assert o.state(b)["done"] == 1
+    assert int(eng.debug(B.DBG_PATH)[1]) == 0, "a persistent launch timed out at a grid barrier"
     eng.close()
     del eng, dv, dd, ws_dev
     torch.cuda.empty_cache()

@@ -47,3 +47,17 @@ def zeros_like_ws(wl):
 
 def to_f64(a, dtype):
     return si.bf16_to_f32(a).astype(np.float64) if dtype == "bf16" else a.astype(np.float64)
+
+# Shapes the persistent-launch path takes (every projection K a multiple of 512), small enough
+# for the float64 oracle: one layer each, then two layers with head dim 128, two sequences.
+MK1 = Workload(
+    name="mk-one-layer", verifier=Dims(1, 512, 8, 2, 1024, 2048, 5e5), drafter=Dims(1, 512, 8, 2, 1024, 2048, 5e5),
+    dtype="bf16", k=3, batch=1, prompt=(6, 6), new_tokens=8, temperature=1.0, seed=11)
+MK2 = Workload(
+    name="mk-two-layers", verifier=Dims(2, 1024, 8, 2, 2048, 4096, 5e5), drafter=Dims(2, 512, 8, 4, 1536, 4096, 5e5),
+    dtype="bf16", k=4, batch=2, prompt=(5, 13), new_tokens=12, temperature=1.0, seed=12)
+# Split-K projections on the persistent path: drafter down projection K = 14336 (4 ranges of 3584
+# columns, 7 waves per unit), verifier K = 8192 (2 ranges, 8 waves per unit); 6 verifier rows.
+MK3 = Workload(
+    name="mk-split-k", verifier=Dims(1, 512, 4, 2, 8192, 8192, 5e5), drafter=Dims(1, 512, 4, 2, 14336, 8192, 5e5),
+    dtype="bf16", k=5, batch=1, prompt=(7, 7), new_tokens=7, temperature=1.0, seed=13)

@@ -1,0 +1,30 @@
+"""Persistent-launch round path (one launch per drafter step and per verify pass) against the
+CPU oracle on small shapes that path takes, and the one-kernel-per-operation path on the same."""
+import pytest
+
+from oracle_fixtures import MK1, MK2, MK3
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(wl, **kw):
+    from gpu_harness import parity_run
+    st = parity_run(wl, **kw)
+    assert st.pinned > 0
+    return st
+
+
+def test_mk_one_layer_separate_kernels():
+    _run(MK1, expect_path=0, separate_kernels=True)
+
+
+def test_mk_one_layer_persistent():
+    _run(MK1, expect_path=1)
+
+
+def test_mk_two_layers_two_sequences_persistent():
+    _run(MK2, expect_path=1)
+
+
+def test_mk_split_k_persistent():
+    _run(MK3, expect_path=1)

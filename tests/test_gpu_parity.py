@@ -42,10 +42,28 @@ def host_8b():
 
 def test_parity_8b_shapes_short_prompt(host_8b):
     """Full 8B/1B model dimensions (32 x d4096 GQA verifier, 16 x d2048 drafter, 128256 vocab),
-    sampling at T=1, k=5, batch 1; a 16-token prompt keeps the float64 oracle within seconds."""
+    sampling at T=1, k=5, batch 1; a 16-token prompt keeps the float64 oracle within seconds.
+    Rounds run as persistent launches (one per drafter step, one per verify pass)."""
     wl = si.LLAMA8B.with_(prompt=(16, 16), new_tokens=10)
     wv, wd, ws = host_8b
-    _run(wl, wv=wv, wd=wd, ws=ws)
+    _run(wl, wv=wv, wd=wd, ws=ws, expect_path=1)
+
+
+def test_parity_8b_shapes_separate_kernels(host_8b):
+    """The same workload with one kernel per operation (the path used where the persistent
+    launches do not apply)."""
+    wl = si.LLAMA8B.with_(prompt=(16, 16), new_tokens=10)
+    wv, wd, ws = host_8b
+    _run(wl, wv=wv, wd=wd, ws=ws, expect_path=0, separate_kernels=True)
+
+
+def test_parity_8b_shapes_two_ragged_sequences(host_8b):
+    """Two sequences with different prompt lengths (k=2: 6 verifier rows per pass) on the
+    persistent launches: per-sequence positions, catch-up rows and finished sequences inside one
+    launch."""
+    wl = si.LLAMA8B.with_(batch=2, k=2, prompt=(9, 21), new_tokens=9)
+    wv, wd, ws = host_8b
+    _run(wl, wv=wv, wd=wd, ws=ws, expect_path=1)
 
 
 def test_parity_8b_batched_ragged_sampled_sequences(host_8b):
