@@ -13,7 +13,7 @@ constexpr int kMkWaves = 8;                      // weight-streaming waves per w
 constexpr int kMkThreads = kMkWaves * 64;
 constexpr int kMkMaxRows = 16;                   // activation rows per launch
 constexpr int kMkSpan = 64;                      // cache positions per attention unit
-constexpr int kMkMaxNq = 64;                     // query vectors per attention unit
+constexpr int kMkMaxNq = 32;                     // query vectors per attention unit (8 waves x 4)
 constexpr int kMkMaxKR = 4096;                   // K-range staged per workgroup
 constexpr int kMkLdsBudget = 150 * 1024;         // dynamic LDS per workgroup
 constexpr int kMkLine = 32;                      // ints per 128-byte line
@@ -40,7 +40,7 @@ struct MkPhase {
     int32_t* cnt;            // S > 1: arrival counter per tile; ATTN: per (sequence, KV head)
     float* qout;             // Qkv: queries [M][H*hd]; ATTN: query source
     float* aout;             // ATTN: output [M][H*hd]
-    float* apart;            // ATTN: partials [M][H][nsplit][hd+2]
+    float* apart;            // ATTN: partials [M][H][nsplit][hd+4] (outputs, span max, span sum)
 };
 
 // Launch-wide arguments.

@@ -41,6 +41,7 @@ typedef unsigned int mk_u2 __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(1))) mk_u4* mk_gu4p;
 typedef const __attribute__((address_space(1))) mk_u2* mk_gu2p;
 typedef const __attribute__((address_space(1))) mk_f4* mk_gf4p;
+typedef const __attribute__((address_space(1))) mk_f2* mk_gf2p;
 typedef const __attribute__((address_space(1))) float* mk_gfp;
 typedef const __attribute__((address_space(1))) int32_t* mk_gip;
 
@@ -59,12 +60,25 @@ __device__ __forceinline__ float4 mk_ldg4(const float* p) {
     mk_f4 v = *(mk_gf4p)p;
     return make_float4(v.x, v.y, v.z, v.w);
 }
+__device__ __forceinline__ float2 mk_ldg2(const float* p) {
+    mk_f2 v = *(mk_gf2p)p;
+    return make_float2(v.x, v.y);
+}
 __device__ __forceinline__ float mk_ldbf(const uint16_t* p) {
     return bf16_to_f32(*(const __attribute__((address_space(1))) uint16_t*)p);
 }
 __device__ __forceinline__ int mk_ldi(const int32_t* p) { return *(mk_gip)p; }
 __device__ __forceinline__ uint32_t mk_ldu(const void* p) { return *(const __attribute__((address_space(1))) uint32_t*)p; }
 __device__ __forceinline__ void mk_vmwait() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+// Thread index seen through an empty asm: index arithmetic of a phase then stays inside that
+// phase instead of being hoisted out of the phase loop, where the values of every phase kind
+// would stay live together and spill.
+__device__ __forceinline__ int mk_tid() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
 
 // Uniform copy of a value every lane holds identically (descriptor fields read from LDS): kept in
 // scalar registers instead of a stack copy of the whole descriptor.
@@ -222,7 +236,7 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
     const int owpu = mk_uni(od.wpu), osubs = mk_uni(od.subs), oxsrc = mk_uni(od.xsrc);
     const float* oX = mk_uni(od.X);
     const uint16_t* ogamma = mk_uni(od.gamma);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
     const int G = a.G, M = a.M;
     const int s = blockIdx.x % oS, g = blockIdx.x / oS, gs = G / oS;
     const int k0 = s * oKR, KR = oKR, ldk = KR + 8;
@@ -496,8 +510,7 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
     o.aout = mk_uni(od.aout);
     o.apart = mk_uni(od.apart);
     o.cnt = mk_uni(od.cnt);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nwaves = kMkThreads / 64;
+    const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
     const int Gq = a.H / a.Hkv;
     const int nq = a.rps * Gq;
     const int nseq = a.M / a.rps;
@@ -516,117 +529,223 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
         for (int i = 0; i < a.rps; ++i) maxq = max(maxq, rp.pos[sq * a.rps + i]);
         const int p0 = sp * kMkSpan;
         const int nvalid = maxq >= p0 ? min(kMkSpan, maxq - p0 + 1) : 0;
-        if (nvalid > 0) {
+        // live spans of this sequence (those holding a position some query sees)
+        const int nl = maxq >= 0 ? min(o.nsplit, maxq / kMkSpan + 1) : 0;
+        if (nl == 0 && sp == 0) {
+            // no live position (padding): the outputs are zero
+            for (int e = tid; e < nq * HD; e += kMkThreads) {
+                const int qi = e / HD, d = e % HD;
+                mk_stf(o.aout + (size_t)(sq * a.rps + qi / Gq) * a.H * HD + (kvh * Gq + qi % Gq) * HD + d, 0.f);
+            }
+        }
+        if (nvalid == 0) continue;  // dead span: no work and no hand-off
+        {
             const size_t head_base = (((size_t)o.layer * a.max_batch + rp.seq[sq * a.rps]) * a.Hkv + kvh) * a.cap * HD;
             const float* kg = a.kc + head_base + (size_t)p0 * HD;
             const float* vg = a.vc + head_base + (size_t)p0 * HD;
-            // K and V rows of the span (rows past the last valid one re-read it; masked below)
-            for (int e4 = tid; e4 < kMkSpan * HD / 4; e4 += kMkThreads) {
+            // every load of the unit is issued before any is used: K and V rows of the span (rows
+            // past the last valid one re-read it; masked below) and the queries
+            constexpr int F4 = kMkSpan * HD / 4 / kMkThreads;   // float4 of K (and of V) per thread
+            constexpr int Q4 = (kMkMaxNq * HD / 4 + kMkThreads - 1) / kMkThreads;  // float4 of queries per thread
+            float4 kv4[F4], vv4[F4], qv4[Q4];
+#pragma unroll
+            for (int i = 0; i < F4; ++i) {
+                const int e4 = tid + i * kMkThreads;
                 const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
                 const int jj = j < nvalid ? j : nvalid - 1;
-                const float4 kv = mk_ldg4(kg + (size_t)jj * HD + d);
-                const float4 vv = mk_ldg4(vg + (size_t)jj * HD + d);
-                *(float4*)(ks + j * (HD + 4) + d) = kv;
-                *(float4*)(vs + j * HD + d) = vv;
+                kv4[i] = mk_ldg4(kg + (size_t)jj * HD + d);
+                vv4[i] = mk_ldg4(vg + (size_t)jj * HD + d);
             }
-            for (int e = tid; e < nq * HD; e += kMkThreads) {
+#pragma unroll
+            for (int i = 0; i < Q4; ++i) {
+                const int e = (tid + i * kMkThreads) * 4;
                 const int qi = e / HD, d = e % HD;
-                const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
-                qs[e] = mk_ldg(o.qout + (size_t)row * a.H * HD + h * HD + d) * a.scale;
+                const int qc = qi < nq ? qi : 0;  // also keeps e past kMkMaxNq*HD in bounds
+                const int row = sq * a.rps + qc / Gq, h = kvh * Gq + qc % Gq;
+                qv4[i] = mk_ldg4(o.qout + (size_t)row * a.H * HD + h * HD + d);
+            }
+#pragma unroll
+            for (int i = 0; i < F4; ++i) {
+                const int e4 = tid + i * kMkThreads;
+                const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
+                *(float4*)(ks + j * (HD + 4) + d) = kv4[i];
+                *(float4*)(vs + j * HD + d) = vv4[i];
+            }
+#pragma unroll
+            for (int i = 0; i < Q4; ++i) {
+                const int e = (tid + i * kMkThreads) * 4;
+                const float4 v = qv4[i];
+                if (e < kMkMaxNq * HD) *(float4*)(qs + e) = make_float4(v.x * a.scale, v.y * a.scale, v.z * a.scale, v.w * a.scale);
             }
             __syncthreads();
-            // scores: one wave per query vector, one lane per position
-            for (int qi = wave; qi < nq; qi += nwaves) {
-                const int row = sq * a.rps + qi / Gq;
-                const int qp = rp.pos[row];
-                float sc = -INFINITY;
-                if (lane < nvalid && p0 + lane <= qp) {
-                    const float4* qr = (const float4*)(qs + qi * HD);
-                    const float4* kr = (const float4*)(ks + lane * (HD + 4));
-                    float d0 = 0.f, d1 = 0.f;
-#pragma unroll 8
+            // scores, one lane per position: with few query vectors one wave per vector, else wave
+            // w takes vectors 4w..4w+3 so that a K row read from LDS feeds four dot products
+            const bool few = nq <= kMkWaves;
+            const int qw = few ? 1 : 4;
+            if (qw * wave < nq) {
+                float sc[4] = {0.f, 0.f, 0.f, 0.f};
+                const float4* kr = (const float4*)(ks + lane * (HD + 4));
+                if (few) {
+                    const float4* qr = (const float4*)(qs + wave * HD);
+#pragma unroll 4
                     for (int d4 = 0; d4 < HD / 4; ++d4) {
-                        const float4 qv = qr[d4], kv = kr[d4];
-                        d0 += qv.x * kv.x + qv.z * kv.z;
-                        d1 += qv.y * kv.y + qv.w * kv.w;
+                        const float4 kv = kr[d4], qv = qr[d4];
+                        sc[0] += qv.x * kv.x + qv.y * kv.y + qv.z * kv.z + qv.w * kv.w;
                     }
-                    sc = d0 + d1;
+                } else {
+#pragma unroll 2
+                    for (int d4 = 0; d4 < HD / 4; ++d4) {
+                        const float4 kv = kr[d4];
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float4 qv = ((const float4*)(qs + (4 * wave + i) * HD))[d4];
+                            sc[i] += qv.x * kv.x + qv.y * kv.y + qv.z * kv.z + qv.w * kv.w;
+                        }
+                    }
                 }
-                const float mx = wave_max(sc);
-                const float p = sc == -INFINITY ? 0.f : expf(sc - mx);
-                const float sm = wave_sum(p);
-                ps[qi * kMkSpan + lane] = p;
-                if (lane == 0) { mq[qi] = mx; lq[qi] = sm; }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int qi = qw * wave + i;
+                    if (i >= qw || qi >= nq) break;
+                    const int qp = rp.pos[sq * a.rps + qi / Gq];
+                    const float v = (lane < nvalid && p0 + lane <= qp) ? sc[i] : -INFINITY;
+                    const float mx = wave_max(v);
+                    const float pr = v == -INFINITY ? 0.f : expf(v - mx);
+                    const float sm = wave_sum(pr);
+                    ps[lane * kMkMaxNq + qi] = pr;  // [position][query]
+                    if (lane == 0) { mq[qi] = mx; lq[qi] = sm; }
+                }
             }
             __syncthreads();
-            // un-normalised outputs of the span
-            for (int e = tid; e < nq * HD; e += kMkThreads) {
-                const int qi = e / HD, d = e % HD;
-                const float* pr = ps + qi * kMkSpan;
-                float acc = 0.f;
+            // un-normalised outputs: with few query vectors a thread per (vector, head dim), else
+            // wave -> (block of 8 vectors, 64 head dims); the probabilities of a position are read
+            // as a broadcast, each V element once per block
+            if (few) {
+                for (int e = tid; e < nq * HD; e += kMkThreads) {
+                    const int qi = e / HD, d = e % HD;
+                    float acc = 0.f;
 #pragma unroll 8
-                for (int j = 0; j < kMkSpan; ++j) acc += pr[j] * vs[j * HD + d];
-                const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
-                float* pp = o.apart + (((size_t)row * a.H + h) * o.nsplit + sp) * (HD + 2);
-                mk_stf(pp + d, acc);
-                if (d == 0) {
-                    mk_stf(pp + HD, mq[qi]);
-                    mk_stf(pp + HD + 1, lq[qi]);
+                    for (int j = 0; j < kMkSpan; ++j) acc += ps[j * kMkMaxNq + qi] * vs[j * HD + d];
+                    const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
+                    if (nl == 1) {
+                        const float l = lq[qi];
+                        mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, l > 0.f ? acc / l : 0.f);
+                    } else {
+                        float* pp = o.apart + (((size_t)row * a.H + h) * o.nsplit + sp) * (HD + 4);
+                        mk_stf(pp + d, acc);
+                        if (d == 0) {
+                            mk_stf(pp + HD, mq[qi]);
+                            mk_stf(pp + HD + 1, lq[qi]);
+                        }
+                    }
+                }
+            } else {
+                const int ndg = HD / 64 > 0 ? HD / 64 : 1;   // 64-wide groups of head dims
+                const int qb = wave / ndg, dg = wave % ndg;
+                const int d = dg * 64 + lane;
+                if (8 * qb < nq && d < HD) {
+                    float acc[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+#pragma unroll 2
+                    for (int j = 0; j < kMkSpan; ++j) {
+                        const float4 pa = *(const float4*)(ps + j * kMkMaxNq + 8 * qb);
+                        const float4 pb = *(const float4*)(ps + j * kMkMaxNq + 8 * qb + 4);
+                        const float v = vs[j * HD + d];
+                        acc[0] += pa.x * v; acc[1] += pa.y * v; acc[2] += pa.z * v; acc[3] += pa.w * v;
+                        acc[4] += pb.x * v; acc[5] += pb.y * v; acc[6] += pb.z * v; acc[7] += pb.w * v;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        const int qi = 8 * qb + i;
+                        if (qi >= nq) break;
+                        const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
+                        if (nl == 1) {
+                            // the only live span: normalise and write the output itself
+                            const float l = lq[qi];
+                            mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, l > 0.f ? acc[i] / l : 0.f);
+                        } else {
+                            float* pp = o.apart + (((size_t)row * a.H + h) * o.nsplit + sp) * (HD + 4);
+                            mk_stf(pp + d, acc[i]);
+                            if (d == 0) {
+                                mk_stf(pp + HD, mq[qi]);
+                                mk_stf(pp + HD + 1, lq[qi]);
+                            }
+                        }
+                    }
                 }
             }
         }
-        // count in; the last span of this (sequence, KV head) merges the live spans
+        if (nl == 1) {
+            __syncthreads();  // LDS of this unit is reused by the next
+            continue;
+        }
+        // count in; the last live span of this (sequence, KV head) merges the live spans
         mk_vmwait();
         __syncthreads();
         if (tid == 0) {
             int32_t* c = o.cnt + sq * a.Hkv + kvh;
             const int prev = mk_add(c, 1);
-            *last_flag = prev == o.nsplit - 1;
-            if (prev == o.nsplit - 1) mk_sti(c, 0);
+            *last_flag = prev == nl - 1;
+            if (prev == nl - 1) mk_sti(c, 0);
         }
         __syncthreads();
         if (*last_flag) {
-            const int nlive = maxq >= 0 ? min(o.nsplit, maxq / kMkSpan + 1) : 0;
-            for (int e = tid; e < nq * HD; e += kMkThreads) {
-                const int qi = e / HD, d = e % HD;
+            // a thread per (query vector, 4 head dims) requests the partial outputs and the
+            // (max, sum) of sixteen spans at once and folds them into a running (max, sum, output)
+            constexpr int D4 = HD / 4;
+            for (int e = tid; e < nq * D4; e += kMkThreads) {
+                const int qi = e / D4, d = (e % D4) * 4;
                 const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
-                float resv = 0.f;
+                float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
                 if (rp.pos[row] >= 0) {
-                    const float* pp = o.apart + ((size_t)row * a.H + h) * o.nsplit * (HD + 2);
-                    // spans are merged 16 at a time: every partial of a group is requested before
-                    // any is used, and the running (max, sum, output) is rescaled per group
-                    float Mx = -INFINITY, L = 0.f, O = 0.f;
-                    for (int s0 = 0; s0 < nlive; s0 += 16) {
-                        float mv[16], lv[16], ov[16];
+                    const float* pb = o.apart + ((size_t)row * a.H + h) * o.nsplit * (HD + 4);
+                    float Mx = -INFINITY, L = 0.f;
+                    float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+                    for (int s0 = 0; s0 < nl; s0 += 16) {
+                        float4 v[16];
+                        float2 ml[16];
 #pragma unroll
                         for (int i = 0; i < 16; ++i) {
-                            const float* e2 = pp + (size_t)(s0 + i) * (HD + 2);
-                            const bool live = s0 + i < nlive;
-                            mv[i] = live ? mk_ldg(e2 + HD) : -INFINITY;
-                            lv[i] = live ? mk_ldg(e2 + HD + 1) : 0.f;
-                            ov[i] = live ? mk_ldg(e2 + d) : 0.f;
+                            const float* e2 = pb + (size_t)min(s0 + i, nl - 1) * (HD + 4);
+                            v[i] = mk_ldg4(e2 + d);
+                            ml[i] = mk_ldg2(e2 + HD);
                         }
                         float cm = -INFINITY;
 #pragma unroll
-                        for (int i = 0; i < 16; ++i) cm = fmaxf(cm, mv[i]);
+                        for (int i = 0; i < 16; ++i)
+                            if (s0 + i < nl) cm = fmaxf(cm, ml[i].x);
                         if (cm == -INFINITY) continue;
                         if (cm > Mx) {
                             const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
                             L *= sc;
-                            O *= sc;
+                            O.x *= sc;
+                            O.y *= sc;
+                            O.z *= sc;
+                            O.w *= sc;
                             Mx = cm;
                         }
 #pragma unroll
                         for (int i = 0; i < 16; ++i) {
-                            if (mv[i] == -INFINITY) continue;
-                            const float w = expf(mv[i] - Mx);
-                            L += w * lv[i];
-                            O += w * ov[i];
+                            if (s0 + i >= nl || ml[i].x == -INFINITY) continue;
+                            const float w = expf(ml[i].x - Mx);
+                            L += w * ml[i].y;
+                            O.x += w * v[i].x;
+                            O.y += w * v[i].y;
+                            O.z += w * v[i].z;
+                            O.w += w * v[i].w;
                         }
                     }
-                    resv = L > 0.f ? O / L : 0.f;
+                    if (L > 0.f) {
+                        const float inv = 1.f / L;
+                        r = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+                    }
                 }
-                mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, resv);
+                float* op = o.aout + (size_t)row * a.H * HD + h * HD + d;
+                mk_stf(op, r.x);
+                mk_stf(op + 1, r.y);
+                mk_stf(op + 2, r.z);
+                mk_stf(op + 3, r.w);
             }
         }
         __syncthreads();
@@ -765,7 +884,7 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         float* xa = ar.take<float>((size_t)M * dm);
         float* hbuf = ar.take<float>((size_t)M * F);
         float* xf = ar.take<float>((size_t)M * dm);
-        float* apart = ar.take<float>((size_t)M * H * nsplit * (hd + 2));
+        float* apart = ar.take<float>((size_t)M * H * nsplit * (hd + 4));
         float* ss = (l == L - 1) ? ar.take<float>((size_t)M * (dm / 16)) : nullptr;
         MkPhase qkv{};
         if (!gemv(kEpiQkv, (H + 2 * Hkv) * hd, dm, Wl[kAttnNorm], true, 1, qkv)) return false;

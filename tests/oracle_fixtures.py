@@ -61,3 +61,8 @@ MK2 = Workload(
 MK3 = Workload(
     name="mk-split-k", verifier=Dims(1, 512, 4, 2, 8192, 8192, 5e5), drafter=Dims(1, 512, 4, 2, 14336, 8192, 5e5),
     dtype="bf16", k=5, batch=1, prompt=(7, 7), new_tokens=7, temperature=1.0, seed=13)
+# Contexts over several 64-position attention spans on the persistent path, ragged: prompts of
+# 232, 273 and 63 tokens (the last crosses a span boundary while generating).
+MK4 = Workload(
+    name="mk-long-ragged", verifier=Dims(1, 512, 8, 2, 1024, 2048, 5e5), drafter=Dims(1, 512, 8, 2, 1024, 2048, 5e5),
+    dtype="bf16", k=3, batch=3, prompt=(40, 300), new_tokens=24, temperature=1.0, seed=15)

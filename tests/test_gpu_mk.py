@@ -2,7 +2,7 @@
 CPU oracle on small shapes that path takes, and the one-kernel-per-operation path on the same."""
 import pytest
 
-from oracle_fixtures import MK1, MK2, MK3
+from oracle_fixtures import MK1, MK2, MK3, MK4
 
 pytestmark = pytest.mark.gpu
 
@@ -28,3 +28,11 @@ def test_mk_two_layers_two_sequences_persistent():
 
 def test_mk_split_k_persistent():
     _run(MK3, expect_path=1)
+
+
+def test_mk_long_ragged_contexts_persistent():
+    _run(MK4, expect_path=1)
+
+
+def test_mk_long_ragged_contexts_separate_kernels():
+    _run(MK4, expect_path=0, separate_kernels=True)
