@@ -74,12 +74,17 @@ def cpu_baseline(wl, wv, wd, ws, toks, lens, budget_s):
 # rocprofv3 post-processing (host-only; no GPU).  Rounds are delimited by k_set_flag, the one
 # single-thread kernel every sd2_round launches first.
 # ---------------------------------------------------------------------------------------------
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_wsgemv_8b-bf16-b1_traffic.json")
-TRAFFIC_SOURCES = ("paper_2511_09844_amd/csrc/wsgemv.hip", "paper_2511_09844_amd/csrc/device_common.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_mk_8b-bf16-b1_traffic.json")
+TRAFFIC_SOURCES = ("paper_2511_09844_amd/csrc/mk.hip", "paper_2511_09844_amd/csrc/mk.h",
+                   "paper_2511_09844_amd/csrc/device_common.h")
+ROOFLINE_KERNEL = "k_mk"
 
 
 def _kclass(name):
-    return "k_wsgemv" if "k_wsgemv" in name else "k_attn" if "k_attn" in name else "other"
+    for k in ("k_mk", "k_wsgemv", "k_attn"):
+        if k + "(" in name or k + "<" in name:
+            return k
+    return "other"
 
 
 def _round_windows(names, skip_first):
@@ -97,7 +102,8 @@ def summarize_trace(path, last_eager):
             rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
     rows.sort()
     wins = _round_windows([r[2] for r in rows], 0)
-    groups = (("graph-launched rounds", wins[:len(wins) - last_eager]), ("eager (event-timed) rounds", wins[-last_eager:]))
+    groups = (("timed rounds (graph replays; eager launches on the persistent path)", wins[:len(wins) - last_eager]),
+              ("profiled (event-timed, eager) rounds", wins[-last_eager:]))
     for title, ws in groups:
         if not ws:
             continue
@@ -124,8 +130,9 @@ def _source_hash():
 
 
 def summarize_pmc(fetch_csv, write_csv, write_json):
-    """HBM traffic per k_wsgemv launch from FETCH_SIZE and WRITE_SIZE runs (KiB per dispatch), each
-    scaled by what the same counter reads for the 1 GiB calibration copy."""
+    """HBM traffic per k_mk launch (persistent drafter-step and verify-pass launches) from
+    FETCH_SIZE and WRITE_SIZE runs (KiB per dispatch), each scaled by what the same counter reads
+    for the 1 GiB calibration copy."""
     import csv
     out = {}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
@@ -138,19 +145,19 @@ def summarize_pmc(fetch_csv, write_csv, write_json):
         n, kib = 0, 0.0
         for a, b in wins:
             for _, name, v in rows[a:b]:
-                if "k_wsgemv" in name:
+                if _kclass(name) == ROOFLINE_KERNEL:
                     n += 1
                     kib += v
         copy = max((v for _, name, v in rows if "copyBuffer" in name), default=0.0)
         factor = (1 << 20) / copy if copy else float("nan")
         out[counter] = {"launches": n, "kib_per_launch_raw": kib / max(1, n), "copy_kib_raw": copy,
                         "scale": factor, "bytes_per_launch": kib / max(1, n) * factor * 1024}
-        print(f"{counter}: {n} k_wsgemv launches in {len(wins)} rounds, {kib / max(1, n):.1f} KiB/launch raw; "
+        print(f"{counter}: {n} {ROOFLINE_KERNEL} launches in {len(wins)} rounds, {kib / max(1, n):.1f} KiB/launch raw; "
               f"1 GiB copy reads {copy:.0f} KiB -> scale {factor:.4f}; {out[counter]['bytes_per_launch'] / 1e6:.3f} MB/launch")
     total = out["FETCH_SIZE"]["bytes_per_launch"] + out["WRITE_SIZE"]["bytes_per_launch"]
-    print(f"traffic per k_wsgemv launch: {total / 1e6:.3f} MB")
+    print(f"traffic per {ROOFLINE_KERNEL} launch: {total / 1e6:.3f} MB")
     if write_json:
-        rec = {"kernel": "k_wsgemv", "workload": "8b-bf16-b1", "source_sha256": _source_hash(),
+        rec = {"kernel": ROOFLINE_KERNEL, "workload": "8b-bf16-b1", "source_sha256": _source_hash(),
                "traffic_bytes_per_launch": total, "counters": out}
         with open(write_json, "w") as f:
             json.dump(rec, f, indent=1)
@@ -158,7 +165,7 @@ def summarize_pmc(fetch_csv, write_csv, write_json):
 
 
 def stored_traffic(workload):
-    """Counter-measured bytes per k_wsgemv launch, if taken on the current kernel source and workload."""
+    """Counter-measured bytes per k_mk launch, if taken on the current kernel source and workload."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
@@ -186,7 +193,7 @@ def main():
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print the per-round breakdown of a rocprofv3 kernel trace of this script and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="print k_wsgemv HBM traffic from two rocprofv3 --pmc runs of this script with "
+                    help="print k_mk HBM traffic from two rocprofv3 --pmc runs of this script with "
                          "--calib-copy and exit")
     ap.add_argument("--write-traffic", action="store_true", help="with --summarize-pmc: store the result")
     args = ap.parse_args()
@@ -254,7 +261,8 @@ def main():
         st1 = eng.state()
         log(f"timed {args.steps} rounds: {ms:.2f} ms")
         # kernel-level timing: HIP events around every launch of the same rounds, recorded into the graph
-        prof = {c: [0, 0.0, 0.0] for c in (B.PROF_GEMV, B.PROF_ATTN, B.PROF_SAMPLER, B.PROF_OTHER)}
+        prof = {c: [0, 0.0, 0.0] for c in (B.PROF_PROGRAM, B.PROF_GEMV, B.PROF_ATTN, B.PROF_SAMPLER, B.PROF_OTHER)}
+        stp0 = eng.state()
         if args.prof_rounds > 0:
             eng.profile(True)
             for _ in range(args.prof_rounds):
@@ -266,6 +274,7 @@ def main():
                     prof[c][2] += pby
             eng.profile(False)
         torch.cuda.synchronize()
+        stp1 = eng.state()
         if args.calib_copy:
             src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
             dst = torch.empty_like(src)
@@ -287,11 +296,29 @@ def main():
         kvd_b += kvd
     bytes_round = w_b + kvv_b + kvd_b
     ms_round = ms / args.steps
-    g_n, g_ms, g_by = prof[B.PROF_GEMV]
+    # roofline of the dominant kernel: the persistent launches (weights they stream, from the
+    # library, plus the KV rows their attention phases read, from the sequence lengths)
+    pr = max(1, args.prof_rounds)
+    kv_prof = 0.0
+    for b in range(wl.batch):
+        if stp0[b]["done"]:
+            continue
+        t_p = stp0[b]["t"] + (stp1[b]["t"] - stp0[b]["t"]) * (pr - 1) / (2 * pr)
+        _, kvv, kvd = round_bytes(wl, t_p)
+        kv_prof += (kvv + kvd) * args.prof_rounds
+    p_n, p_ms, p_by = prof[B.PROF_PROGRAM]
+    if p_n:
+        r_kernel = ("k_mk (persistent launch: one per drafter step, one per verify pass; every projection, "
+                    "attention and LM head of that forward)")
+        g_n, g_ms, g_by = p_n, p_ms, p_by + kv_prof
+    else:
+        r_kernel = "k_wsgemv (every weight-streaming projection: QKV, O, gate|up, down, LM heads, W_s)"
+        g_n, g_ms, g_by = prof[B.PROF_GEMV]
     gemv_gbs = g_by / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
     log(f"round: {ms_round:.3f} ms, {bytes_round / 1e9:.3f} GB algorithmic -> "
         f"{bytes_round / (ms_round / 1e3) / 1e9:.0f} GB/s ({bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS:.1%} of HBM)")
-    for c, name in ((B.PROF_GEMV, "gemv"), (B.PROF_ATTN, "attn"), (B.PROF_SAMPLER, "sampler"), (B.PROF_OTHER, "other")):
+    for c, name in ((B.PROF_PROGRAM, "program"), (B.PROF_GEMV, "gemv"), (B.PROF_ATTN, "attn"),
+                    (B.PROF_SAMPLER, "sampler"), (B.PROF_OTHER, "other")):
         n, pms, pby = prof[c]
         log(f"  {name}: {n / max(1, args.prof_rounds):.0f} launches/round, {pms / max(1, args.prof_rounds):.3f} ms/round"
             + (f", {pby / (pms / 1e3) / 1e9:.0f} GB/s" if pby and pms else ""))
@@ -318,9 +345,10 @@ def main():
         "block_efficiency": tau,
         "round_bytes": bytes_round,
         "round_hbm_frac": bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS,
-        "roofline": {"bound": "hbm", "kernel": "k_wsgemv (every weight-streaming projection: QKV, O, gate|up, down, LM heads, W_s)",
+        "roofline": {"bound": "hbm", "kernel": r_kernel,
                      "achieved": gemv_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gemv_gbs / PEAK_HBM_GBS,
-                     "traffic": stored_traffic(wl.name), "launches_per_round": g_n / max(1, args.prof_rounds),
+                     "traffic": stored_traffic(wl.name) if p_n else None,
+                     "launches_per_round": g_n / max(1, args.prof_rounds),
                      "avg_launch_us": g_ms / max(1, g_n) * 1e3,
                      "bytes_per_launch": g_by / max(1, g_n)},
         "cpu_baseline": None,

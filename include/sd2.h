@@ -165,6 +165,7 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
 #define SD2_PROF_ATTN 2      /* attention over the KV cache */
 #define SD2_PROF_SAMPLER 3   /* draft picks, accept test, final draw, commit */
 #define SD2_PROF_OTHER 4     /* embedding/planning, RoPE and cache append */
+#define SD2_PROF_PROGRAM 5   /* persistent launches (one per drafter step, one per verify pass) */
 
 /*
  * Measurement hook.  enable != 0: following rounds are launched one kernel at a time (not from
@@ -176,7 +177,8 @@ sd2_status sd2_profile(sd2_handle_t h, int32_t enable);
 /*
  * For the last profiled round (synchronises the stream): number of launches of class cls,
  * the sum of their event-to-event durations in milliseconds, and the sum of their algorithmic
- * bytes (for SD2_PROF_GEMV: weights + input rows + output rows; 0 for other classes).
+ * bytes (SD2_PROF_GEMV: weights + input rows + output rows; SD2_PROF_PROGRAM: the weights the
+ * launch streams, KV-cache reads not included; 0 for other classes).
  */
 sd2_status sd2_profile_read(sd2_handle_t h, int32_t cls, int32_t* launches, double* total_ms, double* bytes);
 

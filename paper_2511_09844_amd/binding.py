@@ -20,7 +20,7 @@ DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG
 
 EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
            "sd2_status_string", "sd2_last_error", "sd2_debug_read", "sd2_profile", "sd2_profile_read"]
-PROF_GEMV, PROF_ATTN, PROF_SAMPLER, PROF_OTHER = 1, 2, 3, 4
+PROF_GEMV, PROF_ATTN, PROF_SAMPLER, PROF_OTHER, PROF_PROGRAM = 1, 2, 3, 4, 5
 
 
 class Dims(ctypes.Structure):

@@ -82,7 +82,7 @@ struct Workspace {
 };
 
 // Per-launch timing entries (HIP events recorded on the engine's stream).
-enum ProfClass { kProfGemv = 1, kProfAttn = 2, kProfSampler = 3, kProfOther = 4 };
+enum ProfClass { kProfGemv = 1, kProfAttn = 2, kProfSampler = 3, kProfOther = 4, kProfProgram = 5 };
 constexpr int kProfMax = 4096;
 struct ProfEntry {
     int cls;

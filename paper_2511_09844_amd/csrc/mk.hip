@@ -1112,7 +1112,7 @@ hipError_t mk_launch(Engine& e, int j) {
     a.trace = (e.prof_on && s.trace) ? s.trace + (size_t)j * kMkTracePhases : nullptr;
     a.G = s.G;
     void* args[] = {&a};
-    ProfEntry* pe = prof_slot(&e, kProfGemv, s.bytes[j]);
+    ProfEntry* pe = prof_slot(&e, kProfProgram, s.bytes[j]);
     if (pe) (void)hipEventRecord(pe->a, e.stream);
     hipError_t err = hipLaunchCooperativeKernel((const void*)k_mk, dim3(s.G), dim3(kMkThreads), args, s.lds, e.stream);
     if (pe) {
