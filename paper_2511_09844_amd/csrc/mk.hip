@@ -46,6 +46,7 @@ typedef const __attribute__((address_space(1))) float* mk_gfp;
 typedef const __attribute__((address_space(1))) int32_t* mk_gip;
 
 constexpr int kNW = kMkWaves;
+constexpr int kMkPreSteps = 8;      // 64-column slices of a phase's first unit requested during its barrier
 constexpr int kMkMinWG = 256;       // workgroups assumed by the LDS plans (one per compute unit)
 constexpr int kNT = kMkWaves * 64;  // streaming threads
 constexpr int kCtl = 0;             // thread that runs the grid barrier (no loads in flight there)
@@ -135,45 +136,6 @@ __device__ __forceinline__ void mk_plan(const MkArgs& a, MkRows& rp) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Grid barrier.  Counters: one per XCD group (workgroup id mod 8), one global; the last arriver
-// of a group resets it and counts the group in; the last group resets the global counter and
-// publishes the next generation on 8 lines (one per group) that the control threads poll.  The
-// generation only grows, so no reset races with a poll.
-// ---------------------------------------------------------------------------------------------
-__device__ __forceinline__ void mk_barrier(const MkArgs& a, int& gen, long& spins) {
-    __builtin_amdgcn_s_barrier();
-    if (threadIdx.x == kCtl) {
-        int32_t* base = a.bar;
-        const int x = blockIdx.x & 7;
-        const int ngroup = a.G < 8 ? a.G : 8;
-        const int per = a.G / 8 + (x < a.G % 8 ? 1 : 0);
-        const int prev = mk_add(base + (2 + x) * kMkLine, 1);
-        if (prev == per - 1) {
-            mk_sti(base + (2 + x) * kMkLine, 0);
-            mk_vmwait();
-            const int gp = mk_add(base + kMkLine, 1);
-            if (gp == ngroup - 1) {
-                mk_sti(base + kMkLine, 0);
-                mk_vmwait();
-                for (int i = 0; i < 8; ++i) mk_sti(base + (10 + i) * kMkLine, gen + 1);
-            }
-        }
-        gen += 1;
-        if (spins >= 0) {
-            while ((int)(mk_ld(base + (10 + x) * kMkLine) - gen) < 0) {
-                if (++spins > kMkSpin) {
-                    mk_sti(a.err, 1);
-                    spins = -1;  // give up waiting for the rest of the launch (results invalid)
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-        }
-    }
-    __builtin_amdgcn_s_barrier();
-}
-
-// ---------------------------------------------------------------------------------------------
 // Projection phase.
 // ---------------------------------------------------------------------------------------------
 struct MkBuf {
@@ -208,13 +170,59 @@ __device__ __forceinline__ int mk_units(int tiles, int S, int subs, int G) {
 }
 
 // stride 8 (16-byte words per 64 columns) for a real unit; 0 re-reads one word (absent unit)
+template <int ST0 = 0, int ST1 = 8>
 __device__ __forceinline__ void mk_issue(MkBuf& b, const uint16_t* wp, int stride) {
     mk_gu4p p = (mk_gu4p)wp;
 #pragma unroll
-    for (int st = 0; st < 8; ++st) {
+    for (int st = ST0; st < ST1; ++st) {
         b.w[st][0] = p[st * stride];
         b.w[st][1] = p[st * stride + (stride >> 3)];
     }
+}
+
+// Geometry of a projection phase for this workgroup and wave, from its descriptor in LDS.
+struct MkGeo {
+    MkW ow;
+    int s, g, gs, k0, nsub, wpu, groups, gr, kw0, subs;
+    bool streams;
+};
+__device__ __forceinline__ MkGeo mk_geo(const MkArgs& a, const MkPhase& od, int wave) {
+    MkGeo q;
+    q.ow.w0 = mk_uni(od.W[0]);
+    q.ow.w1 = mk_uni(od.W[1]);
+    q.ow.w2 = mk_uni(od.W[2]);
+    q.ow.K = mk_uni(od.K);
+    q.ow.mode = mk_uni(od.mode);
+    q.ow.nseg = mk_uni(od.nseg);
+    q.ow.st0 = mk_uni(od.seg_tiles[0]);
+    q.ow.st1 = mk_uni(od.seg_tiles[1]);
+    const int tiles = mk_uni(od.tiles), S = mk_uni(od.S), KR = mk_uni(od.KR);
+    q.wpu = mk_uni(od.wpu);
+    q.subs = mk_uni(od.subs);
+    q.s = blockIdx.x % S;
+    q.g = blockIdx.x / S;
+    q.gs = a.G / S;
+    q.k0 = q.s * KR;
+    q.nsub = mk_units(tiles, S, q.subs, a.G);
+    q.groups = kNW / q.wpu;
+    q.gr = wave / q.wpu;
+    q.streams = wave < kNW && q.gr < q.groups;
+    q.kw0 = (wave % q.wpu) * 512;
+    return q;
+}
+
+// Weight unit of round r for this wave: its address for lane (n, qq), and the stride to pass to
+// mk_issue (0 when the wave has no unit in that round: one word of the zero page is re-read).
+__device__ __forceinline__ const uint16_t* mk_uptr(const MkArgs& a, const MkGeo& q, int r, int n, int qq, int lane,
+                                                   int& stride) {
+    const int u = r * q.groups + q.gr;
+    if (!(q.streams && u < q.nsub)) {
+        stride = 0;
+        return a.dummy + lane * 8;
+    }
+    stride = 8;
+    const int tile = q.g + (q.subs == 2 ? (u >> 1) : u) * q.gs;
+    return mk_row(q.ow, a.hd, tile, q.subs == 2 ? (u & 1) : 0, n) + q.k0 + q.kw0 + 16 * qq;
 }
 
 // Embedding row value of activation row m, column c (+ steering for drafter launches).
@@ -226,57 +234,88 @@ __device__ __forceinline__ float mk_embed_at(const MkArgs& a, const MkRows& rp, 
 }
 
 __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, float* inv_rms,
-                        int* flags, int* last_flag) {
+                        int* flags, int* last_flag, MkBuf& bf) {
     // descriptor fields (od lives in LDS), uniform
-    MkW ow;
-    ow.w0 = mk_uni(od.W[0]); ow.w1 = mk_uni(od.W[1]); ow.w2 = mk_uni(od.W[2]);
-    ow.K = mk_uni(od.K); ow.mode = mk_uni(od.mode); ow.nseg = mk_uni(od.nseg);
-    ow.st0 = mk_uni(od.seg_tiles[0]); ow.st1 = mk_uni(od.seg_tiles[1]);
-    const int oK = ow.K, omode = ow.mode, otiles = mk_uni(od.tiles), oS = mk_uni(od.S), oKR = mk_uni(od.KR);
-    const int owpu = mk_uni(od.wpu), osubs = mk_uni(od.subs), oxsrc = mk_uni(od.xsrc);
+    const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
+    const MkGeo q0 = mk_geo(a, od, wave);
+    const MkW& ow = q0.ow;
+    const int oK = ow.K, omode = ow.mode, oS = mk_uni(od.S), oKR = mk_uni(od.KR);
+    const int osubs = q0.subs, oxsrc = mk_uni(od.xsrc);
     const float* oX = mk_uni(od.X);
     const uint16_t* ogamma = mk_uni(od.gamma);
-    const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
-    const int G = a.G, M = a.M;
-    const int s = blockIdx.x % oS, g = blockIdx.x / oS, gs = G / oS;
-    const int k0 = s * oKR, KR = oKR, ldk = KR + 8;
-    const int nsub = mk_units(otiles, oS, osubs, G);
+    const int M = a.M;
+    const int s = q0.s, g = q0.g, gs = q0.gs;
+    const int k0 = q0.k0, KR = oKR, ldk = KR + 8;
+    const int nsub = q0.nsub;
     if (nsub == 0) return;
     uint16_t* xh = (uint16_t*)smem;
     uint16_t* xl = xh + (size_t)M * ldk;
     float* red = (float*)(xl + (size_t)M * ldk);  // [2][8][256] wave partial tiles
     float* res = red + 2 * kNW * 256;             // [nsub][256] reduced tiles
     const int n = lane & 15, q = lane >> 4;
-    const int wpu = owpu, groups = kNW / wpu, gr = wave / wpu;
-    const bool streams = wave < kNW && gr < groups;
-    const int kw0 = (wave % wpu) * 512;
+    const int wpu = q0.wpu, groups = q0.groups;
+    const int kw0 = q0.kw0;
     const int nround = (nsub + groups - 1) / groups;
-    auto uptr = [&](int r) -> const uint16_t* {
-        const int u = r * groups + gr;
-        if (!(streams && u < nsub)) return a.dummy + lane * 8;
-        const int tile = g + (osubs == 2 ? (u >> 1) : u) * gs;
-        return mk_row(ow, a.hd, tile, osubs == 2 ? (u & 1) : 0, n) + k0 + kw0 + 16 * q;
-    };
-    auto ustride = [&](int r) { const int u = r * groups + gr; return (streams && u < nsub) ? 8 : 0; };
-    MkBuf bf;
-    // The first weight unit is requested before anything else; activation rows follow.
-    if (wave < kNW) mk_issue(bf, uptr(0), ustride(0));
+    // The first kMkPreSteps slices of the first weight unit were requested before this call
+    // (during the grid barrier); the rest of it, then the activation rows, follow.
+    {
+        int st0;
+        const uint16_t* p0 = mk_uptr(a, q0, 0, n, q, lane, st0);
+        mk_issue<kMkPreSteps, 8>(bf, p0, st0);
+    }
     asm volatile("" ::: "memory");
-    // Norm gain slice (one 16-byte word per thread) into LDS, in the reduction area.
-    uint16_t* gl = (uint16_t*)red;
     float* ssq = red + 2048;  // [kMkMaxRows][8] wave partials of the rows' sums of squares
-    // gain of this K-range (the ones vector, which covers one whole range, when there is no norm)
-    const uint16_t* gam = ogamma ? ogamma + k0 : a.ones;
-    mk_u4 gword = {0, 0, 0, 0};
-    if (tid * 8 < KR) gword = *(mk_gu4p)(gam + tid * 8);
-    if (tid * 8 < KR) *(mk_u4*)(gl + tid * 8) = gword;
-    __syncthreads();
-    // Stage rows in passes of four: x (times the gain) as a bf16 hi/lo pair in LDS.
-    const int n4 = KR / 4;
-    for (int m0 = 0; m0 < M; m0 += 4) {
-        float4 xv[4][2];
+    // Epilogue inputs that come from memory (output row map, residual, RoPE factors) for this
+    // workgroup's first kPreTiles tiles, requested together with the activation rows.  Element
+    // (m, c) of a tile belongs to thread 16 m + c of the first 256.
+    const int em = tid >> 4, ec = tid & 15;
+    const int ntile = nsub / osubs;
+    const int oldy = mk_uni(od.ldy), ores_embed = mk_uni(od.res_embed);
+    const float* oxres = mk_uni(od.xres);
+    const int32_t* oout_map = mk_uni(od.out_map);
+    constexpr int kPreTiles = 2;
+    float pre0[kPreTiles] = {0.f, 0.f}, pre1[kPreTiles] = {0.f, 0.f};
+    int orow = em;
+    if (em < M) {
+        if (omode == kEpiStore) {
+            if (oout_map) orow = mk_ldi(oout_map + em);
+        } else if (omode == kEpiAdd) {
+            if (!ores_embed) {
 #pragma unroll
-        for (int mm = 0; mm < 4; ++mm)
+                for (int jt = 0; jt < kPreTiles; ++jt)
+                    if (jt < ntile) pre0[jt] = mk_ldg(oxres + (size_t)em * oldy + (g + jt * gs) * 16 + ec);
+            }
+        } else if (omode == kEpiQkv) {
+            const int pos = rp.pos[em], pp = pos < 0 ? 0 : pos, half = a.hd / 2, per_head = a.hd / 16;
+#pragma unroll
+            for (int jt = 0; jt < kPreTiles; ++jt) {
+                int lt = g + jt * gs;
+                if (jt < ntile && lt < ow.st0 + ow.st1) {  // Q and K tiles are rotated
+                    if (lt >= ow.st0) lt -= ow.st0;
+                    const int i = 8 * (lt % per_head) + (ec & 7);
+                    pre0[jt] = mk_ldg(a.rcos + (size_t)pp * half + i);
+                    pre1[jt] = mk_ldg(a.rsin + (size_t)pp * half + i);
+                }
+            }
+        }
+    }
+    // Stage rows in passes of eight: x (times the gain) as a bf16 hi/lo pair in LDS.  Each thread
+    // reads the gain of its own columns (bf16 ones when the phase has no norm).
+    const int n4 = KR / 4;
+    uint2 gw[2];
+#pragma unroll
+    for (int jc = 0; jc < 2; ++jc) {
+        const int c = tid + 512 * jc;
+        gw[jc] = make_uint2(0x3f803f80u, 0x3f803f80u);
+        if (ogamma && c < n4) {
+            const mk_u2 w = *(mk_gu2p)(ogamma + k0 + 4 * c);
+            gw[jc] = make_uint2(w.x, w.y);
+        }
+    }
+    for (int m0 = 0; m0 < M; m0 += 8) {
+        float4 xv[8][2];
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm)
 #pragma unroll
             for (int jc = 0; jc < 2; ++jc) {
                 const int m = m0 + mm, c = tid + 512 * jc;
@@ -292,7 +331,7 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                 }
             }
 #pragma unroll
-        for (int mm = 0; mm < 4; ++mm) {
+        for (int mm = 0; mm < 8; ++mm) {
             const int m = m0 + mm;
             if (m >= M) break;
             float sq = 0.f;
@@ -301,9 +340,9 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                 const int c = tid + 512 * jc;
                 if (tid < kNT && c < n4) {
                     const float4 v = xv[mm][jc];
-                    const uint2 gw = *(const uint2*)(gl + 4 * c);
-                    const mk_f2 a0 = {v.x * __uint_as_float(gw.x << 16), v.y * __uint_as_float(gw.x & 0xffff0000u)};
-                    const mk_f2 a1 = {v.z * __uint_as_float(gw.y << 16), v.w * __uint_as_float(gw.y & 0xffff0000u)};
+                    const uint2 gg = gw[jc];
+                    const mk_f2 a0 = {v.x * __uint_as_float(gg.x << 16), v.y * __uint_as_float(gg.x & 0xffff0000u)};
+                    const mk_f2 a1 = {v.z * __uint_as_float(gg.y << 16), v.w * __uint_as_float(gg.y & 0xffff0000u)};
                     const mk_bf16x2 h0 = __builtin_convertvector(a0, mk_bf16x2), h1 = __builtin_convertvector(a1, mk_bf16x2);
                     const mk_bf16x2 l0 = __builtin_convertvector(a0 - __builtin_convertvector(h0, mk_f2), mk_bf16x2);
                     const mk_bf16x2 l1 = __builtin_convertvector(a1 - __builtin_convertvector(h1, mk_f2), mk_bf16x2);
@@ -365,7 +404,11 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
     for (; r + 1 < nround; ++r) {
         mk_f4 acc = {0.f, 0.f, 0.f, 0.f};
         if (wave < kNW) acc = mma();
-        if (wave < kNW) mk_issue(bf, uptr(r + 1), ustride(r + 1));
+        if (wave < kNW) {
+            int st1;
+            const uint16_t* p1 = mk_uptr(a, q0, r + 1, n, q, lane, st1);
+            mk_issue(bf, p1, st1);
+        }
         if (wave < kNW) put(acc, r & 1);
         if (r & 1) reduce(r - 1, 2);
     }
@@ -378,27 +421,23 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
     else reduce(r, 1);
 
     // ---- epilogue: element (m, c) of a tile is held by thread 16 m + c of the first 256 ----
-    const int em = tid >> 4, ec = tid & 15;
-    const int ntile = nsub / osubs;
-    const int oldy = mk_uni(od.ldy), ores_embed = mk_uni(od.res_embed), olayer = mk_uni(od.layer);
+    const int olayer = mk_uni(od.layer);
     float* oY = mk_uni(od.Y);
     float* oss_out = mk_uni(od.ss_out);
-    const float* oxres = mk_uni(od.xres);
-    const int32_t* oout_map = mk_uni(od.out_map);
     float* oqout = mk_uni(od.qout);
-    auto epilogue = [&](int tile, float v0, float v1) {
+    auto epilogue = [&](int jt, float v0, float v1) {
+        const int tile = g + jt * gs;
         // every thread of the first 256 calls this (sums of squares need whole 16-lane groups)
         const bool valid = em < M;
         if (omode == kEpiStore) {
-            if (valid) {
-                const int orow = oout_map ? mk_ldi(oout_map + em) : em;
-                if (orow >= 0) mk_stf(oY + (size_t)orow * oldy + tile * 16 + ec, v0);
-            }
+            if (valid && orow >= 0) mk_stf(oY + (size_t)orow * oldy + tile * 16 + ec, v0);
         } else if (omode == kEpiAdd) {
             float nv = 0.f;
             if (valid) {
                 const int col = tile * 16 + ec;
-                const float res0 = ores_embed ? mk_embed_at(a, rp, em, col) : mk_ldg(oxres + (size_t)em * oldy + col);
+                const float res0 = ores_embed ? mk_embed_at(a, rp, em, col)
+                                   : jt < kPreTiles ? (jt == 0 ? pre0[0] : pre0[1])
+                                                    : mk_ldg(oxres + (size_t)em * oldy + col);
                 nv = res0 + v0;
                 mk_stf(oY + (size_t)em * oldy + col, nv);
             }
@@ -424,7 +463,14 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
             float out = v0;
             if (seg < 2) {
                 const int pp = pos < 0 ? 0 : pos;
-                const float c = mk_ldg(a.rcos + (size_t)pp * half + i), sn = mk_ldg(a.rsin + (size_t)pp * half + i);
+                float c, sn;
+                if (jt < kPreTiles) {
+                    c = jt == 0 ? pre0[0] : pre0[1];
+                    sn = jt == 0 ? pre1[0] : pre1[1];
+                } else {
+                    c = mk_ldg(a.rcos + (size_t)pp * half + i);
+                    sn = mk_ldg(a.rsin + (size_t)pp * half + i);
+                }
                 out = ec < 8 ? v0 * c - partner * sn : v0 * c + partner * sn;
             }
             if (seg == 0) {
@@ -438,11 +484,10 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
     };
     if (oS == 1) {
         for (int jt = 0; jt < ntile; ++jt) {
-            const int tile = g + jt * gs;
             if (tid < 256) {
                 const float v0 = res[(jt * osubs) * 256 + tid];
                 const float v1 = osubs == 2 ? res[(jt * 2 + 1) * 256 + tid] : v0;
-                epilogue(tile, v0, v1);
+                epilogue(jt, v0, v1);
             }
         }
         return;
@@ -484,7 +529,7 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                 v0 += p0[s0];
                 v1 += p1[s0];
             }
-            epilogue(tile, v0, osubs == 2 ? v1 : v0);
+            epilogue(jt, v0, osubs == 2 ? v1 : v0);
         }
     }
 }
@@ -752,6 +797,55 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
     }
 }
 
+// Grid barrier at the start of a phase.  Counters: one per XCD group (workgroup id mod 8), one
+// global, one release line per group; all of them only grow (generation g of the barrier: a group
+// counter reaches g * workgroups-in-group, the global one g * groups), so no counter is ever reset
+// and nothing waits for a store to complete on the barrier's path.  The last arriver of a group
+// counts the group in; the last group publishes generation g on the 8 release lines that the
+// groups' control threads poll.
+//
+// With a weight buffer (projection phases) the phase's first weight unit is requested after this
+// workgroup's arrival has been counted, so that it streams during the barrier: waves 1..7 skip
+// the arrival code and issue at once; wave 0 issues once its control lane has the atomics'
+// results, which would otherwise wait for those loads.  The buffer is local to the projection
+// phase, so it holds no registers in other phases.
+__device__ __forceinline__ void mk_barrier(const MkArgs& a, int& gen, long& spins, const MkPhase* ph, MkBuf* bf) {
+    int32_t* base = a.bar;
+    const int x = blockIdx.x & 7;
+    const unsigned g1 = (unsigned)gen + 1u;
+    if (threadIdx.x == kCtl) {
+        const unsigned ngroup = a.G < 8 ? a.G : 8;
+        const unsigned per = a.G / 8 + (x < a.G % 8 ? 1 : 0);
+        const unsigned prev = (unsigned)mk_add(base + (2 + x) * kMkLine, 1);
+        if (prev + 1u == g1 * per) {
+            const unsigned gp = (unsigned)mk_add(base + kMkLine, 1);
+            if (gp + 1u == g1 * ngroup)
+                for (int i = 0; i < 8; ++i) mk_sti(base + (10 + i) * kMkLine, (int)g1);
+        }
+    }
+    if (bf) {
+        const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
+        const MkGeo q = mk_geo(a, *ph, wave);
+        int st;
+        const uint16_t* wp = mk_uptr(a, q, 0, lane & 15, lane >> 4, lane, st);
+        mk_issue<0, kMkPreSteps>(*bf, wp, st);
+    }
+    if (threadIdx.x == kCtl) {
+        gen = (int)g1;
+        if (spins >= 0) {
+            while ((int)((unsigned)mk_ld(base + (10 + x) * kMkLine) - g1) < 0) {
+                if (++spins > kMkSpin) {
+                    mk_sti(a.err, 1);
+                    spins = -1;  // give up waiting for the rest of the launch (results invalid)
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+    }
+    __builtin_amdgcn_s_barrier();
+}
+
 __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ MkPhase op_lds[2];
@@ -777,15 +871,26 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
         uint32_t nw = 0;
         if (threadIdx.x < kWords && p + 1 < a.nphase) nw = mk_ldu((const uint32_t*)&a.prog[p + 1] + threadIdx.x);
         if (op == kMkGemv) {
-            mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag);
+            MkBuf bf;  // weight unit in flight, per wave
+            if (p > 0) {
+                mk_barrier(a, gen, spins, &o, &bf);
+            } else {
+                const int tid = mk_tid(), lane = tid & 63;
+                const MkGeo q = mk_geo(a, o, tid >> 6);
+                int st;
+                const uint16_t* wp = mk_uptr(a, q, 0, lane & 15, lane >> 4, lane, st);
+                mk_issue<0, kMkPreSteps>(bf, wp, st);
+            }
+            mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag, bf);
         } else if (op == kMkAttn) {
+            if (p > 0) mk_barrier(a, gen, spins, nullptr, nullptr);
             if (a.hd == 64) mk_attn_t<64>(a, o, rp, smem, &last_flag);
             else if (a.hd == 128) mk_attn_t<128>(a, o, rp, smem, &last_flag);
             else mk_attn_t<32>(a, o, rp, smem, &last_flag);
         }
         mk_vmwait();  // this phase's stores are complete before the workgroup counts in
         if (threadIdx.x < kWords && p + 1 < a.nphase) ((uint32_t*)&op_lds[(p + 1) & 1])[threadIdx.x] = nw;
-        if (p + 1 < a.nphase) mk_barrier(a, gen, spins);
+        __syncthreads();  // next descriptor in LDS; this phase's LDS use is over
         if (a.trace && blockIdx.x == 0 && threadIdx.x == kCtl && p + 1 < kMkTracePhases) a.trace[p + 1] = wall_clock64();
     }
 }
