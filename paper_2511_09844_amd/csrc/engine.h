@@ -134,7 +134,7 @@ void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, i
 void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps);
 // Final-norm LM head of `rows` residual rows into Y[out_map[r]] (bf16 path via the projection kernel).
 void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map);
-void launch_steer(Engine& e, const float* X, const float* ss, int nss, const int32_t* in_map, int rows);
+void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows);
 enum Epi { kEpiStore = 0, kEpiAdd = 1, kEpiSwiglu = 2, kEpiQkv = 3 };
 
 // One bf16 weight-streaming projection (see wsgemv.hip).

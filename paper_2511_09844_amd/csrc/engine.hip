@@ -198,6 +198,8 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
             st.bar = cv.take<int32_t>(kMkBarInts);
             st.err = cv.take<int32_t>(64);
             st.cnt = cv.take<int32_t>(mk_counter_ints(c));
+            st.dummy = cv.take<uint16_t>(512);
+            st.ones = cv.take<uint16_t>(kMkMaxKR);
             st.trace = cv.take<int64_t>((size_t)kMkMaxLaunch * kMkTracePhases);
         }
         if (mk) *mk = st;
@@ -279,7 +281,7 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
         hipError_t err = mk_launch(e, 0);
         if (err != hipSuccess) { e.launch_err = err; return; }
         launch_verify_decide(s, e, out_tokens, out_counts);
-        launch_steer(e, e.mk.final_x, e.mk.final_ss, e.mk.final_nss, e.ws.steer_map, B);
+        launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
         return;
     }
     for (int j = 1; j <= k; ++j) {
@@ -294,7 +296,7 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
     for (int l = 0; l < e.mv.dm.n_layers; ++l) launch_layer(s, e, e.mv, l, rows, k + 1);
     launch_lm_head(e, e.mv, rows, e.ws.logits_v, nullptr);
     launch_verify_decide(s, e, out_tokens, out_counts);
-    launch_steer(e, e.mv.x, e.mv.ss, e.mv.dm.d_model / 16, e.ws.steer_map, B);
+    launch_steer(e, e.mv.x, e.mv.ss, e.ws.steer_map, B);
 }
 
 void drop_graph(Engine& e) {
@@ -431,7 +433,7 @@ sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, con
         for (int l = 0; l < e->mv.dm.n_layers; ++l) launch_layer(s, *e, e->mv, l, rows, chunk);
         launch_prefill_capture(s, *e, rows, lens, max_prompt);
     }
-    launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, e->mv.dm.d_model / 16, nullptr, batch);
+    launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, nullptr, batch);
     for (int c = 0; c < nchunks; ++c) {
         launch_plan_embed(s, *e, e->md, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
         for (int l = 0; l < e->md.dm.n_layers; ++l) launch_layer(s, *e, e->md, l, rows, chunk);

@@ -460,10 +460,10 @@ void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* o
                 kEpiStore, Y, m.dm.vocab, out_map);
 }
 
-void launch_steer(Engine& e, const float* X, const float* ss, int nss, const int32_t* in_map, int rows) {
+void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows) {
     if (e.bf16) {
         WsCall c = ws_base(e, e.mv);
-        c.X = X; c.in_map = in_map; c.M = rows; c.K = e.mv.dm.d_model; c.gamma = e.mv.final_norm; c.ss = ss; c.nss = nss;
+        c.X = X; c.in_map = in_map; c.M = rows; c.K = e.mv.dm.d_model; c.gamma = e.mv.final_norm; c.ss = ss;
         c.W[0] = e.w_steer; c.seg_rows[0] = e.md.dm.d_model; c.nseg = 1; c.mode = kEpiStore;
         c.Y = e.ws.steer; c.ldy = e.md.dm.d_model;
         launch_wsgemv(&e, e.stream, c);
