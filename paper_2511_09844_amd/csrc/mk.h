@@ -13,7 +13,7 @@ constexpr int kMkWaves = 8;                      // weight-streaming waves per w
 constexpr int kMkThreads = kMkWaves * 64;
 constexpr int kMkMaxRows = 16;                   // activation rows per launch
 constexpr int kMkSpan = 64;                      // cache positions per attention unit
-constexpr int kMkMaxNq = 32;                     // query vectors per attention unit (8 waves x 4)
+constexpr int kMkMaxNq = 32;                     // query vectors per (sequence, KV head): rows x query heads per KV head
 constexpr int kMkMaxKR = 4096;                   // K-range staged per workgroup
 constexpr int kMkLdsBudget = 150 * 1024;         // dynamic LDS per workgroup
 constexpr int kMkLine = 32;                      // ints per 128-byte line

@@ -535,14 +535,115 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
 }
 
 // ---------------------------------------------------------------------------------------------
-// Attention phase: units (sequence, KV head, span of kMkSpan positions).  A unit scores all
-// query vectors of the sequence's rows for the KV head's query heads against its span (one wave
-// per query vector, one lane per position), writes an un-normalised partial (output, max, sum),
-// and the last span of a (sequence, KV head) to arrive merges all live spans in span order.
-// Positions beyond the longest query row of the sequence are never loaded.
+// Attention phase: units (sequence, KV head, group of up to kMkQG query vectors, span of kMkSpan
+// positions).  The query vectors of a sequence's rows for a KV head's query heads are numbered
+// (row, head) row-major and cut into groups of kMkQG, one vector per wave.  A unit scores its
+// group against its span (one lane per position), writes an un-normalised partial (output, max,
+// sum), and the last span of a (sequence, KV head, group) to arrive merges all live spans in span
+// order.  Positions beyond the group's last query position are never loaded.
+//
+// Cache rows written by earlier launches do not depend on this launch, so a workgroup requests
+// those of its first unit while the grid barrier in front of the phase is still open; only the
+// rows this launch appends (positions from the sequence's first row on) and the queries are
+// read after it.  A cache line holds one row (hd >= 32 floats), so the early reads never bring a
+// line that this launch writes into a cache.
 // ---------------------------------------------------------------------------------------------
+constexpr int kMkQG = kMkWaves;  // query vectors per attention unit
+
 template <int HD>
-__device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, int* last_flag) {
+struct MkKv {
+    static constexpr int F4 = kMkSpan * HD / 4 / kMkThreads;  // float4 of K (and of V) per thread
+    float4 k[F4], v[F4];
+};
+
+struct MkAttnUnit {
+    int sp, kvh, sq, qg, q0, nqu, p0, nvalid, nl, newpos;
+};
+
+// Spans any row of the launch sees: units are numbered over these only.
+__device__ __forceinline__ int mk_attn_spans(const MkArgs& a, const MkRows& rp, int nsplit) {
+    int mx = -1;
+    for (int r = 0; r < a.M; ++r) mx = max(mx, rp.pos[r]);
+    return mx >= 0 ? min(nsplit, mx / kMkSpan + 1) : 1;
+}
+
+__device__ __forceinline__ MkAttnUnit mk_attn_unit(const MkArgs& a, const MkRows& rp, int nsplit, int nspan, int u) {
+    MkAttnUnit t;
+    const int Gq = a.H / a.Hkv, nq = a.rps * Gq, nqg = (nq + kMkQG - 1) / kMkQG;
+    t.sp = u % nspan;
+    int r = u / nspan;
+    t.qg = r % nqg;
+    r /= nqg;
+    t.kvh = r % a.Hkv;
+    t.sq = r / a.Hkv;
+    t.q0 = t.qg * kMkQG;
+    t.nqu = min(kMkQG, nq - t.q0);
+    int maxq = -1, minq = 0x7fffffff;
+    for (int i = 0; i < a.rps; ++i) {
+        const int ps = rp.pos[t.sq * a.rps + i];
+        if (i >= t.q0 / Gq && i <= (t.q0 + t.nqu - 1) / Gq) maxq = max(maxq, ps);
+        if (ps >= 0) minq = min(minq, ps);
+    }
+    t.p0 = t.sp * kMkSpan;
+    t.nvalid = maxq >= t.p0 ? min(kMkSpan, maxq - t.p0 + 1) : 0;
+    // live spans of the group (those holding a position one of its queries sees)
+    t.nl = maxq >= 0 ? min(nsplit, maxq / kMkSpan + 1) : 0;
+    t.newpos = minq;  // first position this launch appends for the sequence
+    return t;
+}
+
+// K and V rows of a unit's span held by this thread: rows older than the launch (fresh = false)
+// or the rows it appends (fresh = true).  Rows past the last valid one re-read it.
+template <int HD>
+__device__ __forceinline__ void mk_attn_kv(const MkArgs& a, const MkRows& rp, int layer, const MkAttnUnit& t, bool fresh,
+                                           MkKv<HD>& kv) {
+    if (t.nvalid == 0) return;
+    const int tid = mk_tid();
+    const size_t head_base = (((size_t)layer * a.max_batch + rp.seq[t.sq * a.rps]) * a.Hkv + t.kvh) * a.cap * HD;
+    const float* kg = a.kc + head_base + (size_t)t.p0 * HD;
+    const float* vg = a.vc + head_base + (size_t)t.p0 * HD;
+#pragma unroll
+    for (int i = 0; i < MkKv<HD>::F4; ++i) {
+        const int e4 = tid + i * kMkThreads;
+        const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
+        const int jj = j < t.nvalid ? j : t.nvalid - 1;
+        if ((t.p0 + jj >= t.newpos) == fresh) {
+            kv.k[i] = mk_ldg4(kg + (size_t)jj * HD + d);
+            kv.v[i] = mk_ldg4(vg + (size_t)jj * HD + d);
+        }
+    }
+}
+
+// Wave-wide max / sum through DPP row operations (no LDS round trips): pairs, quads, half rows
+// and rows by swaps and mirrors, then rows 0-3 folded into row 3 by the row broadcasts; the
+// result of lane 63 is returned to every lane.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float mk_dpp(float old, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old), __builtin_bit_cast(int, v),
+                                                                 CTRL, ROWS, 0xf, false));
+}
+__device__ __forceinline__ float mk_wmax(float v) {
+    v = fmaxf(v, mk_dpp<0xB1, 0xf>(v, v));   // quad_perm [1,0,3,2]
+    v = fmaxf(v, mk_dpp<0x4E, 0xf>(v, v));   // quad_perm [2,3,0,1]
+    v = fmaxf(v, mk_dpp<0x141, 0xf>(v, v));  // row_half_mirror
+    v = fmaxf(v, mk_dpp<0x140, 0xf>(v, v));  // row_mirror
+    v = fmaxf(v, mk_dpp<0x142, 0xa>(v, v));  // row_bcast:15 into rows 1 and 3
+    v = fmaxf(v, mk_dpp<0x143, 0xc>(v, v));  // row_bcast:31 into rows 2 and 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+__device__ __forceinline__ float mk_wsum(float v) {
+    v += mk_dpp<0xB1, 0xf>(0.f, v);
+    v += mk_dpp<0x4E, 0xf>(0.f, v);
+    v += mk_dpp<0x141, 0xf>(0.f, v);
+    v += mk_dpp<0x140, 0xf>(0.f, v);
+    v += mk_dpp<0x142, 0xa>(0.f, v);
+    v += mk_dpp<0x143, 0xc>(0.f, v);
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+template <int HD>
+__device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, int* last_flag,
+                                          MkKv<HD>& kv) {
     struct {
         int nsplit, layer;
         const float* qout;
@@ -557,165 +658,141 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
     o.cnt = mk_uni(od.cnt);
     const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
     const int Gq = a.H / a.Hkv;
-    const int nq = a.rps * Gq;
+    const int nq = a.rps * Gq, nqg = (nq + kMkQG - 1) / kMkQG;
     const int nseq = a.M / a.rps;
-    const int nunit = nseq * a.Hkv * o.nsplit;
-    float* qs = (float*)smem;                 // [nq][HD]   pre-scaled queries
-    float* ks = qs + kMkMaxNq * HD;           // [64][HD+4]
-    float* vs = ks + kMkSpan * (HD + 4);      // [64][HD]
-    float* ps = vs + kMkSpan * HD;            // [nq][64]   probabilities
-    float* mq = ps + kMkMaxNq * kMkSpan;      // [nq] span max
-    float* lq = mq + kMkMaxNq;                // [nq] span sum
+    const int nspan = mk_attn_spans(a, rp, o.nsplit);
+    const int nunit = nseq * a.Hkv * nqg * nspan;
+    constexpr int F4 = MkKv<HD>::F4;
+    constexpr int D4 = HD / 4;
+    float* qs = (float*)smem;                 // [kMkQG][HD]   pre-scaled queries
+    float* ks = qs + kMkQG * HD;              // [kMkSpan][HD+4]
+    float* vs = ks + kMkSpan * (HD + 4);      // [kMkSpan][HD]
+    float* ps = vs + kMkSpan * HD;            // [kMkQG][kMkSpan] probabilities
+    float* mq = ps + kMkSpan * kMkQG;         // [kMkQG] span max
+    float* lq = mq + kMkQG;                   // [kMkQG] span sum
     for (int u = blockIdx.x; u < nunit; u += a.G) {
-        const int sp = u % o.nsplit;
-        const int kvh = (u / o.nsplit) % a.Hkv;
-        const int sq = u / (o.nsplit * a.Hkv);
-        int maxq = -1;
-        for (int i = 0; i < a.rps; ++i) maxq = max(maxq, rp.pos[sq * a.rps + i]);
-        const int p0 = sp * kMkSpan;
-        const int nvalid = maxq >= p0 ? min(kMkSpan, maxq - p0 + 1) : 0;
-        // live spans of this sequence (those holding a position some query sees)
-        const int nl = maxq >= 0 ? min(o.nsplit, maxq / kMkSpan + 1) : 0;
+        const MkAttnUnit t = mk_attn_unit(a, rp, o.nsplit, nspan, u);
+        const int sp = t.sp, kvh = t.kvh, sq = t.sq, nl = t.nl, nvalid = t.nvalid, q0 = t.q0, nqu = t.nqu;
         if (nl == 0 && sp == 0) {
             // no live position (padding): the outputs are zero
-            for (int e = tid; e < nq * HD; e += kMkThreads) {
-                const int qi = e / HD, d = e % HD;
-                mk_stf(o.aout + (size_t)(sq * a.rps + qi / Gq) * a.H * HD + (kvh * Gq + qi % Gq) * HD + d, 0.f);
+            for (int e = tid; e < nqu * HD; e += kMkThreads) {
+                const int qv = q0 + e / HD, d = e % HD;
+                mk_stf(o.aout + (size_t)(sq * a.rps + qv / Gq) * a.H * HD + (kvh * Gq + qv % Gq) * HD + d, 0.f);
             }
         }
         if (nvalid == 0) continue;  // dead span: no work and no hand-off
         {
-            const size_t head_base = (((size_t)o.layer * a.max_batch + rp.seq[sq * a.rps]) * a.Hkv + kvh) * a.cap * HD;
-            const float* kg = a.kc + head_base + (size_t)p0 * HD;
-            const float* vg = a.vc + head_base + (size_t)p0 * HD;
-            // every load of the unit is issued before any is used: K and V rows of the span (rows
-            // past the last valid one re-read it; masked below) and the queries
-            constexpr int F4 = kMkSpan * HD / 4 / kMkThreads;   // float4 of K (and of V) per thread
-            constexpr int Q4 = (kMkMaxNq * HD / 4 + kMkThreads - 1) / kMkThreads;  // float4 of queries per thread
-            float4 kv4[F4], vv4[F4], qv4[Q4];
-#pragma unroll
-            for (int i = 0; i < F4; ++i) {
-                const int e4 = tid + i * kMkThreads;
-                const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
-                const int jj = j < nvalid ? j : nvalid - 1;
-                kv4[i] = mk_ldg4(kg + (size_t)jj * HD + d);
-                vv4[i] = mk_ldg4(vg + (size_t)jj * HD + d);
-            }
+            // rows of this launch (and, past the first unit, all rows) and the queries
+            if (u != (int)blockIdx.x) mk_attn_kv<HD>(a, rp, o.layer, t, false, kv);
+            mk_attn_kv<HD>(a, rp, o.layer, t, true, kv);
+            constexpr int Q4 = (kMkQG * D4 + kMkThreads - 1) / kMkThreads;  // float4 of queries per thread
+            float4 qv4[Q4];
 #pragma unroll
             for (int i = 0; i < Q4; ++i) {
-                const int e = (tid + i * kMkThreads) * 4;
-                const int qi = e / HD, d = e % HD;
-                const int qc = qi < nq ? qi : 0;  // also keeps e past kMkMaxNq*HD in bounds
-                const int row = sq * a.rps + qc / Gq, h = kvh * Gq + qc % Gq;
+                const int e = tid + i * kMkThreads;
+                const int qi = e / D4, d = (e % D4) * 4;
+                const int qv = q0 + (qi < nqu ? qi : 0);  // vectors past the group repeat its first
+                const int row = sq * a.rps + qv / Gq, h = kvh * Gq + qv % Gq;
                 qv4[i] = mk_ldg4(o.qout + (size_t)row * a.H * HD + h * HD + d);
             }
 #pragma unroll
             for (int i = 0; i < F4; ++i) {
                 const int e4 = tid + i * kMkThreads;
                 const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
-                *(float4*)(ks + j * (HD + 4) + d) = kv4[i];
-                *(float4*)(vs + j * HD + d) = vv4[i];
+                *(float4*)(ks + j * (HD + 4) + d) = kv.k[i];
+                *(float4*)(vs + j * HD + d) = kv.v[i];
             }
 #pragma unroll
             for (int i = 0; i < Q4; ++i) {
-                const int e = (tid + i * kMkThreads) * 4;
+                const int e = tid + i * kMkThreads;
                 const float4 v = qv4[i];
-                if (e < kMkMaxNq * HD) *(float4*)(qs + e) = make_float4(v.x * a.scale, v.y * a.scale, v.z * a.scale, v.w * a.scale);
+                if (e < kMkQG * D4) *(float4*)(qs + 4 * e) = make_float4(v.x * a.scale, v.y * a.scale, v.z * a.scale, v.w * a.scale);
             }
             __syncthreads();
-            // scores, one lane per position: with few query vectors one wave per vector, else wave
-            // w takes vectors 4w..4w+3 so that a K row read from LDS feeds four dot products
-            const bool few = nq <= kMkWaves;
-            const int qw = few ? 1 : 4;
-            if (qw * wave < nq) {
-                float sc[4] = {0.f, 0.f, 0.f, 0.f};
+            // scores and probabilities: wave w takes query vector w of the group, lane = position
+            if (wave < nqu) {
+                // blocks of 32 head dims: all of a block's K and query words are requested from LDS
+                // before its products (two accumulators)
+                float sc0 = 0.f, sc1 = 0.f;
                 const float4* kr = (const float4*)(ks + lane * (HD + 4));
-                if (few) {
-                    const float4* qr = (const float4*)(qs + wave * HD);
-#pragma unroll 4
-                    for (int d4 = 0; d4 < HD / 4; ++d4) {
-                        const float4 kv = kr[d4], qv = qr[d4];
-                        sc[0] += qv.x * kv.x + qv.y * kv.y + qv.z * kv.z + qv.w * kv.w;
-                    }
-                } else {
-#pragma unroll 2
-                    for (int d4 = 0; d4 < HD / 4; ++d4) {
-                        const float4 kv = kr[d4];
+                const float4* qr = (const float4*)(qs + wave * HD);
+#pragma unroll 1
+                for (int d0 = 0; d0 < D4; d0 += 8) {
+                    float4 kx[8], qx[8];
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float4 qv = ((const float4*)(qs + (4 * wave + i) * HD))[d4];
-                            sc[i] += qv.x * kv.x + qv.y * kv.y + qv.z * kv.z + qv.w * kv.w;
-                        }
+                    for (int i = 0; i < 8; ++i) {
+                        kx[i] = kr[d0 + i];
+                        qx[i] = qr[d0 + i];
+                    }
+#pragma unroll
+                    for (int i = 0; i < 8; i += 2) {
+                        sc0 += qx[i].x * kx[i].x + qx[i].y * kx[i].y + qx[i].z * kx[i].z + qx[i].w * kx[i].w;
+                        sc1 += qx[i + 1].x * kx[i + 1].x + qx[i + 1].y * kx[i + 1].y + qx[i + 1].z * kx[i + 1].z +
+                               qx[i + 1].w * kx[i + 1].w;
                     }
                 }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int qi = qw * wave + i;
-                    if (i >= qw || qi >= nq) break;
-                    const int qp = rp.pos[sq * a.rps + qi / Gq];
-                    const float v = (lane < nvalid && p0 + lane <= qp) ? sc[i] : -INFINITY;
-                    const float mx = wave_max(v);
-                    const float pr = v == -INFINITY ? 0.f : expf(v - mx);
-                    const float sm = wave_sum(pr);
-                    ps[lane * kMkMaxNq + qi] = pr;  // [position][query]
-                    if (lane == 0) { mq[qi] = mx; lq[qi] = sm; }
+                const float sc = sc0 + sc1;
+                const int qv = q0 + wave;
+                const int qp = rp.pos[sq * a.rps + qv / Gq];
+                const float v = (lane < nvalid && t.p0 + lane <= qp) ? sc : -INFINITY;
+                const float mx = mk_wmax(v);
+                const float pr = v == -INFINITY ? 0.f : expf(v - mx);
+                const float sm = mk_wsum(pr);
+                ps[wave * kMkSpan + lane] = pr;  // [query][position]
+                if (lane == 0) {
+                    mq[wave] = mx;
+                    lq[wave] = sm;
                 }
             }
             __syncthreads();
-            // un-normalised outputs: with few query vectors a thread per (vector, head dim), else
-            // wave -> (block of 8 vectors, 64 head dims); the probabilities of a position are read
-            // as a broadcast, each V element once per block
-            if (few) {
-                for (int e = tid; e < nq * HD; e += kMkThreads) {
-                    const int qi = e / HD, d = e % HD;
-                    float acc = 0.f;
-#pragma unroll 8
-                    for (int j = 0; j < kMkSpan; ++j) acc += ps[j * kMkMaxNq + qi] * vs[j * HD + d];
-                    const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
+            // un-normalised outputs: a thread per (query vector, head dim), NI vectors kMkThreads / HD
+            // apart; a position's probability is a broadcast read, its V element is read once
+            constexpr int STEP = kMkThreads / HD;  // vectors between a thread's items
+            constexpr int NI = (kMkQG + STEP - 1) / STEP;
+            static_assert(NI == 1 || NI * STEP == kMkQG, "a thread's items stay inside the group");
+            const int d = tid % HD, qi0 = tid / HD;  // qi0 < STEP
+            if (qi0 < nqu) {
+                float acc[NI];
+#pragma unroll
+                for (int i = 0; i < NI; ++i) acc[i] = 0.f;
+                // blocks of 16 positions: V elements and probabilities are all requested from LDS
+                // before the block's products
+#pragma unroll 1
+                for (int j0 = 0; j0 < kMkSpan; j0 += 16) {
+                    float vv[16];
+                    float4 pp[NI][4];
+#pragma unroll
+                    for (int jj = 0; jj < 16; ++jj) vv[jj] = vs[(j0 + jj) * HD + d];
+#pragma unroll
+                    for (int i = 0; i < NI; ++i)
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) pp[i][k] = *(const float4*)(ps + (qi0 + i * STEP) * kMkSpan + j0 + 4 * k);
+#pragma unroll
+                    for (int i = 0; i < NI; ++i)
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            acc[i] += pp[i][k].x * vv[4 * k];
+                            acc[i] += pp[i][k].y * vv[4 * k + 1];
+                            acc[i] += pp[i][k].z * vv[4 * k + 2];
+                            acc[i] += pp[i][k].w * vv[4 * k + 3];
+                        }
+                }
+#pragma unroll
+                for (int i = 0; i < NI; ++i) {
+                    const int qi = qi0 + i * STEP;
+                    if (qi >= nqu) break;
+                    const int qv = q0 + qi;
+                    const int row = sq * a.rps + qv / Gq, h = kvh * Gq + qv % Gq;
                     if (nl == 1) {
+                        // the only live span: normalise and write the output itself
                         const float l = lq[qi];
-                        mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, l > 0.f ? acc / l : 0.f);
+                        mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, l > 0.f ? acc[i] / l : 0.f);
                     } else {
                         float* pp = o.apart + (((size_t)row * a.H + h) * o.nsplit + sp) * (HD + 4);
-                        mk_stf(pp + d, acc);
+                        mk_stf(pp + d, acc[i]);
                         if (d == 0) {
                             mk_stf(pp + HD, mq[qi]);
                             mk_stf(pp + HD + 1, lq[qi]);
-                        }
-                    }
-                }
-            } else {
-                const int ndg = HD / 64 > 0 ? HD / 64 : 1;   // 64-wide groups of head dims
-                const int qb = wave / ndg, dg = wave % ndg;
-                const int d = dg * 64 + lane;
-                if (8 * qb < nq && d < HD) {
-                    float acc[8];
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
-#pragma unroll 2
-                    for (int j = 0; j < kMkSpan; ++j) {
-                        const float4 pa = *(const float4*)(ps + j * kMkMaxNq + 8 * qb);
-                        const float4 pb = *(const float4*)(ps + j * kMkMaxNq + 8 * qb + 4);
-                        const float v = vs[j * HD + d];
-                        acc[0] += pa.x * v; acc[1] += pa.y * v; acc[2] += pa.z * v; acc[3] += pa.w * v;
-                        acc[4] += pb.x * v; acc[5] += pb.y * v; acc[6] += pb.z * v; acc[7] += pb.w * v;
-                    }
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        const int qi = 8 * qb + i;
-                        if (qi >= nq) break;
-                        const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
-                        if (nl == 1) {
-                            // the only live span: normalise and write the output itself
-                            const float l = lq[qi];
-                            mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, l > 0.f ? acc[i] / l : 0.f);
-                        } else {
-                            float* pp = o.apart + (((size_t)row * a.H + h) * o.nsplit + sp) * (HD + 4);
-                            mk_stf(pp + d, acc[i]);
-                            if (d == 0) {
-                                mk_stf(pp + HD, mq[qi]);
-                                mk_stf(pp + HD + 1, lq[qi]);
-                            }
                         }
                     }
                 }
@@ -725,73 +802,70 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
             __syncthreads();  // LDS of this unit is reused by the next
             continue;
         }
-        // count in; the last live span of this (sequence, KV head) merges the live spans
+        // count in; the last live span of this (sequence, KV head, group) merges the live spans
         mk_vmwait();
         __syncthreads();
         if (tid == 0) {
-            int32_t* c = o.cnt + sq * a.Hkv + kvh;
+            int32_t* c = o.cnt + ((size_t)sq * a.Hkv + kvh) * nqg + t.qg;
             const int prev = mk_add(c, 1);
             *last_flag = prev == nl - 1;
             if (prev == nl - 1) mk_sti(c, 0);
         }
         __syncthreads();
-        if (*last_flag) {
+        if (*last_flag && tid < nqu * D4) {
             // a thread per (query vector, 4 head dims) requests the partial outputs and the
             // (max, sum) of sixteen spans at once and folds them into a running (max, sum, output)
-            constexpr int D4 = HD / 4;
-            for (int e = tid; e < nq * D4; e += kMkThreads) {
-                const int qi = e / D4, d = (e % D4) * 4;
-                const int row = sq * a.rps + qi / Gq, h = kvh * Gq + qi % Gq;
-                float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (rp.pos[row] >= 0) {
-                    const float* pb = o.apart + ((size_t)row * a.H + h) * o.nsplit * (HD + 4);
-                    float Mx = -INFINITY, L = 0.f;
-                    float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
-                    for (int s0 = 0; s0 < nl; s0 += 16) {
-                        float4 v[16];
-                        float2 ml[16];
+            const int qv = q0 + tid / D4, d = (tid % D4) * 4;
+            const int row = sq * a.rps + qv / Gq, h = kvh * Gq + qv % Gq;
+            float4 r = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (rp.pos[row] >= 0) {
+                const float* pb = o.apart + ((size_t)row * a.H + h) * o.nsplit * (HD + 4);
+                float Mx = -INFINITY, L = 0.f;
+                float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int s0 = 0; s0 < nl; s0 += 16) {
+                    float4 v[16];
+                    float2 ml[16];
 #pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            const float* e2 = pb + (size_t)min(s0 + i, nl - 1) * (HD + 4);
-                            v[i] = mk_ldg4(e2 + d);
-                            ml[i] = mk_ldg2(e2 + HD);
-                        }
-                        float cm = -INFINITY;
-#pragma unroll
-                        for (int i = 0; i < 16; ++i)
-                            if (s0 + i < nl) cm = fmaxf(cm, ml[i].x);
-                        if (cm == -INFINITY) continue;
-                        if (cm > Mx) {
-                            const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
-                            L *= sc;
-                            O.x *= sc;
-                            O.y *= sc;
-                            O.z *= sc;
-                            O.w *= sc;
-                            Mx = cm;
-                        }
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            if (s0 + i >= nl || ml[i].x == -INFINITY) continue;
-                            const float w = expf(ml[i].x - Mx);
-                            L += w * ml[i].y;
-                            O.x += w * v[i].x;
-                            O.y += w * v[i].y;
-                            O.z += w * v[i].z;
-                            O.w += w * v[i].w;
-                        }
+                    for (int i = 0; i < 16; ++i) {
+                        const float* e2 = pb + (size_t)min(s0 + i, nl - 1) * (HD + 4);
+                        v[i] = mk_ldg4(e2 + d);
+                        ml[i] = mk_ldg2(e2 + HD);
                     }
-                    if (L > 0.f) {
-                        const float inv = 1.f / L;
-                        r = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+                    float cm = -INFINITY;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        if (s0 + i < nl) cm = fmaxf(cm, ml[i].x);
+                    if (cm == -INFINITY) continue;
+                    if (cm > Mx) {
+                        const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
+                        L *= sc;
+                        O.x *= sc;
+                        O.y *= sc;
+                        O.z *= sc;
+                        O.w *= sc;
+                        Mx = cm;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        if (s0 + i >= nl || ml[i].x == -INFINITY) continue;
+                        const float w = expf(ml[i].x - Mx);
+                        L += w * ml[i].y;
+                        O.x += w * v[i].x;
+                        O.y += w * v[i].y;
+                        O.z += w * v[i].z;
+                        O.w += w * v[i].w;
                     }
                 }
-                float* op = o.aout + (size_t)row * a.H * HD + h * HD + d;
-                mk_stf(op, r.x);
-                mk_stf(op + 1, r.y);
-                mk_stf(op + 2, r.z);
-                mk_stf(op + 3, r.w);
+                if (L > 0.f) {
+                    const float inv = 1.f / L;
+                    r = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+                }
             }
+            float* op = o.aout + (size_t)row * a.H * HD + h * HD + d;
+            mk_stf(op, r.x);
+            mk_stf(op + 1, r.y);
+            mk_stf(op + 2, r.z);
+            mk_stf(op + 3, r.w);
         }
         __syncthreads();
     }
@@ -846,6 +920,26 @@ __device__ __forceinline__ void mk_barrier(const MkArgs& a, int& gen, long& spin
     __builtin_amdgcn_s_barrier();
 }
 
+// Attention phase with the barrier in front of it: the older cache rows of this workgroup's first
+// unit are requested before the release (by waves 1..7 before, by wave 0, which runs the barrier,
+// after it, so that its polls do not return behind them).
+template <int HD>
+__device__ __forceinline__ void mk_attn_phase(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem,
+                                              int* last_flag, int& gen, long& spins, int p) {
+    MkKv<HD> kv;
+    const int nsplit = mk_uni(od.nsplit), layer = mk_uni(od.layer);
+    const int nq = a.rps * (a.H / a.Hkv);
+    const int nspan = mk_attn_spans(a, rp, nsplit);
+    const int nunit = (a.M / a.rps) * a.Hkv * ((nq + kMkQG - 1) / kMkQG) * nspan;
+    const bool first = (int)blockIdx.x < nunit;
+    MkAttnUnit t{};
+    if (first) t = mk_attn_unit(a, rp, nsplit, nspan, blockIdx.x);
+    if (first && threadIdx.x >= 64) mk_attn_kv<HD>(a, rp, layer, t, false, kv);
+    if (p > 0) mk_barrier(a, gen, spins, nullptr, nullptr);
+    if (first && threadIdx.x < 64) mk_attn_kv<HD>(a, rp, layer, t, false, kv);
+    mk_attn_t<HD>(a, od, rp, smem, last_flag, kv);
+}
+
 __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ MkPhase op_lds[2];
@@ -883,10 +977,9 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
             }
             mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag, bf);
         } else if (op == kMkAttn) {
-            if (p > 0) mk_barrier(a, gen, spins, nullptr, nullptr);
-            if (a.hd == 64) mk_attn_t<64>(a, o, rp, smem, &last_flag);
-            else if (a.hd == 128) mk_attn_t<128>(a, o, rp, smem, &last_flag);
-            else mk_attn_t<32>(a, o, rp, smem, &last_flag);
+            if (a.hd == 64) mk_attn_phase<64>(a, o, rp, smem, &last_flag, gen, spins, p);
+            else if (a.hd == 128) mk_attn_phase<128>(a, o, rp, smem, &last_flag, gen, spins, p);
+            else mk_attn_phase<32>(a, o, rp, smem, &last_flag, gen, spins, p);
         }
         mk_vmwait();  // this phase's stores are complete before the workgroup counts in
         if (threadIdx.x < kWords && p + 1 < a.nphase) ((uint32_t*)&op_lds[(p + 1) & 1])[threadIdx.x] = nw;
@@ -931,8 +1024,8 @@ MkPlanG mk_plan_gemv(int M, int N, int K, bool norm, int subs) {
 }
 
 size_t mk_attn_lds(int hd) {
-    return sizeof(float) * ((size_t)kMkMaxNq * hd + (size_t)kMkSpan * (hd + 4) + (size_t)kMkSpan * hd +
-                            (size_t)kMkMaxNq * kMkSpan + 2 * kMkMaxNq);
+    return sizeof(float) * ((size_t)kMkQG * hd + (size_t)kMkSpan * (hd + 4) + (size_t)kMkSpan * hd +
+                            (size_t)kMkQG * kMkSpan + 2 * kMkQG);
 }
 
 struct Arena {
@@ -1114,7 +1207,8 @@ int mk_phase_count(const sd2_config& c) {
 size_t mk_counter_ints(const sd2_config& c) {
     const int v = c.verifier.vocab / 16 + 1;
     const int f = std::max(c.verifier.d_ff, c.drafter.d_ff) / 16 + 1;
-    const int kv = kMkMaxRows * std::max(c.verifier.n_kv_heads, c.drafter.n_kv_heads);
+    // attention: one counter per (sequence, KV head, group of query vectors)
+    const int kv = kMkMaxRows * std::max(c.verifier.n_kv_heads, c.drafter.n_kv_heads) * (kMkMaxNq / kMkQG);
     return (size_t)std::max(std::max(v, f), kv);
 }
 
