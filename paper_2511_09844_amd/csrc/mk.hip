@@ -369,18 +369,29 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
     const int arow = n < M ? n : M - 1;  // rows >= M repeat row M-1; their outputs are discarded
     const uint16_t* ahp = xh + (size_t)arow * ldk + kw0 + 16 * q;
     const uint16_t* alp = xl + (size_t)arow * ldk + kw0 + 16 * q;
+    // Activation fragments are read from LDS two slices at a time, all eight requests ahead of
+    // the slices' eight MFMAs (left to itself the scheduler waits on every single read).
     auto mma = [&]() {
         mk_f4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = acc;
 #pragma unroll
-        for (int st = 0; st < 8; ++st)
+        for (int s0 = 0; s0 < 8; s0 += 2) {
+            mk_bf16x8 ah[4], al[4];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const mk_bf16x8 ah = *(const mk_bf16x8*)(ahp + st * 64 + 8 * h);
-                const mk_bf16x8 al = *(const mk_bf16x8*)(alp + st * 64 + 8 * h);
-                const mk_bf16x8 b = __builtin_bit_cast(mk_bf16x8, bf.w[st][h]);
-                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc, 0, 0, 0);
-                acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc2, 0, 0, 0);
+            for (int i = 0; i < 4; ++i) {
+                const int st = s0 + (i >> 1), h = i & 1;
+                ah[i] = *(const mk_bf16x8*)(ahp + st * 64 + 8 * h);
+                al[i] = *(const mk_bf16x8*)(alp + st * 64 + 8 * h);
             }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int st = s0 + (i >> 1), h = i & 1;
+                const mk_bf16x8 b = __builtin_bit_cast(mk_bf16x8, bf.w[st][h]);
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[i], b, acc, 0, 0, 0);
+                acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[i], b, acc2, 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // the 8 LDS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);  // then the 8 MFMAs
+        }
         return acc + acc2;
     };
     auto put = [&](const mk_f4& v, int slot) {
