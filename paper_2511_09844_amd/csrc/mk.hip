@@ -95,6 +95,33 @@ __device__ __forceinline__ T mk_uni(const T& v) {
     return r;
 }
 
+// Wave-wide max / sum through DPP row operations (no LDS round trips): pairs, quads, half rows
+// and rows by swaps and mirrors, then rows 0-3 folded into row 3 by the row broadcasts; the
+// result of lane 63 is returned to every lane.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float mk_dpp(float old, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old), __builtin_bit_cast(int, v),
+                                                                 CTRL, ROWS, 0xf, false));
+}
+__device__ __forceinline__ float mk_wmax(float v) {
+    v = fmaxf(v, mk_dpp<0xB1, 0xf>(v, v));   // quad_perm [1,0,3,2]
+    v = fmaxf(v, mk_dpp<0x4E, 0xf>(v, v));   // quad_perm [2,3,0,1]
+    v = fmaxf(v, mk_dpp<0x141, 0xf>(v, v));  // row_half_mirror
+    v = fmaxf(v, mk_dpp<0x140, 0xf>(v, v));  // row_mirror
+    v = fmaxf(v, mk_dpp<0x142, 0xa>(v, v));  // row_bcast:15 into rows 1 and 3
+    v = fmaxf(v, mk_dpp<0x143, 0xc>(v, v));  // row_bcast:31 into rows 2 and 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+__device__ __forceinline__ float mk_wsum(float v) {
+    v += mk_dpp<0xB1, 0xf>(0.f, v);
+    v += mk_dpp<0x4E, 0xf>(0.f, v);
+    v += mk_dpp<0x141, 0xf>(0.f, v);
+    v += mk_dpp<0x140, 0xf>(0.f, v);
+    v += mk_dpp<0x142, 0xa>(0.f, v);
+    v += mk_dpp<0x143, 0xc>(0.f, v);
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
 // Row plan of the launch, one entry per activation row (position -1: inactive row).
 struct MkRows {
     int pos[kMkMaxRows], seq[kMkMaxRows], tok[kMkMaxRows];
@@ -330,11 +357,12 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                     }
                 }
             }
+        float sq[8];
 #pragma unroll
         for (int mm = 0; mm < 8; ++mm) {
             const int m = m0 + mm;
-            if (m >= M) break;
-            float sq = 0.f;
+            sq[mm] = 0.f;
+            if (m >= M) continue;
 #pragma unroll
             for (int jc = 0; jc < 2; ++jc) {
                 const int c = tid + 512 * jc;
@@ -350,12 +378,17 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                         make_uint2(__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1));
                     *(uint2*)(xl + (size_t)m * ldk + 4 * c) =
                         make_uint2(__builtin_bit_cast(uint32_t, l0), __builtin_bit_cast(uint32_t, l1));
-                    sq += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+                    sq[mm] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
                 }
             }
-            sq = wave_sum(sq);
-            if (lane == 0 && wave < kNW) ssq[m * kNW + wave] = sq;
         }
+        // the rows' wave sums are independent DPP chains
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm)
+            if (m0 + mm < M) sq[mm] = mk_wsum(sq[mm]);
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm)
+            if (m0 + mm < M && lane == 0 && wave < kNW) ssq[(m0 + mm) * kNW + wave] = sq[mm];
     }
     __syncthreads();
     if (tid < M) {
@@ -404,8 +437,13 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
             const int i = e / (groups * 256), gg = (e / 256) % groups, c = e & 255;
             const int u = (r0 + i) * groups + gg;
             if (u < nsub) {
+                // all eight wave slots are read at once (slots past the unit's waves are dropped)
+                float rv[kNW];
+#pragma unroll
+                for (int ww = 0; ww < kNW; ++ww) rv[ww] = red[(i * kNW + ((gg * wpu + ww) & (kNW - 1))) * 256 + c];
                 float x = 0.f;
-                for (int ww = 0; ww < wpu; ++ww) x += red[(i * kNW + gg * wpu + ww) * 256 + c];
+#pragma unroll
+                for (int ww = 0; ww < kNW; ++ww) x += ww < wpu ? rv[ww] : 0.f;
                 res[u * 256 + c] = x * inv_rms[c >> 4];
             }
         }
@@ -623,33 +661,6 @@ __device__ __forceinline__ void mk_attn_kv(const MkArgs& a, const MkRows& rp, in
             kv.v[i] = mk_ldg4(vg + (size_t)jj * HD + d);
         }
     }
-}
-
-// Wave-wide max / sum through DPP row operations (no LDS round trips): pairs, quads, half rows
-// and rows by swaps and mirrors, then rows 0-3 folded into row 3 by the row broadcasts; the
-// result of lane 63 is returned to every lane.
-template <int CTRL, int ROWS>
-__device__ __forceinline__ float mk_dpp(float old, float v) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old), __builtin_bit_cast(int, v),
-                                                                 CTRL, ROWS, 0xf, false));
-}
-__device__ __forceinline__ float mk_wmax(float v) {
-    v = fmaxf(v, mk_dpp<0xB1, 0xf>(v, v));   // quad_perm [1,0,3,2]
-    v = fmaxf(v, mk_dpp<0x4E, 0xf>(v, v));   // quad_perm [2,3,0,1]
-    v = fmaxf(v, mk_dpp<0x141, 0xf>(v, v));  // row_half_mirror
-    v = fmaxf(v, mk_dpp<0x140, 0xf>(v, v));  // row_mirror
-    v = fmaxf(v, mk_dpp<0x142, 0xa>(v, v));  // row_bcast:15 into rows 1 and 3
-    v = fmaxf(v, mk_dpp<0x143, 0xc>(v, v));  // row_bcast:31 into rows 2 and 3
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
-}
-__device__ __forceinline__ float mk_wsum(float v) {
-    v += mk_dpp<0xB1, 0xf>(0.f, v);
-    v += mk_dpp<0x4E, 0xf>(0.f, v);
-    v += mk_dpp<0x141, 0xf>(0.f, v);
-    v += mk_dpp<0x140, 0xf>(0.f, v);
-    v += mk_dpp<0x142, 0xa>(0.f, v);
-    v += mk_dpp<0x143, 0xc>(0.f, v);
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
 template <int HD>
