@@ -52,10 +52,17 @@ constexpr int kNT = kMkWaves * 64;  // streaming threads
 constexpr int kCtl = 0;             // thread that runs the grid barrier (no loads in flight there)
 constexpr long kMkSpin = 1L << 22;  // grid-barrier polls before a workgroup gives up (reports err)
 
-__device__ __forceinline__ int mk_ld(int32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ int mk_add(int32_t* p, int v) { return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ void mk_sti(int32_t* p, int v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ __forceinline__ void mk_stf(float* p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+// Device-scope accesses through global-address-space pointers: through generic pointers they
+// become flat instructions, and a later LDS access then waits until every earlier flat store has
+// completed (a flat address might have been LDS).
+typedef __attribute__((address_space(1))) int32_t* mk_gip_w;
+typedef __attribute__((address_space(1))) float* mk_gfp_w;
+__device__ __forceinline__ int mk_ld(int32_t* p) { return __hip_atomic_load((mk_gip_w)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ int mk_add(int32_t* p, int v) {
+    return __hip_atomic_fetch_add((mk_gip_w)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void mk_sti(int32_t* p, int v) { __hip_atomic_store((mk_gip_w)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ __forceinline__ void mk_stf(float* p, float v) { __hip_atomic_store((mk_gfp_w)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 __device__ __forceinline__ float mk_ldg(const float* p) { return *(mk_gfp)p; }
 __device__ __forceinline__ float4 mk_ldg4(const float* p) {
     mk_f4 v = *(mk_gf4p)p;
@@ -176,7 +183,12 @@ struct MkW {
     int K, mode, nseg, st0, st1;
 };
 __device__ __forceinline__ const uint16_t* mk_row(const MkW& o, int hd, int tile, int sub, int n) {
-    if (o.mode == kEpiSwiglu) return (sub ? o.w1 : o.w0) + (size_t)(tile * 16 + n) * o.K;
+    // gate|up: with two sub-tiles, sub 0 streams 16 gate rows and sub 1 the 16 up rows of the same
+    // features; with one, lane rows 0-7 are gate rows and 8-15 the up rows of the same 8 features
+    if (o.mode == kEpiSwiglu) {
+        if (o.nseg == 2) return (sub ? o.w1 : o.w0) + (size_t)(tile * 16 + n) * o.K;
+        return (n < 8 ? o.w0 : o.w1) + (size_t)(tile * 8 + (n & 7)) * o.K;
+    }
     int seg = 0, lt = tile;
     if (o.nseg > 1 && lt >= o.st0) { lt -= o.st0; seg = 1; }
     if (o.nseg > 2 && seg == 1 && lt >= o.st1) { lt -= o.st1; seg = 2; }
@@ -497,7 +509,13 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                 if (valid && ec == 0) mk_stf(oss_out + (size_t)em * (oldy / 16) + tile, sq);
             }
         } else if (omode == kEpiSwiglu) {
-            if (valid) mk_stf(oY + (size_t)em * oldy + tile * 16 + ec, silu(v0) * v1);
+            if (osubs == 2) {
+                if (valid) mk_stf(oY + (size_t)em * oldy + tile * 16 + ec, silu(v0) * v1);
+            } else {
+                // column c < 8 holds gate feature 8 tile + c, column c + 8 its up row
+                const float up = __shfl_xor(v0, 8, 16);
+                if (valid && ec < 8) mk_stf(oY + (size_t)em * oldy + tile * 8 + ec, silu(v0) * up);
+            }
         } else {  // Q|K|V: rotate-half RoPE on Q and K, cache append of K and V
             const float partner = __shfl_xor(v0, 8, 16);
             if (!valid) return;
@@ -527,7 +545,11 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
             } else if (pos >= 0) {
                 const size_t idx =
                     ((((size_t)olayer * a.max_batch + rp.seq[em]) * a.Hkv + h) * a.cap + pos) * a.hd + dim;
-                mk_stf(seg == 1 ? a.kc + idx : a.vc + idx, out);
+                // both cache pointers in registers first: selecting between the adjacent
+                // arguments directly indexes a stack copy of them
+                float* const kcp = mk_uni(a.kc);
+                float* const vcp = mk_uni(a.vc);
+                mk_stf((seg == 1 ? kcp : vcp) + idx, out);
             }
         }
     };
@@ -1137,8 +1159,16 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         o.Y = xa;
         o.ldy = dm;
         MkPhase gu{};
-        if (!gemv(kEpiSwiglu, F, dm, Wl[kFfnNorm], true, 2, gu)) return false;
-        gu.nseg = 1;
+        // Tiles of 16 features with a gate and an up sub-tile when F / 16 tiles spread evenly over
+        // the workgroups; else tiles of 8 gate + 8 up rows (2F / 16 of them: twice as many, so the
+        // last round is not left to half of the workgroups)
+        const bool pair_tiles = G > 0 && (F / 16) % G == 0;
+        if (pair_tiles) {
+            if (!gemv(kEpiSwiglu, F, dm, Wl[kFfnNorm], true, 2, gu)) return false;
+        } else if (F % 8 || !gemv(kEpiSwiglu, 2 * F, dm, Wl[kFfnNorm], true, 1, gu)) {
+            return false;
+        }
+        gu.nseg = pair_tiles ? 2 : 1;
         gu.W[0] = (const uint16_t*)Wl[kWg];
         gu.W[1] = (const uint16_t*)Wl[kWu];
         gu.X = xa;
