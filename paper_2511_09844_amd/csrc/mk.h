@@ -17,7 +17,7 @@ constexpr int kMkMaxNq = 32;                     // query vectors per (sequence,
 constexpr int kMkMaxKR = 4096;                   // K-range staged per workgroup
 constexpr int kMkLdsBudget = 150 * 1024;         // dynamic LDS per workgroup
 constexpr int kMkLine = 32;                      // ints per 128-byte line
-constexpr int kMkBarInts = 18 * kMkLine;         // barrier state: 2 + 8 + 8 lines
+constexpr int kMkBarInts = 16 * kMkLine;         // barrier state: per XCD group a counter line (0..7) and a release line (8..15)
 
 enum MkOp : int32_t { kMkGemv = 1, kMkAttn = 2 };
 enum MkX : int32_t { kMkXBuf = 0, kMkXEmbed = 1 };
@@ -60,6 +60,7 @@ struct MkArgs {
     const uint16_t* dummy;   // 1 KB of zeros (loads of absent units)
     const uint16_t* ones;    // kMkMaxKR bf16 ones (gain of projections without a norm)
     int32_t* bar;            // kMkBarInts
+    uint32_t bar_gen;        // grid barriers completed on this state before this launch
     int32_t* err;            // set to 1 if a grid barrier timed out
     int64_t* trace;          // profiling: end time of every phase (device clock, 100 MHz), or null
     int32_t G;
@@ -74,6 +75,7 @@ struct MkState {
     int prog_cap;         // capacity in phases
     char* arena;          // per-launch activation buffers
     int32_t* bar;         // grid-barrier state
+    uint32_t bar_gen;     // grid barriers completed so far (every launch of nphase phases adds nphase - 1)
     int32_t* err;         // barrier time-out flag
     int32_t* cnt;         // hand-off counters
     uint16_t* dummy;      // 1 KB of zeros

@@ -915,31 +915,27 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
     }
 }
 
-// Grid barrier at the start of a phase.  Counters: one per XCD group (workgroup id mod 8), one
-// global, one release line per group; all of them only grow (generation g of the barrier: a group
-// counter reaches g * workgroups-in-group, the global one g * groups), so no counter is ever reset
-// and nothing waits for a store to complete on the barrier's path.  The last arriver of a group
-// counts the group in; the last group publishes generation g on the 8 release lines that the
-// groups' control threads poll.
+// Grid barrier at the start of a phase.  One arrival counter per XCD group (workgroup id mod 8)
+// and one release line per group; both only grow (after barrier g of this state, group x's counter
+// holds g * (workgroups in group x) and its release line g), and the host passes the number of
+// barriers before the launch, so no workgroup reads a starting value that a faster one may already
+// have advanced.  A workgroup's control thread adds 1 to its group's counter; the group's last
+// arriver writes g to the group's release line; lanes 0..7 of wave 0 poll the eight release lines
+// until all hold g.  The polled lines never take atomics (polling the counters themselves, or one
+// word per workgroup, measured slower: the polls then contend with the arrivals).
 //
-// With a weight buffer (projection phases) the phase's first weight unit is requested after this
-// workgroup's arrival has been counted, so that it streams during the barrier: waves 1..7 skip
-// the arrival code and issue at once; wave 0 issues once its control lane has the atomics'
-// results, which would otherwise wait for those loads.  The buffer is local to the projection
-// phase, so it holds no registers in other phases.
+// With a weight buffer (projection phases) the phase's first weight unit is requested right after
+// the arrival, so that it streams during the barrier.
 __device__ __forceinline__ void mk_barrier(const MkArgs& a, int& gen, long& spins, const MkPhase* ph, MkBuf* bf) {
-    int32_t* base = a.bar;
-    const int x = blockIdx.x & 7;
+    int32_t* cnt = a.bar;
+    int32_t* rel = a.bar + 8 * kMkLine;
     const unsigned g1 = (unsigned)gen + 1u;
+    gen = (int)g1;
     if (threadIdx.x == kCtl) {
-        const unsigned ngroup = a.G < 8 ? a.G : 8;
-        const unsigned per = a.G / 8 + (x < a.G % 8 ? 1 : 0);
-        const unsigned prev = (unsigned)mk_add(base + (2 + x) * kMkLine, 1);
-        if (prev + 1u == g1 * per) {
-            const unsigned gp = (unsigned)mk_add(base + kMkLine, 1);
-            if (gp + 1u == g1 * ngroup)
-                for (int i = 0; i < 8; ++i) mk_sti(base + (10 + i) * kMkLine, (int)g1);
-        }
+        const int x = blockIdx.x & 7;
+        const unsigned per = (unsigned)(a.G / 8 + (x < a.G % 8 ? 1 : 0));
+        const unsigned prev = (unsigned)mk_add(cnt + x * kMkLine, 1);
+        if (prev + 1u == g1 * per) mk_sti(rel + x * kMkLine, (int)g1);
     }
     if (bf) {
         const int tid = mk_tid(), lane = tid & 63, wave = tid >> 6;
@@ -948,17 +944,17 @@ __device__ __forceinline__ void mk_barrier(const MkArgs& a, int& gen, long& spin
         const uint16_t* wp = mk_uptr(a, q, 0, lane & 15, lane >> 4, lane, st);
         mk_issue<0, kMkPreSteps>(*bf, wp, st);
     }
-    if (threadIdx.x == kCtl) {
-        gen = (int)g1;
-        if (spins >= 0) {
-            while ((int)((unsigned)mk_ld(base + (10 + x) * kMkLine) - g1) < 0) {
-                if (++spins > kMkSpin) {
-                    mk_sti(a.err, 1);
-                    spins = -1;  // give up waiting for the rest of the launch (results invalid)
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
+    if (threadIdx.x < 64 && spins >= 0) {
+        const int l = threadIdx.x;
+        for (;;) {
+            const bool ok = l >= 8 || (int)((unsigned)mk_ld(rel + l * kMkLine) - g1) >= 0;
+            if (__builtin_amdgcn_read_exec() == __ballot(ok)) break;
+            if (++spins > kMkSpin) {
+                if (l == 0) mk_sti(a.err, 1);
+                spins = -1;  // give up waiting for the rest of the launch (results invalid)
+                break;
             }
+            __builtin_amdgcn_s_sleep(1);
         }
     }
     __builtin_amdgcn_s_barrier();
@@ -991,14 +987,12 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
     __shared__ float inv_rms[kMkMaxRows];
     __shared__ int flags[64];
     __shared__ int last_flag;
-    __shared__ int gen0;
     constexpr int kWords = (int)(sizeof(MkPhase) / 4);
     static_assert(sizeof(MkPhase) % 4 == 0 && kWords <= 64, "phase descriptor larger than one wave");
     mk_plan(a, rp);
     if (threadIdx.x < kWords) ((uint32_t*)&op_lds[0])[threadIdx.x] = mk_ldu((const uint32_t*)&a.prog[0] + threadIdx.x);
-    if (threadIdx.x == kCtl) gen0 = mk_ld(a.bar + 10 * kMkLine + (blockIdx.x & 7) * kMkLine);
     __syncthreads();
-    int gen = gen0;
+    int gen = (int)a.bar_gen;
     long spins = 0;
     if (a.trace && blockIdx.x == 0 && threadIdx.x == kCtl) a.trace[0] = wall_clock64();
     for (int p = 0; p < a.nphase; ++p) {
@@ -1270,6 +1264,7 @@ __global__ void k_mk_init(uint16_t* ones, int n) {
 }
 
 void mk_init_buffers(Engine& e) {
+    e.mk.bar_gen = 0;  // the barrier counters are zero in a fresh workspace
     if (!e.mk.ones) return;
     k_mk_init<<<(kMkMaxKR + 255) / 256, 256, 0, e.stream>>>(e.mk.ones, kMkMaxKR);
 }
@@ -1359,6 +1354,7 @@ hipError_t mk_launch(Engine& e, int j) {
     a.dummy = s.dummy;
     a.ones = s.ones;
     a.bar = s.bar;
+    a.bar_gen = s.bar_gen;
     a.err = s.err;
     a.trace = (e.prof_on && s.trace) ? s.trace + (size_t)j * kMkTracePhases : nullptr;
     a.G = s.G;
@@ -1370,6 +1366,7 @@ hipError_t mk_launch(Engine& e, int j) {
         (void)hipEventRecord(pe->b, e.stream);
         prof_commit(&e);
     }
+    if (err == hipSuccess) s.bar_gen += (uint32_t)(s.n[j] - 1);  // one barrier per phase after the first
     return err;
 }
 
