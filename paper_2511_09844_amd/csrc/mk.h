@@ -20,7 +20,7 @@ constexpr int kMkLine = 32;                      // ints per 128-byte line
 constexpr int kMkBarInts = 16 * kMkLine;         // barrier state: per XCD group a counter line (0..7) and a release line (8..15)
 
 enum MkOp : int32_t { kMkGemv = 1, kMkAttn = 2 };
-enum MkX : int32_t { kMkXBuf = 0, kMkXEmbed = 1 };
+enum MkX : int32_t { kMkXBuf = 0, kMkXEmbed = 1, kMkXAttn = 2 };
 
 // One phase.  GEMV: Y (op)= W . xn over `tiles` 16-row tiles, K cut into S ranges of KR columns;
 // each unit is a tile times a 512-column slice per wave, wpu waves per tile.  ATTN: causal GQA
@@ -29,8 +29,9 @@ struct MkPhase {
     int32_t op, mode, K, tiles, S, KR, wpu, subs, nseg, xsrc, res_embed, ldy;
     int32_t seg_tiles[3];
     int32_t layer, nsplit;
+    int32_t defer;           // ATTN: leave the span partials unmerged (the next projection merges them)
     const uint16_t* W[3];
-    const float* X;          // activation rows [M][K] (xsrc == kMkXBuf)
+    const float* X;          // activation rows [M][K] (kMkXBuf), or attention partials (kMkXAttn)
     const uint16_t* gamma;   // RMSNorm gain, or null (no norm)
     const float* xres;       // Add: residual rows [M][ldy] (unless res_embed)
     float* Y;                // output

@@ -351,56 +351,122 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
             gw[jc] = make_uint2(w.x, w.y);
         }
     }
-    for (int m0 = 0; m0 < M; m0 += 8) {
-        float4 xv[8][2];
+    if (oxsrc == kMkXAttn) {
+        // The rows are attention outputs still split into span partials (output, span max, span
+        // sum per row, head and span): each thread merges its 4 columns over the spans its row
+        // sees, all spans' partials requested at once (up to 16 per round trip), then stages them.
+        const int HD = a.hd, ns = mk_uni(od.nsplit);
+        for (int m = 0; m < M; ++m) {
+            const int pos = rp.pos[m];
+            const int nl = pos >= 0 ? min(ns, pos / kMkSpan + 1) : 0;
+            float sqm = 0.f;
+            for (int c = tid; c < n4 && tid < kNT; c += kNT) {
+                const int kk = k0 + 4 * c, h = kk / HD, d = kk % HD;
+                float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+                const float* pb = oX + ((size_t)m * a.H + h) * ns * (HD + 4);
+                float Mx = -INFINITY, L = 0.f;
+                float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int s0 = 0; s0 < nl; s0 += 16) {
+                    float4 v[16];
+                    float2 ml[16];
 #pragma unroll
-        for (int mm = 0; mm < 8; ++mm)
+                    for (int i = 0; i < 16; ++i) {
+                        const float* e2 = pb + (size_t)min(s0 + i, nl - 1) * (HD + 4);
+                        v[i] = mk_ldg4(e2 + d);
+                        ml[i] = mk_ldg2(e2 + HD);
+                    }
+                    float cm = -INFINITY;
 #pragma unroll
-            for (int jc = 0; jc < 2; ++jc) {
-                const int m = m0 + mm, c = tid + 512 * jc;
-                xv[mm][jc] = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (m < M && tid < kNT && c < n4) {
-                    if (oxsrc == kMkXEmbed) {
-                        const int cc = k0 + 4 * c;
-                        xv[mm][jc] = make_float4(mk_embed_at(a, rp, m, cc), mk_embed_at(a, rp, m, cc + 1),
-                                                 mk_embed_at(a, rp, m, cc + 2), mk_embed_at(a, rp, m, cc + 3));
-                    } else {
-                        xv[mm][jc] = mk_ldg4(oX + (size_t)m * oK + k0 + 4 * c);
+                    for (int i = 0; i < 16; ++i)
+                        if (s0 + i < nl) cm = fmaxf(cm, ml[i].x);
+                    if (cm == -INFINITY) continue;
+                    if (cm > Mx) {
+                        const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
+                        L *= sc;
+                        O.x *= sc;
+                        O.y *= sc;
+                        O.z *= sc;
+                        O.w *= sc;
+                        Mx = cm;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        if (s0 + i >= nl || ml[i].x == -INFINITY) continue;
+                        const float w = expf(ml[i].x - Mx);
+                        L += w * ml[i].y;
+                        O.x += w * v[i].x;
+                        O.y += w * v[i].y;
+                        O.z += w * v[i].z;
+                        O.w += w * v[i].w;
+                    }
+                }
+                if (L > 0.f) {
+                    const float inv = 1.f / L;
+                    x = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+                }
+                const mk_f2 a0 = {x.x, x.y}, a1 = {x.z, x.w};
+                const mk_bf16x2 h0 = __builtin_convertvector(a0, mk_bf16x2), h1 = __builtin_convertvector(a1, mk_bf16x2);
+                const mk_bf16x2 l0 = __builtin_convertvector(a0 - __builtin_convertvector(h0, mk_f2), mk_bf16x2);
+                const mk_bf16x2 l1 = __builtin_convertvector(a1 - __builtin_convertvector(h1, mk_f2), mk_bf16x2);
+                *(uint2*)(xh + (size_t)m * ldk + 4 * c) = make_uint2(__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1));
+                *(uint2*)(xl + (size_t)m * ldk + 4 * c) = make_uint2(__builtin_bit_cast(uint32_t, l0), __builtin_bit_cast(uint32_t, l1));
+                sqm += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+            }
+            sqm = mk_wsum(sqm);
+            if (lane == 0 && wave < kNW) ssq[m * kNW + wave] = sqm;
+        }
+    } else {
+        for (int m0 = 0; m0 < M; m0 += 8) {
+            float4 xv[8][2];
+    #pragma unroll
+            for (int mm = 0; mm < 8; ++mm)
+    #pragma unroll
+                for (int jc = 0; jc < 2; ++jc) {
+                    const int m = m0 + mm, c = tid + 512 * jc;
+                    xv[mm][jc] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    if (m < M && tid < kNT && c < n4) {
+                        if (oxsrc == kMkXEmbed) {
+                            const int cc = k0 + 4 * c;
+                            xv[mm][jc] = make_float4(mk_embed_at(a, rp, m, cc), mk_embed_at(a, rp, m, cc + 1),
+                                                     mk_embed_at(a, rp, m, cc + 2), mk_embed_at(a, rp, m, cc + 3));
+                        } else {
+                            xv[mm][jc] = mk_ldg4(oX + (size_t)m * oK + k0 + 4 * c);
+                        }
+                    }
+                }
+            float sq[8];
+    #pragma unroll
+            for (int mm = 0; mm < 8; ++mm) {
+                const int m = m0 + mm;
+                sq[mm] = 0.f;
+                if (m >= M) continue;
+    #pragma unroll
+                for (int jc = 0; jc < 2; ++jc) {
+                    const int c = tid + 512 * jc;
+                    if (tid < kNT && c < n4) {
+                        const float4 v = xv[mm][jc];
+                        const uint2 gg = gw[jc];
+                        const mk_f2 a0 = {v.x * __uint_as_float(gg.x << 16), v.y * __uint_as_float(gg.x & 0xffff0000u)};
+                        const mk_f2 a1 = {v.z * __uint_as_float(gg.y << 16), v.w * __uint_as_float(gg.y & 0xffff0000u)};
+                        const mk_bf16x2 h0 = __builtin_convertvector(a0, mk_bf16x2), h1 = __builtin_convertvector(a1, mk_bf16x2);
+                        const mk_bf16x2 l0 = __builtin_convertvector(a0 - __builtin_convertvector(h0, mk_f2), mk_bf16x2);
+                        const mk_bf16x2 l1 = __builtin_convertvector(a1 - __builtin_convertvector(h1, mk_f2), mk_bf16x2);
+                        *(uint2*)(xh + (size_t)m * ldk + 4 * c) =
+                            make_uint2(__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1));
+                        *(uint2*)(xl + (size_t)m * ldk + 4 * c) =
+                            make_uint2(__builtin_bit_cast(uint32_t, l0), __builtin_bit_cast(uint32_t, l1));
+                        sq[mm] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
                     }
                 }
             }
-        float sq[8];
-#pragma unroll
-        for (int mm = 0; mm < 8; ++mm) {
-            const int m = m0 + mm;
-            sq[mm] = 0.f;
-            if (m >= M) continue;
-#pragma unroll
-            for (int jc = 0; jc < 2; ++jc) {
-                const int c = tid + 512 * jc;
-                if (tid < kNT && c < n4) {
-                    const float4 v = xv[mm][jc];
-                    const uint2 gg = gw[jc];
-                    const mk_f2 a0 = {v.x * __uint_as_float(gg.x << 16), v.y * __uint_as_float(gg.x & 0xffff0000u)};
-                    const mk_f2 a1 = {v.z * __uint_as_float(gg.y << 16), v.w * __uint_as_float(gg.y & 0xffff0000u)};
-                    const mk_bf16x2 h0 = __builtin_convertvector(a0, mk_bf16x2), h1 = __builtin_convertvector(a1, mk_bf16x2);
-                    const mk_bf16x2 l0 = __builtin_convertvector(a0 - __builtin_convertvector(h0, mk_f2), mk_bf16x2);
-                    const mk_bf16x2 l1 = __builtin_convertvector(a1 - __builtin_convertvector(h1, mk_f2), mk_bf16x2);
-                    *(uint2*)(xh + (size_t)m * ldk + 4 * c) =
-                        make_uint2(__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1));
-                    *(uint2*)(xl + (size_t)m * ldk + 4 * c) =
-                        make_uint2(__builtin_bit_cast(uint32_t, l0), __builtin_bit_cast(uint32_t, l1));
-                    sq[mm] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-                }
-            }
+            // the rows' wave sums are independent DPP chains
+    #pragma unroll
+            for (int mm = 0; mm < 8; ++mm)
+                if (m0 + mm < M) sq[mm] = mk_wsum(sq[mm]);
+    #pragma unroll
+            for (int mm = 0; mm < 8; ++mm)
+                if (m0 + mm < M && lane == 0 && wave < kNW) ssq[(m0 + mm) * kNW + wave] = sq[mm];
         }
-        // the rows' wave sums are independent DPP chains
-#pragma unroll
-        for (int mm = 0; mm < 8; ++mm)
-            if (m0 + mm < M) sq[mm] = mk_wsum(sq[mm]);
-#pragma unroll
-        for (int mm = 0; mm < 8; ++mm)
-            if (m0 + mm < M && lane == 0 && wave < kNW) ssq[(m0 + mm) * kNW + wave] = sq[mm];
     }
     __syncthreads();
     if (tid < M) {
@@ -689,13 +755,14 @@ template <int HD>
 __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, int* last_flag,
                                           MkKv<HD>& kv) {
     struct {
-        int nsplit, layer;
+        int nsplit, layer, defer;
         const float* qout;
         float *aout, *apart;
         int32_t* cnt;
     } o;
     o.nsplit = mk_uni(od.nsplit);
     o.layer = mk_uni(od.layer);
+    o.defer = mk_uni(od.defer);
     o.qout = mk_uni(od.qout);
     o.aout = mk_uni(od.aout);
     o.apart = mk_uni(od.apart);
@@ -827,7 +894,7 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
                     if (qi >= nqu) break;
                     const int qv = q0 + qi;
                     const int row = sq * a.rps + qv / Gq, h = kvh * Gq + qv % Gq;
-                    if (nl == 1) {
+                    if (nl == 1 && !o.defer) {
                         // the only live span: normalise and write the output itself
                         const float l = lq[qi];
                         mk_stf(o.aout + (size_t)row * a.H * HD + h * HD + d, l > 0.f ? acc[i] / l : 0.f);
@@ -842,7 +909,7 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
                 }
             }
         }
-        if (nl == 1) {
+        if (nl == 1 || o.defer) {
             __syncthreads();  // LDS of this unit is reused by the next
             continue;
         }
@@ -1143,11 +1210,18 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         at.aout = att;
         at.apart = apart;
         at.cnt = cnt;
+        // Few rows (drafter steps): the O projection merges the span partials while it stages its
+        // input, so no attention workgroup waits to merge; each O workgroup then reads all rows'
+        // partials (at most 256 KB, mostly from L2).
+        at.defer = (size_t)M * H * nsplit * (hd + 4) * sizeof(float) <= 256 * 1024 ? 1 : 0;
         MkPhase o{};
         if (!gemv(kEpiAdd, dm, H * hd, nullptr, false, 1, o)) return false;
+        if (at.defer && o.S != 1) at.defer = 0;
         o.nseg = 1;
         o.W[0] = (const uint16_t*)Wl[kWo];
-        o.X = att;
+        o.X = at.defer ? apart : att;
+        o.xsrc = at.defer ? kMkXAttn : kMkXBuf;
+        o.nsplit = nsplit;
         o.xres = x_prev;
         o.res_embed = x_prev ? 0 : 1;
         o.Y = xa;
