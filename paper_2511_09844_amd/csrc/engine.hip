@@ -197,6 +197,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
             st.arena = cv.take<char>(mk_arena_bytes(c, st.max_batch));
             st.bar = cv.take<int32_t>(kMkBarInts);
             st.err = cv.take<int32_t>(64);
+            st.qc = cv.take<int32_t>((size_t)2 * kMkQcLines * kMkLine);
             st.cnt = cv.take<int32_t>(mk_counter_ints(c));
             st.dummy = cv.take<uint16_t>(512);
             st.ones = cv.take<uint16_t>(kMkMaxKR);

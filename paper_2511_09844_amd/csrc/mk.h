@@ -30,6 +30,8 @@ struct MkPhase {
     int32_t seg_tiles[3];
     int32_t layer, nsplit;
     int32_t defer;           // ATTN: leave the span partials unmerged (the next projection merges them)
+    int32_t kvsig;           // Q|K|V: count every finished tile in on its KV head's counter
+    int32_t kvwait;          // ATTN: wait for the unit's KV head counter instead of a grid barrier
     const uint16_t* W[3];
     const float* X;          // activation rows [M][K] (kMkXBuf), or attention partials (kMkXAttn)
     const uint16_t* gamma;   // RMSNorm gain, or null (no norm)
@@ -62,11 +64,15 @@ struct MkArgs {
     const uint16_t* ones;    // kMkMaxKR bf16 ones (gain of projections without a norm)
     int32_t* bar;            // kMkBarInts
     uint32_t bar_gen;        // grid barriers completed on this state before this launch
+    int32_t* qc;             // this model's KV-head counters (one line each): Q|K|V tiles finished
+    uint32_t qc_base;        // their value before this launch
+    int32_t qc_tpk;          // Q|K|V tiles per KV head (each counter grows by this per layer)
     int32_t* err;            // set to 1 if a grid barrier timed out
     int64_t* trace;          // profiling: end time of every phase (device clock, 100 MHz), or null
     int32_t G;
 };
 
+constexpr int kMkQcLines = 64;   // KV heads per model the counters cover
 constexpr int kMkMaxLaunch = 33;  // drafter steps 1..k (k <= 32) and the verifier block (index 0)
 constexpr int kMkTracePhases = 1024;  // phase end times kept per launch when profiling
 
@@ -76,7 +82,10 @@ struct MkState {
     int prog_cap;         // capacity in phases
     char* arena;          // per-launch activation buffers
     int32_t* bar;         // grid-barrier state
-    uint32_t bar_gen;     // grid barriers completed so far (every launch of nphase phases adds nphase - 1)
+    uint32_t bar_gen;     // grid barriers completed so far (a launch adds one per phase after the first,
+                          // except attention phases that wait on KV-head counters)
+    int32_t* qc;          // [2 models][kMkQcLines] KV-head counters (verifier, drafter)
+    uint32_t qc_total[2]; // their current value per model
     int32_t* err;         // barrier time-out flag
     int32_t* cnt;         // hand-off counters
     uint16_t* dummy;      // 1 KB of zeros

@@ -751,9 +751,25 @@ __device__ __forceinline__ void mk_attn_kv(const MkArgs& a, const MkRows& rp, in
     }
 }
 
+// Wait until KV head kvh's counter reaches `want` (every Q|K|V tile of that head in this layer has
+// been written and counted in); bounded like the grid barrier.
+__device__ __forceinline__ void mk_kv_wait(const MkArgs& a, int kvh, unsigned want, long& spins) {
+    if (threadIdx.x == kCtl && spins >= 0) {
+        while ((int)((unsigned)mk_ld(a.qc + kvh * kMkLine) - want) < 0) {
+            if (++spins > kMkSpin) {
+                mk_sti(a.err, 1);
+                spins = -1;  // give up waiting for the rest of the launch (results invalid)
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    __syncthreads();
+}
+
 template <int HD>
 __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, int* last_flag,
-                                          MkKv<HD>& kv) {
+                                          MkKv<HD>& kv, unsigned kv_want, long& spins) {
     struct {
         int nsplit, layer, defer;
         const float* qout;
@@ -794,7 +810,10 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
         if (nvalid == 0) continue;  // dead span: no work and no hand-off
         {
             // rows of this launch (and, past the first unit, all rows) and the queries
-            if (u != (int)blockIdx.x) mk_attn_kv<HD>(a, rp, o.layer, t, false, kv);
+            if (u != (int)blockIdx.x) {
+                if (kv_want) mk_kv_wait(a, kvh, kv_want, spins);
+                mk_attn_kv<HD>(a, rp, o.layer, t, false, kv);
+            }
             mk_attn_kv<HD>(a, rp, o.layer, t, true, kv);
             constexpr int Q4 = (kMkQG * D4 + kMkThreads - 1) / kMkThreads;  // float4 of queries per thread
             float4 qv4[Q4];
@@ -1041,10 +1060,16 @@ __device__ __forceinline__ void mk_attn_phase(const MkArgs& a, const MkPhase& od
     const bool first = (int)blockIdx.x < nunit;
     MkAttnUnit t{};
     if (first) t = mk_attn_unit(a, rp, nsplit, nspan, blockIdx.x);
+    const int kvwait = mk_uni(od.kvwait);
+    const unsigned want = a.qc_base + (unsigned)(layer + 1) * (unsigned)a.qc_tpk;
     if (first && threadIdx.x >= 64) mk_attn_kv<HD>(a, rp, layer, t, false, kv);
-    if (p > 0) mk_barrier(a, gen, spins, nullptr, nullptr);
+    if (!kvwait) {
+        if (p > 0) mk_barrier(a, gen, spins, nullptr, nullptr);
+    } else if (first && t.nvalid > 0) {
+        mk_kv_wait(a, t.kvh, want, spins);  // only this unit's KV head: no grid barrier
+    }
     if (first && threadIdx.x < 64) mk_attn_kv<HD>(a, rp, layer, t, false, kv);
-    mk_attn_t<HD>(a, od, rp, smem, last_flag, kv);
+    mk_attn_t<HD>(a, od, rp, smem, last_flag, kv, kvwait ? want : 0u, spins);
 }
 
 __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
@@ -1089,6 +1114,14 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
         mk_vmwait();  // this phase's stores are complete before the workgroup counts in
         if (threadIdx.x < kWords && p + 1 < a.nphase) ((uint32_t*)&op_lds[(p + 1) & 1])[threadIdx.x] = nw;
         __syncthreads();  // next descriptor in LDS; this phase's LDS use is over
+        if (threadIdx.x == kCtl && op == kMkGemv && o.kvsig) {
+            // Q|K|V tiles of this workgroup are written and complete: count each in on its KV head
+            const int st0 = o.seg_tiles[0], st1 = o.seg_tiles[1], ph = a.hd / 16, Gq = a.H / a.Hkv;
+            for (int t = blockIdx.x; t < o.tiles; t += a.G) {
+                const int kvh = t < st0 ? t / ph / Gq : (t < st0 + st1 ? (t - st0) / ph : (t - st0 - st1) / ph);
+                mk_add(a.qc + kvh * kMkLine, 1);
+            }
+        }
         if (a.trace && blockIdx.x == 0 && threadIdx.x == kCtl && p + 1 < kMkTracePhases) a.trace[p + 1] = wall_clock64();
     }
 }
@@ -1155,7 +1188,7 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
     const sd2_dims& d = m.dm;
     const int hd = d.d_model / d.n_heads;
     const int L = d.n_layers, H = d.n_heads, Hkv = d.n_kv_heads, F = d.d_ff, dm = d.d_model;
-    if (M > kMkMaxRows || M < 1) return false;
+    if (M > kMkMaxRows || M < 1 || Hkv > kMkQcLines) return false;
     if (rps * (H / Hkv) > kMkMaxNq) return false;
     if (hd != 32 && hd != 64 && hd != 128) return false;
     const int nsplit = mk_nsplit(c.max_seq_len);
@@ -1199,6 +1232,7 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         qkv.seg_tiles[1] = Hkv * hd / 16;
         qkv.seg_tiles[2] = Hkv * hd / 16;
         qkv.xsrc = x_prev ? kMkXBuf : kMkXEmbed;
+        qkv.kvsig = 1;
         qkv.X = x_prev;
         qkv.qout = q;
         qkv.layer = l;
@@ -1210,6 +1244,7 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         at.aout = att;
         at.apart = apart;
         at.cnt = cnt;
+        at.kvwait = 1;  // waits for its KV head's Q|K|V tiles only (the Q|K|V phase counts them in)
         // Few rows (drafter steps): the O projection merges the span partials while it stages its
         // input, so no attention workgroup waits to merge; each O workgroup then reads all rows'
         // partials (at most 256 KB, mostly from L2).
@@ -1338,7 +1373,8 @@ __global__ void k_mk_init(uint16_t* ones, int n) {
 }
 
 void mk_init_buffers(Engine& e) {
-    e.mk.bar_gen = 0;  // the barrier counters are zero in a fresh workspace
+    e.mk.bar_gen = 0;  // the barrier and KV-head counters are zero in a fresh workspace
+    e.mk.qc_total[0] = e.mk.qc_total[1] = 0;
     if (!e.mk.ones) return;
     k_mk_init<<<(kMkMaxKR + 255) / 256, 256, 0, e.stream>>>(e.mk.ones, kMkMaxKR);
 }
@@ -1429,6 +1465,9 @@ hipError_t mk_launch(Engine& e, int j) {
     a.ones = s.ones;
     a.bar = s.bar;
     a.bar_gen = s.bar_gen;
+    a.qc = s.qc + (size_t)(ver ? 0 : 1) * kMkQcLines * kMkLine;
+    a.qc_base = s.qc_total[ver ? 0 : 1];
+    a.qc_tpk = (m.dm.n_heads / m.dm.n_kv_heads + 2) * (m.hd / 16);
     a.err = s.err;
     a.trace = (e.prof_on && s.trace) ? s.trace + (size_t)j * kMkTracePhases : nullptr;
     a.G = s.G;
@@ -1440,7 +1479,11 @@ hipError_t mk_launch(Engine& e, int j) {
         (void)hipEventRecord(pe->b, e.stream);
         prof_commit(&e);
     }
-    if (err == hipSuccess) s.bar_gen += (uint32_t)(s.n[j] - 1);  // one barrier per phase after the first
+    if (err == hipSuccess) {
+        // one grid barrier per phase after the first, except the attention phases (one per layer)
+        s.bar_gen += (uint32_t)(s.n[j] - 1 - m.dm.n_layers);
+        s.qc_total[ver ? 0 : 1] += (uint32_t)(m.dm.n_layers * a.qc_tpk);
+    }
     return err;
 }
 
