@@ -1108,8 +1108,7 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
             mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag, bf);
         } else if (op == kMkAttn) {
             if (a.hd == 64) mk_attn_phase<64>(a, o, rp, smem, &last_flag, gen, spins, p);
-            else if (a.hd == 128) mk_attn_phase<128>(a, o, rp, smem, &last_flag, gen, spins, p);
-            else mk_attn_phase<32>(a, o, rp, smem, &last_flag, gen, spins, p);
+            else mk_attn_phase<128>(a, o, rp, smem, &last_flag, gen, spins, p);
         }
         mk_vmwait();  // this phase's stores are complete before the workgroup counts in
         if (threadIdx.x < kWords && p + 1 < a.nphase) ((uint32_t*)&op_lds[(p + 1) & 1])[threadIdx.x] = nw;
@@ -1190,7 +1189,9 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
     const int L = d.n_layers, H = d.n_heads, Hkv = d.n_kv_heads, F = d.d_ff, dm = d.d_model;
     if (M > kMkMaxRows || M < 1 || Hkv > kMkQcLines) return false;
     if (rps * (H / Hkv) > kMkMaxNq) return false;
-    if (hd != 32 && hd != 64 && hd != 128) return false;
+    // head dims 64 and 128 only: each instantiation adds ~15 KB to a kernel that already exceeds
+    // the instruction cache (other head dims take the per-operation path)
+    if (hd != 64 && hd != 128) return false;
     const int nsplit = mk_nsplit(c.max_seq_len);
     size_t mx = mk_attn_lds(hd);
     auto gemv = [&](int mode, int N, int K, const void* gamma, bool norm, int subs, MkPhase& ph) -> bool {
