@@ -1072,6 +1072,9 @@ __device__ __forceinline__ void mk_attn_phase(const MkArgs& a, const MkPhase& od
     mk_attn_t<HD>(a, od, rp, smem, last_flag, kv, kvwait ? want : 0u, spins);
 }
 
+// One kernel per head dim (64: drafter, 128: verifier), so that each holds one attention
+// instantiation: the code of a launch then stays closer to the instruction cache's size.
+template <int HD>
 __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ MkPhase op_lds[2];
@@ -1107,8 +1110,7 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
             }
             mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag, bf);
         } else if (op == kMkAttn) {
-            if (a.hd == 64) mk_attn_phase<64>(a, o, rp, smem, &last_flag, gen, spins, p);
-            else mk_attn_phase<128>(a, o, rp, smem, &last_flag, gen, spins, p);
+            mk_attn_phase<HD>(a, o, rp, smem, &last_flag, gen, spins, p);
         }
         mk_vmwait();  // this phase's stores are complete before the workgroup counts in
         if (threadIdx.x < kWords && p + 1 < a.nphase) ((uint32_t*)&op_lds[(p + 1) & 1])[threadIdx.x] = nw;
@@ -1413,11 +1415,11 @@ bool mk_build(Engine& e, int batch) {
     }
     if ((int)prog.size() > s.prog_cap) return false;
     s.lds = lds;
-    if (hipFuncSetAttribute((const void*)k_mk, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-        return false;
+    for (const void* fn : {(const void*)k_mk<64>, (const void*)k_mk<128>})
+        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) return false;
     int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, (const void*)k_mk, kMkThreads, lds) != hipSuccess || occ < 1)
-        return false;
+    for (const void* fn : {(const void*)k_mk<64>, (const void*)k_mk<128>})
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kMkThreads, lds) != hipSuccess || occ < 1) return false;
     if (hipMemcpyAsync(s.prog, prog.data(), sizeof(MkPhase) * prog.size(), hipMemcpyHostToDevice, e.stream) !=
         hipSuccess)
         return false;
@@ -1475,7 +1477,8 @@ hipError_t mk_launch(Engine& e, int j) {
     void* args[] = {&a};
     ProfEntry* pe = prof_slot(&e, kProfProgram, s.bytes[j]);
     if (pe) (void)hipEventRecord(pe->a, e.stream);
-    hipError_t err = hipLaunchCooperativeKernel((const void*)k_mk, dim3(s.G), dim3(kMkThreads), args, s.lds, e.stream);
+    const void* fn = m.hd == 64 ? (const void*)k_mk<64> : (const void*)k_mk<128>;
+    hipError_t err = hipLaunchCooperativeKernel(fn, dim3(s.G), dim3(kMkThreads), args, s.lds, e.stream);
     if (pe) {
         (void)hipEventRecord(pe->b, e.stream);
         prof_commit(&e);
