@@ -1,6 +1,6 @@
 // Persistent per-launch "round program" kernel (one cooperative launch per drafter step and one
 // for the verifier's block pass): the host records the sequence of phases of a launch once, the
-// kernel walks it with a grid barrier between phases.
+// kernel walks it, with a grid barrier between phases (a KV-head counter wait before attention).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>

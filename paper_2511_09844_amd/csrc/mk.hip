@@ -1,23 +1,24 @@
 // Persistent round-program kernel: one cooperative launch runs a whole drafter step (embedding
 // with the steering injection, every decoder layer, the LM head) or the verifier's (k+1)-row
-// block pass, as a fixed list of phases separated by grid barriers.
+// block pass, as a fixed list of phases.
 //
 // Why: a decode step at batch 1 is a chain of ~80 dependent weight-streaming projections and
 // attention passes.  As separate kernels each pays the launch's own start/finish cost (several
 // microseconds on this part) plus a cold start of its loads; inside one persistent launch a
-// phase boundary is a grid barrier (about 2 us), descriptors are prefetched, and the weights of
-// a phase start streaming as soon as the barrier opens.
+// phase boundary is a grid barrier (one atomic, one store and one poll round trip after the last
+// arrival) or, before attention, a wait on the counter of the unit's KV head; descriptors are
+// prefetched, and the first weight unit of a projection streams while its workgroup waits.
 //
-// Workgroups: one per compute unit, 8 waves; every weight load of a phase has returned before the
-// grid barrier, so the thread that runs it never waits behind weight traffic.
+// Workgroups: one per compute unit, 8 waves, every wave streaming weights.
 //
 // Memory protocol (no device-scope fences: on this part a release fence writes back the whole
 // L2): every value one workgroup produces for another is written with device-scope
 // (write-through) stores and completed (s_waitcnt) before the producer counts in at a barrier
-// or a hand-off counter; consumers read it with ordinary loads.  That is safe because every
+// or on a hand-off counter; consumers read it with ordinary loads.  That is safe because every
 // such buffer is written once per launch before anybody reads it (activations, residuals,
-// partials each get their own region per phase; cache rows are appended before they are read),
-// so no workgroup can hold a stale copy in its caches, which are invalidated at launch start.
+// partials each get their own region per phase; cache rows are appended before they are read,
+// and a cache line holds one row), so no workgroup can hold a stale copy in its caches, which
+// are invalidated at launch start.
 #include <hip/hip_ext.h>
 #include <math.h>
 
