@@ -265,6 +265,19 @@ __device__ __forceinline__ const uint16_t* mk_uptr(const MkArgs& a, const MkGeo&
     return mk_row(q.ow, a.hd, tile, q.subs == 2 ? (u & 1) : 0, n) + q.k0 + q.kw0 + 16 * qq;
 }
 
+// Activation rows m0 .. m0 + R - 1 (rows past M re-read row M - 1), NJ float4 columns per thread
+// (columns past the K range re-read its last one), all loads issued before any is used.
+template <int R, int NJ>
+__device__ __forceinline__ void mk_xload(float4 (&xv)[8][2], const float* X, int m0, int M, int K, int k0, int n4, int tid) {
+#pragma unroll
+    for (int mm = 0; mm < R; ++mm)
+#pragma unroll
+        for (int jc = 0; jc < NJ; ++jc) {
+            const int m = min(m0 + mm, M - 1), c = min(tid + 512 * jc, n4 - 1);
+            xv[mm][jc] = mk_ldg4(X + (size_t)m * K + k0 + 4 * c);
+        }
+}
+
 // Embedding row value of activation row m, column c (+ steering for drafter launches).
 __device__ __forceinline__ float mk_embed_at(const MkArgs& a, const MkRows& rp, int m, int c) {
     if (rp.pos[m] < 0) return 0.f;
@@ -419,22 +432,36 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
     } else {
         for (int m0 = 0; m0 < M; m0 += 8) {
             float4 xv[8][2];
+            if (oxsrc == kMkXEmbed) {
     #pragma unroll
-            for (int mm = 0; mm < 8; ++mm)
+                for (int mm = 0; mm < 8; ++mm)
     #pragma unroll
-                for (int jc = 0; jc < 2; ++jc) {
-                    const int m = m0 + mm, c = tid + 512 * jc;
-                    xv[mm][jc] = make_float4(0.f, 0.f, 0.f, 0.f);
-                    if (m < M && tid < kNT && c < n4) {
-                        if (oxsrc == kMkXEmbed) {
+                    for (int jc = 0; jc < 2; ++jc) {
+                        const int m = m0 + mm, c = tid + 512 * jc;
+                        xv[mm][jc] = make_float4(0.f, 0.f, 0.f, 0.f);
+                        if (m < M && tid < kNT && c < n4) {
                             const int cc = k0 + 4 * c;
                             xv[mm][jc] = make_float4(mk_embed_at(a, rp, m, cc), mk_embed_at(a, rp, m, cc + 1),
                                                      mk_embed_at(a, rp, m, cc + 2), mk_embed_at(a, rp, m, cc + 3));
-                        } else {
-                            xv[mm][jc] = mk_ldg4(oX + (size_t)m * oK + k0 + 4 * c);
                         }
                     }
+            } else {
+                // every row's loads are issued before any is used: no per-element branches (rows
+                // past M and columns past the range re-read the last one; they are not staged)
+                const int nr = min(8, M - m0), nj = n4 > 512 ? 2 : 1;
+                const int rr = nr <= 1 ? 1 : nr <= 2 ? 2 : nr <= 4 ? 4 : 8;
+                if (nj == 1) {
+                    if (rr == 1) mk_xload<1, 1>(xv, oX, m0, M, oK, k0, n4, tid);
+                    else if (rr == 2) mk_xload<2, 1>(xv, oX, m0, M, oK, k0, n4, tid);
+                    else if (rr == 4) mk_xload<4, 1>(xv, oX, m0, M, oK, k0, n4, tid);
+                    else mk_xload<8, 1>(xv, oX, m0, M, oK, k0, n4, tid);
+                } else {
+                    if (rr == 1) mk_xload<1, 2>(xv, oX, m0, M, oK, k0, n4, tid);
+                    else if (rr == 2) mk_xload<2, 2>(xv, oX, m0, M, oK, k0, n4, tid);
+                    else if (rr == 4) mk_xload<4, 2>(xv, oX, m0, M, oK, k0, n4, tid);
+                    else mk_xload<8, 2>(xv, oX, m0, M, oK, k0, n4, tid);
                 }
+            }
             float sq[8];
     #pragma unroll
             for (int mm = 0; mm < 8; ++mm) {
