@@ -265,6 +265,35 @@ __device__ __forceinline__ const uint16_t* mk_uptr(const MkArgs& a, const MkGeo&
     return mk_row(q.ow, a.hd, tile, q.subs == 2 ? (u & 1) : 0, n) + q.k0 + q.kw0 + 16 * qq;
 }
 
+// Fold a batch of up to 16 span partials (output, max, sum; the first cnt of them are live) into
+// a running (max, sum, output) without branches, so that every load of the batch is issued before
+// the first is used (a skip on "no live span" let the compiler sink the output loads behind it).
+// Scaling by exp(0) = 1 and adding zero weights leave the sums exactly as with skips.
+__device__ __forceinline__ void mk_fold16(const float4 (&v)[16], const float2 (&ml)[16], int cnt, float& Mx, float& L,
+                                          float4& O) {
+    float cm = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) cm = i < cnt ? fmaxf(cm, ml[i].x) : cm;
+    const float nm = fmaxf(Mx, cm);
+    const float sc = Mx == -INFINITY ? 0.f : expf(Mx - nm);
+    L *= sc;
+    O.x *= sc;
+    O.y *= sc;
+    O.z *= sc;
+    O.w *= sc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const bool live = i < cnt && ml[i].x != -INFINITY;
+        const float w = live ? expf(ml[i].x - nm) : 0.f;
+        L += w * ml[i].y;
+        O.x += w * v[i].x;
+        O.y += w * v[i].y;
+        O.z += w * v[i].z;
+        O.w += w * v[i].w;
+    }
+    Mx = nm;
+}
+
 // Activation rows m0 .. m0 + R - 1 (rows past M re-read row M - 1), NJ float4 columns per thread
 // (columns past the K range re-read its last one), all loads issued before any is used.
 template <int R, int NJ>
@@ -389,30 +418,7 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                         v[i] = mk_ldg4(e2 + d);
                         ml[i] = mk_ldg2(e2 + HD);
                     }
-                    float cm = -INFINITY;
-#pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        if (s0 + i < nl) cm = fmaxf(cm, ml[i].x);
-                    if (cm == -INFINITY) continue;
-                    if (cm > Mx) {
-                        const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
-                        L *= sc;
-                        O.x *= sc;
-                        O.y *= sc;
-                        O.z *= sc;
-                        O.w *= sc;
-                        Mx = cm;
-                    }
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        if (s0 + i >= nl || ml[i].x == -INFINITY) continue;
-                        const float w = expf(ml[i].x - Mx);
-                        L += w * ml[i].y;
-                        O.x += w * v[i].x;
-                        O.y += w * v[i].y;
-                        O.z += w * v[i].z;
-                        O.w += w * v[i].w;
-                    }
+                    mk_fold16(v, ml, nl - s0, Mx, L, O);
                 }
                 if (L > 0.f) {
                     const float inv = 1.f / L;
@@ -989,30 +995,7 @@ __device__ __forceinline__ void mk_attn_t(const MkArgs& a, const MkPhase& od, co
                         v[i] = mk_ldg4(e2 + d);
                         ml[i] = mk_ldg2(e2 + HD);
                     }
-                    float cm = -INFINITY;
-#pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        if (s0 + i < nl) cm = fmaxf(cm, ml[i].x);
-                    if (cm == -INFINITY) continue;
-                    if (cm > Mx) {
-                        const float sc = Mx == -INFINITY ? 0.f : expf(Mx - cm);
-                        L *= sc;
-                        O.x *= sc;
-                        O.y *= sc;
-                        O.z *= sc;
-                        O.w *= sc;
-                        Mx = cm;
-                    }
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        if (s0 + i >= nl || ml[i].x == -INFINITY) continue;
-                        const float w = expf(ml[i].x - Mx);
-                        L += w * ml[i].y;
-                        O.x += w * v[i].x;
-                        O.y += w * v[i].y;
-                        O.z += w * v[i].z;
-                        O.w += w * v[i].w;
-                    }
+                    mk_fold16(v, ml, nl - s0, Mx, L, O);
                 }
                 if (L > 0.f) {
                     const float inv = 1.f / L;
