@@ -687,18 +687,21 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
         const int tile = g + jt * gs;
         const float* pt = opart + (size_t)tile * oS * osubs * 256;
         if (tid < 256) {
-            // all S partials are requested before any is added (one memory round trip)
+            // all S partials are requested before any is added (one memory round trip): the loads
+            // are unconditional (ranges past S re-read the last; all S are complete here), the
+            // sums take the first S in order
             float p0[8], p1[8];
 #pragma unroll
-            for (int s0 = 0; s0 < 8; ++s0) {
-                p0[s0] = s0 < oS ? mk_ldg(pt + (size_t)s0 * osubs * 256 + tid) : 0.f;
-                p1[s0] = (s0 < oS && osubs == 2) ? mk_ldg(pt + (size_t)s0 * osubs * 256 + 256 + tid) : 0.f;
+            for (int s0 = 0; s0 < 8; ++s0) p0[s0] = mk_ldg(pt + (size_t)min(s0, oS - 1) * osubs * 256 + tid);
+            if (osubs == 2) {
+#pragma unroll
+                for (int s0 = 0; s0 < 8; ++s0) p1[s0] = mk_ldg(pt + (size_t)min(s0, oS - 1) * 2 * 256 + 256 + tid);
             }
             float v0 = 0.f, v1 = 0.f;
 #pragma unroll
             for (int s0 = 0; s0 < 8; ++s0) {
-                v0 += p0[s0];
-                v1 += p1[s0];
+                v0 += s0 < oS ? p0[s0] : 0.f;
+                if (osubs == 2) v1 += s0 < oS ? p1[s0] : 0.f;
             }
             epilogue(jt, v0, osubs == 2 ? v1 : v0);
         }
