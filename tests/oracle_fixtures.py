@@ -66,3 +66,10 @@ MK3 = Workload(
 MK4 = Workload(
     name="mk-long-ragged", verifier=Dims(1, 512, 8, 2, 1024, 2048, 5e5), drafter=Dims(1, 512, 8, 2, 1024, 2048, 5e5),
     dtype="bf16", k=3, batch=3, prompt=(40, 300), new_tokens=24, temperature=1.0, seed=15)
+# More attention units than workgroups on the persistent path: verifier with 8 KV heads, 3 groups of
+# 8 query vectors (6 rows x 4 query heads per KV head) and a 730-token prompt (12 live spans of 64
+# positions): 8 x 3 x 12 = 288 units on 256 workgroups, so some workgroups take a second unit.
+MK5 = Workload(
+    name="mk-many-attention-units", verifier=Dims(1, 2048, 32, 8, 1024, 2048, 5e5),
+    drafter=Dims(1, 1024, 16, 8, 1024, 2048, 5e5),
+    dtype="bf16", k=5, batch=1, prompt=(730, 730), new_tokens=8, temperature=1.0, seed=17)

@@ -2,7 +2,7 @@
 CPU oracle on small shapes that path takes, and the one-kernel-per-operation path on the same."""
 import pytest
 
-from oracle_fixtures import MK1, MK2, MK3, MK4
+from oracle_fixtures import MK1, MK2, MK3, MK4, MK5
 
 pytestmark = pytest.mark.gpu
 
@@ -36,3 +36,9 @@ def test_mk_long_ragged_contexts_persistent():
 
 def test_mk_long_ragged_contexts_separate_kernels():
     _run(MK4, expect_path=0, separate_kernels=True)
+
+
+def test_mk_more_attention_units_than_workgroups():
+    # 288 verifier attention units on 256 workgroups: the second unit of a workgroup waits for its
+    # KV head's counter and loads all of its span after the phase has started
+    _run(MK5, expect_path=1)
