@@ -23,8 +23,10 @@ enum MkOp : int32_t { kMkGemv = 1, kMkAttn = 2 };
 enum MkX : int32_t { kMkXBuf = 0, kMkXEmbed = 1, kMkXAttn = 2 };
 
 // One phase.  GEMV: Y (op)= W . xn over `tiles` 16-row tiles, K cut into S ranges of KR columns;
-// each unit is a tile times a 512-column slice per wave, wpu waves per tile.  ATTN: causal GQA
-// attention of the launch's rows over the cache of layer `layer`.
+// each unit is a tile times a 512-column slice per wave, wpu waves per tile (gate|up: a tile is
+// 16 features with a gate and an up sub-tile when subs == 2, else 8 gate + 8 up rows).  ATTN:
+// causal GQA attention of the launch's rows over the cache of layer `layer`, in units of
+// (sequence, KV head, group of up to 8 query vectors, 64-position span).
 struct MkPhase {
     int32_t op, mode, K, tiles, S, KR, wpu, subs, nseg, xsrc, res_embed, ldy;
     int32_t seg_tiles[3];
@@ -40,7 +42,7 @@ struct MkPhase {
     float* ss_out;           // Add: per-16-column sums of squares of the new residual, or null
     const int32_t* out_map;  // Store: output row of each row (-1: none), or null
     float* part;             // S > 1: [tiles][S][subs][256] partial tiles
-    int32_t* cnt;            // S > 1: arrival counter per tile; ATTN: per (sequence, KV head)
+    int32_t* cnt;            // S > 1: arrival counter per tile; ATTN: per (sequence, KV head, query group)
     float* qout;             // Qkv: queries [M][H*hd]; ATTN: query source
     float* aout;             // ATTN: output [M][H*hd]
     float* apart;            // ATTN: partials [M][H][nsplit][hd+4] (outputs, span max, span sum)
