@@ -204,7 +204,7 @@ def main():
         summarize_pmc(*args.summarize_pmc, TRAFFIC_FILE if args.write_traffic else None)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build", file=sys.stderr)
+        print(f"bench.py measures one GPU only (the round runs on one device); --gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
 
     import torch

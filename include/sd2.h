@@ -46,7 +46,7 @@ typedef int32_t sd2_status;
 #define SD2_ERR_CAPACITY (-2)      /* prompt + generation would exceed max_seq_len */
 #define SD2_ERR_STATE (-3)         /* e.g. sd2_round before sd2_prefill */
 #define SD2_ERR_HIP (-4)           /* a HIP runtime call failed; see sd2_last_error */
-#define SD2_ERR_UNSUPPORTED (-5)   /* valid request this build does not handle */
+#define SD2_ERR_UNSUPPORTED (-5)   /* valid request the library does not handle */
 
 typedef struct sd2_handle* sd2_handle_t;
 
