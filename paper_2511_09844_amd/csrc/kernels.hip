@@ -518,17 +518,26 @@ __global__ __launch_bounds__(256) void k_pick_partial(SampArgs a) {
     uint32_t t = (uint32_t)a.t[b];
     ArgBest best{-INFINITY, 0x7fffffff};
     for (int q = v0 + 4 * threadIdx.x; q < v1; q += 4 * blockDim.x) {
+        // the 4 logits are read unconditionally (index clamped) before any comparison, so the
+        // loads are not serialised behind per-element branches
+        float r4[4];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) r4[e2] = row[min(q + e2, v1 - 1)];
         if (a.T > 0.0f) {
             U4 w = philox10(U4{(uint32_t)q >> 2, (uint32_t)a.j, t, (kDraft << 24) | (uint32_t)b}, (uint32_t)a.seed,
                             (uint32_t)(a.seed >> 32));
             uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-            for (int e2 = 0; e2 < 4 && q + e2 < v1; ++e2) {
-                float sc = row[q + e2] / a.T + gumbel(ws[e2]);
+#pragma unroll
+            for (int e2 = 0; e2 < 4; ++e2) {
+                if (q + e2 >= v1) break;
+                float sc = r4[e2] / a.T + gumbel(ws[e2]);
                 if (better(sc, q + e2, best.s, best.i)) best = ArgBest{sc, q + e2};
             }
         } else {
-            for (int e2 = 0; e2 < 4 && q + e2 < v1; ++e2) {
-                float sc = row[q + e2];
+#pragma unroll
+            for (int e2 = 0; e2 < 4; ++e2) {
+                if (q + e2 >= v1) break;
+                float sc = r4[e2];
                 if (better(sc, q + e2, best.s, best.i)) best = ArgBest{sc, q + e2};
             }
         }
@@ -570,7 +579,15 @@ __global__ __launch_bounds__(256) void k_row_partial(SampArgs a) {
     VPart& p = a.part[(size_t)rowid * kVocabChunks + c];
     if (a.T > 0.0f) {
         float m = -INFINITY, sm = 0.0f;
-        for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x) lse_merge(m, sm, row[v] / a.T, 1.0f);
+        // 8 logits per thread are read (index clamped) before they are merged, in the same order
+        for (int vb = v0 + threadIdx.x; vb < v1; vb += 8 * blockDim.x) {
+            float x[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x[i] = row[min(vb + i * (int)blockDim.x, v1 - 1)];
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (vb + i * (int)blockDim.x < v1) lse_merge(m, sm, x[i] / a.T, 1.0f);
+        }
         wave_lse(m, sm);
         int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
         if (lane == 0) { shm[wave] = m; shs[wave] = sm; }
@@ -583,41 +600,74 @@ __global__ __launch_bounds__(256) void k_row_partial(SampArgs a) {
     } else {
         ArgBest best{-INFINITY, 0x7fffffff};
         if (i <= a.k)
-            for (int v = v0 + threadIdx.x; v < v1; v += blockDim.x)
-                if (better(row[v], v, best.s, best.i)) best = ArgBest{row[v], v};
+            for (int vb = v0 + threadIdx.x; vb < v1; vb += 8 * blockDim.x) {
+                float x[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] = row[min(vb + e * (int)blockDim.x, v1 - 1)];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int v = vb + e * (int)blockDim.x;
+                    if (v < v1 && better(x[e], v, best.s, best.i)) best = ArgBest{x[e], v};
+                }
+            }
         block_argbest(best, sha);
         if (threadIdx.x == 0) { p.best = best.s; p.idx = best.i; }
     }
 }
 
-// Accept/reject: one wave per sequence.
+// Accept/reject: one wave per sequence.  Every row's partials and every draft's two logits are
+// requested before any is used (lane i fetches draft i's pair), then lane 0 scans the drafts.
 __global__ __launch_bounds__(64) void k_accept(SampArgs a) {
     int b = blockIdx.x, lane = threadIdx.x;
     int per = 2 * a.k + 1;
     __shared__ float lse[2 * kMaxK + 1];
     __shared__ int amax[kMaxK + 1];
-    for (int i = 0; i < per; ++i) {
-        const VPart& p = a.part[((size_t)b * per + i) * kVocabChunks + lane];
-        if (a.T > 0.0f) {
-            float m = p.m, sm = p.s;
-            wave_lse(m, sm);
-            if (lane == 0) lse[i] = m + logf(sm);
-        } else if (i <= a.k) {
-            ArgBest best = wave_argbest(ArgBest{p.best, p.idx});
-            if (lane == 0) amax[i] = best.i;
+    __shared__ float lpv[kMaxK], lqv[kMaxK];
+    const int* dr = a.drafts + b * a.k;
+    float xv = 0.f, xd = 0.f;
+    if (a.T > 0.0f && lane < a.k) {
+        const int x = dr[lane];
+        xv = a.logits_v[((size_t)b * (a.k + 1) + lane) * a.V + x];
+        xd = a.logits_d[((size_t)b * a.k + lane) * a.V + x];
+    }
+    // rows in batches of 8: the batch's loads (indices clamped, unconditional) and then its
+    // independent wave reductions
+    for (int i0 = 0; i0 < per; i0 += 8) {
+        float f0[8], f1[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const VPart& p = a.part[((size_t)b * per + min(i0 + i, per - 1)) * kVocabChunks + lane];
+            f0[i] = a.T > 0.0f ? p.m : p.best;
+            f1[i] = a.T > 0.0f ? p.s : __int_as_float(p.idx);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int r = i0 + i;
+            if (r >= per) break;
+            if (a.T > 0.0f) {
+                float m = f0[i], sm = f1[i];
+                wave_lse(m, sm);
+                if (lane == 0) lse[r] = m + logf(sm);
+            } else if (r <= a.k) {
+                ArgBest best = wave_argbest(ArgBest{f0[i], __float_as_int(f1[i])});
+                if (lane == 0) amax[r] = best.i;
+            }
         }
     }
+    if (a.T > 0.0f && lane < a.k) {
+        lpv[lane] = xv;
+        lqv[lane] = xd;
+    }
+    __syncthreads();
     if (lane != 0) return;
-    const int* dr = a.drafts + b * a.k;
     uint32_t t = (uint32_t)a.t[b];
     int n = 0;
     if (a.T > 0.0f) {
         for (int i = 0; i <= a.k; ++i) a.lse_v[b * (a.k + 1) + i] = lse[i];
         for (int i = 0; i < a.k; ++i) a.lse_d[b * a.k + i] = lse[a.k + 1 + i];
         for (int i = 0; i < a.k; ++i) {
-            int x = dr[i];
-            float lp = a.logits_v[((size_t)b * (a.k + 1) + i) * a.V + x] / a.T - lse[i];
-            float lq = a.logits_d[((size_t)b * a.k + i) * a.V + x] / a.T - lse[a.k + 1 + i];
+            float lp = lpv[i] / a.T - lse[i];
+            float lq = lqv[i] / a.T - lse[a.k + 1 + i];
             float ratio = lp - lq;
             float lu = logf(u01(rng_word(a.seed, (uint32_t)i, 0u, t, kAccept, (uint32_t)b, 0)));
             if (!(lu < ratio)) break;
@@ -656,14 +706,23 @@ __global__ __launch_bounds__(256) void k_final_partial(SampArgs a) {
         U4 w = philox10(U4{(uint32_t)q >> 2, 0u, t, (kFinal << 24) | (uint32_t)b}, (uint32_t)a.seed,
                         (uint32_t)(a.seed >> 32));
         uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-        for (int e2 = 0; e2 < 4 && q + e2 < v1; ++e2) {
+        // the 4 logits of each row are read (index clamped) before any is used
+        float p4[4], q4[4];
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+            p4[e2] = pr[min(q + e2, v1 - 1)];
+            q4[e2] = qr ? qr[min(q + e2, v1 - 1)] : 0.0f;
+        }
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+            if (q + e2 >= v1) break;
             int v = q + e2;
             float g = gumbel(ws[e2]);
-            float sp = pr[v] / a.T + g;
+            float sp = p4[e2] / a.T + g;
             if (better(sp, v, bp.s, bp.i)) bp = ArgBest{sp, v};
             if (qr) {
-                float p = expf(pr[v] / a.T - lp);
-                float qq = expf(qr[v] / a.T - lq);
+                float p = expf(p4[e2] / a.T - lp);
+                float qq = expf(q4[e2] / a.T - lq);
                 float r = p - qq;
                 if (r > 0.0f) {
                     flag = 1;
