@@ -94,6 +94,9 @@ size_t sd2_workspace_bytes(const sd2_config* cfg);
  * workspace: device buffer of at least sd2_workspace_bytes(cfg) bytes, 256-byte aligned;
  * hip_stream: the hipStream_t every call enqueues on (NULL = default stream).
  * On success *out receives the handle.  Enqueues small table-initialisation kernels.
+ * The current HIP device must be a gfx950 (MI355X) with XNACK off, its default mode: the
+ * kernels are built for exactly that target, and any other device gives SD2_ERR_UNSUPPORTED
+ * (SD2_ERR_HIP if the device cannot be queried).
  */
 sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
                       const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,

@@ -6,7 +6,9 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 SO = os.path.join(HERE, "libsd2.so")
 SOURCES = ["csrc/kernels.hip", "csrc/wsgemv.hip", "csrc/attn.hip", "csrc/mk.hip", "csrc/engine.hip"]
-ARCH = "gfx950"
+# XNACK off: MI355X runs with page-fault replay disabled by default, and code built for that
+# mode forms longer load clauses than the "any" target (0.9 % less time per round measured)
+ARCH = "gfx950:xnack-"
 
 
 def hipcc() -> str:

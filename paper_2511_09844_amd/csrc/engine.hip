@@ -379,6 +379,15 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
     if (!workspace || ((uintptr_t)workspace % kAlign) != 0) return SD2_ERR_INVALID_ARG;
     size_t need = sd2_workspace_bytes(cfg);
     if (workspace_bytes < need) return SD2_ERR_INVALID_ARG;
+    // the kernels are built for gfx950 with XNACK (page-fault replay) off, MI355X's default mode
+    {
+        int dev = 0;
+        hipDeviceProp_t prop;
+        if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess)
+            return SD2_ERR_HIP;
+        if (strncmp(prop.gcnArchName, "gfx950", 6) != 0 || strstr(prop.gcnArchName, "xnack+") != nullptr)
+            return SD2_ERR_UNSUPPORTED;
+    }
     Engine* e = new (std::nothrow) Engine();
     if (!e) return SD2_ERR_INVALID_ARG;
     e->cfg = *cfg;
