@@ -53,7 +53,8 @@ def _load():
         i32, u32, u64, f32 = ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_float
         lib.oracle_create.restype = P
         lib.oracle_create.argtypes = [P, P, P, P, ctypes.c_int, P, P, P, ctypes.c_int, ctypes.c_int,
-                                      ctypes.c_int, ctypes.c_int, f32, u64]
+                                      ctypes.c_int, ctypes.c_int, f32, u64, ctypes.c_int, P, P, P,
+                                      ctypes.c_double]
         lib.oracle_destroy.argtypes = [P]
         lib.oracle_prefill_one.argtypes = [P, ctypes.c_int, P, ctypes.c_int]
         lib.oracle_prefill_one.restype = ctypes.c_int
@@ -66,6 +67,9 @@ def _load():
         lib.oracle_round_log_size.restype = ctypes.c_int
         lib.oracle_forward.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P]
         lib.oracle_steer.argtypes = [P, P, P]
+        lib.oracle_get_ubias.argtypes = [P, ctypes.c_int, P]
+        lib.oracle_forward_mlp.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P, P]
+        lib.oracle_mlp_steer.argtypes = [P, P, P]
         lib.oracle_philox.argtypes = [P, u32, u32, P]
         lib.oracle_uniform.argtypes = [u32]
         lib.oracle_uniform.restype = f32
@@ -136,9 +140,13 @@ class Oracle:
 
     ``wv`` / ``wd`` are dicts as returned by ``sd2_inputs.model_weights`` and
     ``ws`` is W_s [d_D][d_V]; arrays must stay alive (they are referenced).
+    ``mlp`` selects the MLP steering of eq. (2) instead: a dict as returned by
+    ``sd2_inputs.mlp_steer_weights`` (w_s [L_D*F_D][d_V], w_hml [d_V][3 d_V],
+    ln_gain, ln_bias, ln_eps); ``ws`` is then ignored.
     """
 
-    def __init__(self, wl, wv, wd, ws, max_batch=None, cap=None, temperature=None, k=None, max_new=None):
+    def __init__(self, wl, wv, wd, ws, max_batch=None, cap=None, temperature=None, k=None, max_new=None,
+                 mlp=None):
         lib = _load()
         self.wl = wl
         self.k = wl.k if k is None else k
@@ -151,11 +159,23 @@ class Oracle:
         self._dd, self._rd = _dims(wl.drafter)
         self._pv, self._keep_v = _ptrs(wv)
         self._pd, self._keep_d = _ptrs(wd)
-        self._ws = ws
+        self.mlp = mlp
+        if mlp is None:
+            self._ws = ws
+            form, extra = 0, (None, None, None, 0.0)
+        else:
+            self._ws = mlp["w_s"]
+            for key in ("w_s", "w_hml", "ln_gain", "ln_bias"):
+                assert mlp[key].flags["C_CONTIGUOUS"]
+            form = 1
+            extra = (mlp["w_hml"].ctypes.data, mlp["ln_gain"].ctypes.data, mlp["ln_bias"].ctypes.data,
+                     float(mlp["ln_eps"]))
         self.h = lib.oracle_create(self._dv.ctypes.data, self._rv.ctypes.data, self._dd.ctypes.data,
                                    self._rd.ctypes.data, 1 if wl.dtype == "bf16" else 0, self._pv, self._pd,
-                                   ws.ctypes.data, self.k, self.max_batch, self.cap, self.max_new,
-                                   float(self.temperature), int(wl.seed))
+                                   self._ws.ctypes.data, self.k, self.max_batch, self.cap, self.max_new,
+                                   float(self.temperature), int(wl.seed), form, *extra)
+        if not self.h:
+            raise ValueError("oracle_create rejected the steering arguments")
         self.lib = lib
 
     def close(self):
@@ -238,3 +258,36 @@ class Oracle:
         s = np.zeros(self.wl.drafter.d_model, dtype=np.float64)
         self.lib.oracle_steer(self.h, h.ctypes.data, s.ctypes.data)
         return s
+
+    def ubias(self, b):
+        """MLP steering: the up-projection biases [L_D][F_D] of sequence b for its next round."""
+        dm = self.wl.drafter
+        out = np.zeros((dm.n_layers, dm.d_ff), dtype=np.float64)
+        self.lib.oracle_get_ubias(self.h, b, out.ctypes.data)
+        return out
+
+    def forward_mlp(self, which, toks, ubias=None, taps=False):
+        """Whole-sequence forward with optional up-projection biases [L][F] on every row; returns
+        (hF [n][d], logits [n][V], taps [n][3][d] or None) in float64."""
+        dm = self.wl.verifier if which == 0 else self.wl.drafter
+        toks = np.ascontiguousarray(toks, dtype=np.int32)
+        n = len(toks)
+        hF = np.zeros((n, dm.d_model), dtype=np.float64)
+        lg = np.zeros((n, dm.vocab), dtype=np.float64)
+        tp = np.zeros((n, 3, dm.d_model), dtype=np.float64) if taps else None
+        ub = None
+        if ubias is not None:
+            ubias = np.ascontiguousarray(ubias, dtype=np.float64)
+            assert ubias.shape == (dm.n_layers, dm.d_ff)
+            ub = ubias.ctypes.data
+        self.lib.oracle_forward_mlp(self.h, which, toks.ctypes.data, n, ub, tp.ctypes.data if taps else None,
+                                    hF.ctypes.data, lg.ctypes.data)
+        return hF, lg, tp
+
+    def mlp_steer(self, z):
+        """ub = W_s LayerNorm(W_hml z) for z = [h; m; l] (3 d_V); returns [L_D][F_D]."""
+        dm = self.wl.drafter
+        z = np.ascontiguousarray(z, dtype=np.float64).reshape(-1)
+        ub = np.zeros((dm.n_layers, dm.d_ff), dtype=np.float64)
+        self.lib.oracle_mlp_steer(self.h, z.ctypes.data, ub.ctypes.data)
+        return ub

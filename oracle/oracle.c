@@ -35,6 +35,15 @@
  *   - steering tap: the verifier's final-norm hidden state at the row whose
  *     logits produced the final token, i.e. the position of the last token
  *     returned (Sec. "Verification"), projected by W_s.
+ *   - MLP steering, the paper's own form (eq. (2), Sec. "Verification" and
+ *     "Drafting", Fig. 2, training details): the verifier's residual stream
+ *     after decoder blocks L-2, floor(L/2) and 3 (counted from 1; high,
+ *     middle, low) at that same row is concatenated as [h; m; l], mapped by
+ *     W_hml to g, passed through a LayerNorm (population variance, gain and
+ *     shift), and W_s g gives one bias per drafter layer (rows l*F..(l+1)*F of
+ *     W_s), added to the up projection before the gating product:
+ *     W_d((W_u a + b_l) * SiLU(W_g a)).  The bias is computed once per round
+ *     and used for every drafter token processed in that round.
  *   - greedy regime (T = 0): argmax drafts, accept iff the draft equals the
  *     verifier's argmax, final token = verifier argmax (Sec. "Decoding
  *     Parameters").
@@ -169,15 +178,26 @@ static size_t kv_index(const odims* dm, int cap, int layer, int pos, int h) {
     return (((size_t)layer * cap + pos) * dm->n_kv_heads + h) * hd;
 }
 
+/* Decoder blocks whose outputs are the steering taps, in the order h, m, l:
+ * blocks L-2, floor(L/2) and 3 counted from 1, as 0-based layer indices. */
+static void tap_layers(int L, int out[3]) {
+    out[0] = L - 3;
+    out[1] = L / 2 - 1;
+    out[2] = 2;
+}
+
 /*
  * Forward of m consecutive tokens at positions pos0..pos0+m-1 of one sequence
  * whose cache holds positions 0..pos0-1.  `add` (d doubles, may be NULL) is
- * added to every input embedding (the steering injection).  Writes the
- * final-norm hidden state of every row to hF[m][d] and, when logits != NULL,
- * the logits of every row to logits[m][vocab].
+ * added to every input embedding (the steering injection).  `ubias` (NULL for
+ * none) holds one bias of d_ff values per layer, added to the up projection
+ * before the gating product (eq. (2)).  `taps` (NULL for none) receives, per
+ * row, the residual stream after the three tap blocks: taps[m][3][d].  Writes
+ * the final-norm hidden state of every row to hF[m][d] and, when
+ * logits != NULL, the logits of every row to logits[m][vocab].
  */
 static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32_t* toks,
-                          const double* add, double* hF, double* logits) {
+                          const double* add, const double* ubias, double* taps, double* hF, double* logits) {
     const odims* dm = &M->dm;
     int d = dm->d_model, H = dm->n_heads, Hkv = dm->n_kv_heads, F = dm->d_ff;
     int hd = d / H, group = H / Hkv;
@@ -246,9 +266,20 @@ static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32
         for (int r = 0; r < m; ++r) rmsnorm(M->bf16, Wl[W_FFN_NORM], d, dm->rms_eps, x + (size_t)r * d, nrm + (size_t)r * d);
         matmul_rows(M->bf16, Wl[W_GATE], F, d, nrm, m, gate);
         matmul_rows(M->bf16, Wl[W_UP], F, d, nrm, m, up);
-        for (size_t i = 0; i < (size_t)m * F; ++i) gate[i] = silu(gate[i]) * up[i];
+        for (size_t i = 0; i < (size_t)m * F; ++i) {
+            double u = up[i] + (ubias ? ubias[(size_t)l * F + i % F] : 0.0);
+            gate[i] = silu(gate[i]) * u;
+        }
         matmul_rows(M->bf16, Wl[W_DOWN], d, F, gate, m, proj);
         for (size_t i = 0; i < (size_t)m * d; ++i) x[i] += proj[i];
+        if (taps) {
+            int tl[3];
+            tap_layers(dm->n_layers, tl);
+            for (int sl = 0; sl < 3; ++sl)
+                if (tl[sl] == l)
+                    for (int r = 0; r < m; ++r)
+                        memcpy(taps + ((size_t)r * 3 + sl) * d, x + (size_t)r * d, (size_t)d * sizeof(double));
+        }
     }
     for (int r = 0; r < m; ++r) rmsnorm(M->bf16, M->final_norm, d, dm->rms_eps, x + (size_t)r * d, hF + (size_t)r * d);
     if (logits) matmul_rows(M->bf16, M->lm_head, dm->vocab, d, hF, m, logits);
@@ -383,7 +414,11 @@ void oracle_accept_final(int k, int V, float T, uint64_t seed, int t, int b, con
 /* ----------------------------------------------------------------------- */
 typedef struct {
     omodel V, D;
-    const void* w_s;           /* [d_D][d_V], same storage type as the models */
+    const void* w_s;           /* form 0: [d_D][d_V]; form 1: [L_D*F_D][d_V]; storage type of the models */
+    int form;                  /* 0: input-embedding steering; 1: MLP steering (eq. (2)) */
+    const void *w_hml, *ln_gain, *ln_bias;   /* form 1: W_hml [d_V][3 d_V], LayerNorm gain and shift [d_V] */
+    double ln_eps;
+    double* ub;                /* form 1: [max_batch][L_D*F_D] up-projection biases of the current round */
     int k, max_batch, cap, max_new;
     float temperature;
     uint64_t seed;
@@ -408,7 +443,10 @@ static okv kv_alloc(const odims* dm, int cap) {
 ostate* oracle_create(const int32_t* dims_v, const double* rope_eps_v, const int32_t* dims_d,
                       const double* rope_eps_d, int bf16, const void* const* ptrs_v, const void* const* ptrs_d,
                       const void* w_s, int k, int max_batch, int cap, int max_new, float temperature,
-                      uint64_t seed) {
+                      uint64_t seed, int form, const void* w_hml, const void* ln_gain, const void* ln_bias,
+                      double ln_eps) {
+    /* MLP steering taps decoder block 3: the verifier needs at least three layers */
+    if (form != 0 && (form != 1 || dims_v[0] < 3 || !w_hml || !ln_gain || !ln_bias)) return NULL;
     ostate* st = calloc(1, sizeof(ostate));
     omodel* ms[2] = {&st->V, &st->D};
     const int32_t* dims[2] = {dims_v, dims_d};
@@ -427,6 +465,10 @@ ostate* oracle_create(const int32_t* dims_v, const double* rope_eps_v, const int
         M->lm_head = ptrs[i][2 + (size_t)M->dm.n_layers * W_PER_LAYER];
     }
     st->w_s = w_s;
+    st->form = form;
+    st->w_hml = w_hml; st->ln_gain = ln_gain; st->ln_bias = ln_bias; st->ln_eps = ln_eps;
+    if (form == 1)
+        st->ub = calloc((size_t)max_batch * st->D.dm.n_layers * st->D.dm.d_ff, sizeof(double));
     st->k = k; st->max_batch = max_batch; st->cap = cap; st->max_new = max_new;
     st->temperature = temperature; st->seed = seed;
     st->hist = calloc((size_t)max_batch * cap, sizeof(int32_t));
@@ -450,12 +492,33 @@ void oracle_destroy(ostate* st) {
     free(st->kv_v); free(st->kv_d);
     free(st->hist); free(st->t); free(st->len_v); free(st->len_d); free(st->produced); free(st->done);
     free(st->s);
+    free(st->ub);
     free(st);
 }
 
 /* s = W_s h  (W_s is [d_D][d_V]) */
 static void steer(const ostate* st, const double* h, double* s) {
     matmul_rows(st->V.bf16, st->w_s, st->D.dm.d_model, st->V.dm.d_model, h, 1, s);
+}
+
+/* MLP steering (eq. (2)): g = LayerNorm(W_hml [h; m; l]), then the per-layer
+ * up-projection biases ub = W_s g ([L_D*F_D]).  z holds [h; m; l] (3 d_V). */
+static void mlp_steer(const ostate* st, const double* z, double* ub) {
+    int dV = st->V.dm.d_model;
+    int nb = st->D.dm.n_layers * st->D.dm.d_ff;
+    double* g = malloc((size_t)dV * sizeof(double));
+    matmul_rows(st->V.bf16, st->w_hml, dV, 3 * dV, z, 1, g);
+    double mean = 0.0;
+    for (int i = 0; i < dV; ++i) mean += g[i];
+    mean /= dV;
+    double var = 0.0;
+    for (int i = 0; i < dV; ++i) var += (g[i] - mean) * (g[i] - mean);
+    var /= dV;
+    double inv = 1.0 / sqrt(var + st->ln_eps);
+    for (int i = 0; i < dV; ++i)
+        g[i] = (g[i] - mean) * inv * wval(st->V.bf16, st->ln_gain, i) + wval(st->V.bf16, st->ln_bias, i);
+    matmul_rows(st->V.bf16, st->w_s, nb, dV, g, 1, ub);
+    free(g);
 }
 
 /*
@@ -475,13 +538,21 @@ int oracle_prefill_one(ostate* st, int b, const int32_t* prompt, int p) {
     memcpy(st->hist + (size_t)b * st->cap, prompt, (size_t)p * sizeof(int32_t));
     double* s = st->s + (size_t)b * dD;
     for (int i = 0; i < dD; ++i) s[i] = 0.0;
+    size_t nb = (size_t)st->D.dm.n_layers * st->D.dm.d_ff;
+    double* ub = st->form == 1 ? st->ub + (size_t)b * nb : NULL;
+    if (ub)
+        for (size_t i = 0; i < nb; ++i) ub[i] = 0.0;
     if (p >= 2) {
         double* hF = malloc((size_t)(p - 1) * dV * sizeof(double));
-        forward_block(&st->V, &st->kv_v[b], 0, p - 1, prompt, NULL, hF, NULL);
-        steer(st, hF + (size_t)(p - 2) * dV, s);
+        double* taps = ub ? malloc((size_t)(p - 1) * 3 * dV * sizeof(double)) : NULL;
+        forward_block(&st->V, &st->kv_v[b], 0, p - 1, prompt, NULL, NULL, taps, hF, NULL);
+        if (ub) mlp_steer(st, taps + (size_t)(p - 2) * 3 * dV, ub);
+        else steer(st, hF + (size_t)(p - 2) * dV, s);
         free(hF);
+        free(taps);
+        /* the drafter processes the prompt without steering */
         double* hD = malloc((size_t)(p - 1) * dD * sizeof(double));
-        forward_block(&st->D, &st->kv_d[b], 0, p - 1, prompt, NULL, hD, NULL);
+        forward_block(&st->D, &st->kv_d[b], 0, p - 1, prompt, NULL, NULL, NULL, hD, NULL);
         free(hD);
     }
     st->t[b] = p;
@@ -510,6 +581,7 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
     int32_t* hist = st->hist + (size_t)b * st->cap;
     int t = st->t[b];
     double* s = st->s + (size_t)b * dD;
+    double* ub = st->form == 1 ? st->ub + (size_t)b * st->D.dm.n_layers * st->D.dm.d_ff : NULL;
     lg->active = 1;
     lg->t_start = t;
 
@@ -532,7 +604,7 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
             m = 1;
             in = &drafts[j - 2];
         }
-        forward_block(&st->D, &st->kv_d[b], pos0, m, in, s, hD, dl);
+        forward_block(&st->D, &st->kv_d[b], pos0, m, in, ub ? NULL : s, ub, NULL, hD, dl);
         float* q = qlog + (size_t)(j - 1) * V;
         for (int v = 0; v < V; ++v) q[v] = (float)dl[(size_t)(m - 1) * V + v];
         float margin;
@@ -547,7 +619,8 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
     for (int i = 0; i < k; ++i) blk[i + 1] = drafts[i];
     double* hF = malloc((size_t)(k + 1) * dV * sizeof(double));
     double* vl = malloc((size_t)(k + 1) * V * sizeof(double));
-    forward_block(&st->V, &st->kv_v[b], t - 1, k + 1, blk, NULL, hF, vl);
+    double* taps = ub ? malloc((size_t)(k + 1) * 3 * dV * sizeof(double)) : NULL;
+    forward_block(&st->V, &st->kv_v[b], t - 1, k + 1, blk, NULL, NULL, taps, hF, vl);
     for (size_t i = 0; i < (size_t)(k + 1) * V; ++i) plog[i] = (float)vl[i];
 
     /* ---- accept / reject, final token ---- */
@@ -566,13 +639,14 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
     st->len_v[b] = t + n;
     st->len_d[b] = (t + k - 1 < t + n) ? t + k - 1 : t + n;
     st->t[b] = t + n + 1;
-    steer(st, hF + (size_t)n * dV, s);
+    if (ub) mlp_steer(st, taps + (size_t)n * 3 * dV, ub);
+    else steer(st, hF + (size_t)n * dV, s);
 
     if (logits_v_dump) memcpy(logits_v_dump, plog, (size_t)(k + 1) * V * sizeof(float));
     if (logits_d_dump) memcpy(logits_d_dump, qlog, (size_t)k * V * sizeof(float));
     if (hf_v_dump) memcpy(hf_v_dump, hF, (size_t)(k + 1) * dV * sizeof(double));
     for (int i = 0; i < k; ++i) lg->drafts[i] = drafts[i];
-    free(qlog); free(plog); free(dl); free(hD); free(hF); free(vl);
+    free(qlog); free(plog); free(dl); free(hD); free(hF); free(vl); free(taps);
     return 0;
 }
 
@@ -591,6 +665,12 @@ void oracle_get_steer(const ostate* st, int b, double* out) {
 
 void oracle_set_steer(ostate* st, int b, const double* in) {
     memcpy(st->s + (size_t)b * st->D.dm.d_model, in, (size_t)st->D.dm.d_model * sizeof(double));
+}
+
+/* Form 1: the up-projection biases [L_D*F_D] of sequence b for its next round. */
+void oracle_get_ubias(const ostate* st, int b, double* out) {
+    size_t nb = (size_t)st->D.dm.n_layers * st->D.dm.d_ff;
+    memcpy(out, st->ub + (size_t)b * nb, nb * sizeof(double));
 }
 
 void oracle_get_hist(const ostate* st, int b, int32_t* out, int n) {
@@ -612,11 +692,11 @@ void oracle_forward(const ostate* st, int which, const int32_t* toks, int n, con
     const omodel* M = which == 0 ? &st->V : &st->D;
     okv kv = kv_alloc(&M->dm, n);
     if (!add) {
-        forward_block(M, &kv, 0, n, toks, NULL, hF, logits);
+        forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, hF, logits);
     } else {
         int d = M->dm.d_model;
         for (int i = 0; i < n; ++i)
-            forward_block(M, &kv, i, 1, toks + i, add + (size_t)i * d, hF + (size_t)i * d,
+            forward_block(M, &kv, i, 1, toks + i, add + (size_t)i * d, NULL, NULL, hF + (size_t)i * d,
                           logits ? logits + (size_t)i * M->dm.vocab : NULL);
     }
     free(kv.k);
@@ -625,3 +705,21 @@ void oracle_forward(const ostate* st, int which, const int32_t* toks, int n, con
 
 /* Steering projection on its own: s = W_s h. */
 void oracle_steer(const ostate* st, const double* h, double* s) { steer(st, h, s); }
+
+/*
+ * Whole-sequence forward with the MLP-steering pieces exposed: optional
+ * per-layer up-projection biases ubias[L][d_ff] (NULL for none) applied to
+ * every row, and the three steering taps of every row, taps[n][3][d] (NULL for
+ * none).  Outputs as oracle_forward.
+ */
+void oracle_forward_mlp(const ostate* st, int which, const int32_t* toks, int n, const double* ubias, double* taps,
+                        double* hF, double* logits) {
+    const omodel* M = which == 0 ? &st->V : &st->D;
+    okv kv = kv_alloc(&M->dm, n);
+    forward_block(M, &kv, 0, n, toks, NULL, ubias, taps, hF, logits);
+    free(kv.k);
+    free(kv.v);
+}
+
+/* MLP steering on its own: ub = W_s LayerNorm(W_hml z), z = [h; m; l]. */
+void oracle_mlp_steer(const ostate* st, const double* z, double* ub) { mlp_steer(st, z, ub); }

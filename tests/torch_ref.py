@@ -1,9 +1,12 @@
 """Independent float64 forward of the SwiGLU decoder with PyTorch library ops.
 
-Used only to pin the oracle's model forward.  It shares nothing with the
-oracle: attention is ``torch.nn.functional.scaled_dot_product_attention``
-with a causal mask, RoPE is a complex rotation (``torch.polar``), the MLP uses
-``torch.nn.functional.silu``, and the matrix products are ``torch`` matmuls.
+Used only to pin the oracle's model forward and its MLP steering.  It shares
+nothing with the oracle: attention is
+``torch.nn.functional.scaled_dot_product_attention`` with a causal mask, RoPE
+is a complex rotation (``torch.polar``), the MLP uses
+``torch.nn.functional.silu``, the steering LayerNorm is
+``torch.nn.functional.layer_norm``, and the matrix products are ``torch``
+matmuls.
 """
 import numpy as np
 import torch
@@ -29,8 +32,17 @@ def rope_complex(x, pos, theta):
     return torch.cat([z.real, z.imag], dim=-1)
 
 
-def forward(dm, w, dtype, toks, add=None):
-    """Causal forward of a whole sequence; returns (final-norm hidden [T][d], logits [T][V])."""
+def tap_blocks(L):
+    """Decoder blocks (counted from 1) whose outputs feed W_hml, in the order high, middle, low."""
+    return [L - 2, L // 2, 3]
+
+
+def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False):
+    """Causal forward of a whole sequence; returns (final-norm hidden [T][d], logits [T][V]).
+
+    ubias: up-projection biases added before the gating product, [L][F] for every row or
+    [T][L][F] per row.  taps=True also returns the residual stream after the tap blocks,
+    [T][3][d]."""
     T = len(toks)
     d, H, Hkv, hd = dm.d_model, dm.n_heads, dm.n_kv_heads, dm.head_dim
     toks_t = torch.as_tensor(np.asarray(toks, dtype=np.int64))
@@ -38,11 +50,13 @@ def forward(dm, w, dtype, toks, add=None):
     if add is not None:
         x = x + torch.as_tensor(add, dtype=torch.float64)
     pos = torch.arange(T)
+    ub = None if ubias is None else torch.as_tensor(np.asarray(ubias), dtype=torch.float64)
+    outs = []
 
     def norm(v, g):
         return v * torch.rsqrt(v.pow(2).mean(-1, keepdim=True) + dm.rms_eps) * _t(g, dtype)
 
-    for layer in w["layers"]:
+    for li, layer in enumerate(w["layers"]):
         an, wq, wk, wv, wo, fn, wg, wu, wd = layer
         n = norm(x, an)
         q = (n @ _t(wq, dtype).T).view(T, H, hd).transpose(0, 1)
@@ -55,6 +69,23 @@ def forward(dm, w, dtype, toks, add=None):
         o = F.scaled_dot_product_attention(q[None], k[None], v[None], is_causal=True)[0]
         x = x + o.transpose(0, 1).reshape(T, H * hd) @ _t(wo, dtype).T
         n2 = norm(x, fn)
-        x = x + (F.silu(n2 @ _t(wg, dtype).T) * (n2 @ _t(wu, dtype).T)) @ _t(wd, dtype).T
+        up = n2 @ _t(wu, dtype).T
+        if ub is not None:
+            up = up + (ub[li] if ub.dim() == 2 else ub[:, li, :])
+        x = x + (F.silu(n2 @ _t(wg, dtype).T) * up) @ _t(wd, dtype).T
+        outs.append(x)
     hF = norm(x, w["final_norm"])
-    return hF.numpy(), (hF @ _t(w["lm_head"], dtype).T).numpy()
+    logits = (hF @ _t(w["lm_head"], dtype).T).numpy()
+    if not taps:
+        return hF.numpy(), logits
+    tp = torch.stack([outs[blk - 1] for blk in tap_blocks(len(w["layers"]))], dim=1)
+    return hF.numpy(), logits, tp.numpy()
+
+
+def mlp_steer(z, mlp, dtype, n_layers, d_ff):
+    """Per-layer up-projection biases [L][F] from z = [h; m; l]: W_s LayerNorm(W_hml z)."""
+    zt = torch.as_tensor(np.asarray(z, dtype=np.float64)).reshape(-1)
+    g = _t(mlp["w_hml"], dtype) @ zt
+    g = F.layer_norm(g, (g.shape[0],), weight=_t(mlp["ln_gain"], dtype), bias=_t(mlp["ln_bias"], dtype),
+                     eps=mlp["ln_eps"])
+    return (_t(mlp["w_s"], dtype) @ g).reshape(n_layers, d_ff).numpy()
