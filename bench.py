@@ -38,13 +38,22 @@ def kv_row_bytes(dm):
     return dm.n_layers * dm.n_kv_heads * dm.head_dim * 2 * 4
 
 
-def round_bytes(wl, t_avg):
+def steer_weight_bytes(wl, es, steering="input"):
+    """Steering weights read once per round: W_s [d_D][d_V] (input form), or W_hml [d_V][3 d_V]
+    plus the per-layer W_s [L_D F_D][d_V] (MLP form)."""
+    dV = wl.verifier.d_model
+    if steering == "mlp":
+        return (3 * dV * dV + wl.drafter.n_layers * wl.drafter.d_ff * dV) * es
+    return wl.drafter.d_model * dV * es
+
+
+def round_bytes(wl, t_avg, steering="input"):
     """Algorithmic HBM bytes of one round for one sequence at round-start length t_avg:
-    every weight once per forward (verifier once, drafter k times, W_s once) plus the KV rows
-    each attention pass must read and the rows it appends."""
+    every weight once per forward (verifier once, drafter k times, steering weights once) plus
+    the KV rows each attention pass must read and the rows it appends."""
     es = 2 if wl.dtype == "bf16" else 4
     k = wl.k
-    w = weight_bytes(wl.verifier, es) + k * weight_bytes(wl.drafter, es) + wl.drafter.d_model * wl.verifier.d_model * es
+    w = weight_bytes(wl.verifier, es) + k * weight_bytes(wl.drafter, es) + steer_weight_bytes(wl, es, steering)
     kv_v = (t_avg + k + (k + 1)) * kv_row_bytes(wl.verifier)
     kv_d = (k * t_avg + k * (k - 1) / 2 + (k + 1)) * kv_row_bytes(wl.drafter)
     return w, kv_v, kv_d
@@ -187,6 +196,9 @@ def main():
     ap.add_argument("--prof-rounds", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--steering", choices=["input", "mlp"], default="input",
+                    help="input: s = W_s h added to the drafter's input embeddings; mlp: the paper's eq. (2) "
+                         "per-layer up-projection biases from three verifier layers (no CPU baseline)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the rounds, copy one 1 GiB buffer (a plain copy of known size, the reference "
                          "point for scaling hardware traffic counters)")
@@ -215,7 +227,7 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     t0 = time.time()
-    keep_host = not args.no_cpu_baseline
+    keep_host = not args.no_cpu_baseline and args.steering == "input"
     host = {0: {"layers": []}, 1: {"layers": []}}
     models = []
     for which in (0, 1):
@@ -234,12 +246,23 @@ def main():
         models.append(B.DeviceModel(items, dev))
         del items
         log(f"model {which} generated and uploaded ({time.time() - t0:.1f}s)")
-    ws = si.steer_weights(wl)
-    ws_dev = B.to_device(ws, dev)
+    mlp_dev = None
+    if args.steering == "mlp":
+        mlp = si.mlp_steer_weights(wl)
+        mlp_dev = {key: B.to_device(mlp[key], dev) for key in ("w_s", "w_hml", "ln_gain", "ln_bias")}
+        mlp_dev["ln_eps"] = mlp["ln_eps"]
+        del mlp
+        ws, ws_dev = None, None
+        log(f"MLP steering weights generated and uploaded ({time.time() - t0:.1f}s)")
+    else:
+        ws = si.steer_weights(wl)
+        ws_dev = B.to_device(ws, dev)
     toks, lens = si.prompts(wl)
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
-        eng = B.Engine(B.config_of(wl), models[0], models[1], ws_dev, stream=stream, device=dev)
+        steer_form = B.STEER_MLP if mlp_dev is not None else B.STEER_INPUT
+        eng = B.Engine(B.config_of(wl, steering=steer_form), models[0], models[1], ws_dev, stream=stream,
+                       device=dev, mlp=mlp_dev)
         t_tok = torch.from_numpy(toks).to(dev)
         t_len = torch.from_numpy(lens).to(dev)
         torch.cuda.synchronize()
@@ -290,7 +313,7 @@ def main():
     w_b, kvv_b, kvd_b = 0.0, 0.0, 0.0
     for b in active:
         t_avg = st0[b]["t"] + (st1[b]["t"] - st0[b]["t"]) * (args.steps - 1) / (2 * args.steps)
-        w, kvv, kvd = round_bytes(wl, t_avg)
+        w, kvv, kvd = round_bytes(wl, t_avg, args.steering)
         w_b = w
         kvv_b += kvv
         kvd_b += kvd
@@ -336,7 +359,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16 weights, f32 activations/KV" if wl.dtype == "bf16" else "f32",
         "data": "synthetic: seeded N(0,0.02) weights, uniform-random prompt ids",
-        "config": {"workload": wl.name, "batch": wl.batch, "k": wl.k, "prompt": list(wl.prompt),
+        "config": {"workload": wl.name, "steering": args.steering, "batch": wl.batch, "k": wl.k,
+                   "prompt": list(wl.prompt),
                    "new_tokens": wl.new_tokens, "temperature": wl.temperature,
                    "verifier": f"L{wl.verifier.n_layers} d{wl.verifier.d_model} H{wl.verifier.n_heads}/"
                                f"{wl.verifier.n_kv_heads} F{wl.verifier.d_ff} V{wl.verifier.vocab}",
@@ -347,13 +371,13 @@ def main():
         "round_hbm_frac": bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS,
         "roofline": {"bound": "hbm", "kernel": r_kernel,
                      "achieved": gemv_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gemv_gbs / PEAK_HBM_GBS,
-                     "traffic": stored_traffic(wl.name) if p_n else None,
+                     "traffic": stored_traffic(wl.name) if p_n and args.steering == "input" else None,
                      "launches_per_round": g_n / max(1, args.prof_rounds),
                      "avg_launch_us": g_ms / max(1, g_n) * 1e3,
                      "bytes_per_launch": g_by / max(1, g_n)},
         "cpu_baseline": None,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.steering == "input":
         result["cpu_baseline"] = cpu_baseline(wl, host[0], host[1], ws, toks, lens, args.cpu_budget)
     eng.close()
     print(json.dumps(result), flush=True)

@@ -83,7 +83,26 @@ typedef struct {
     int32_t max_new_tokens;        /* generated tokens per sequence; its last round is truncated */
     float temperature;             /* 0 => greedy (argmax drafts, accept iff draft == verifier argmax) */
     uint64_t seed;                 /* Philox4x32-10 key of every random draw */
+    int32_t steering;              /* SD2_STEER_INPUT (sd2_create) or SD2_STEER_MLP (sd2_create_mlp) */
 } sd2_config;
+
+/* How the drafter is steered by the verifier (sd2_config.steering). */
+#define SD2_STEER_INPUT 0  /* s = W_s hF (verifier final-norm hidden state, d_V -> d_D) added to the
+                              drafter's input embedding of every token it processes in the round */
+#define SD2_STEER_MLP 1    /* the paper's eq. (2): g = LayerNorm(W_hml [h; m; l]) from the verifier's
+                              residual stream after decoder blocks L_V-2, floor(L_V/2) and 3 (counted
+                              from 1; high, middle, low; training details) and one bias b_l = W_s^(l) g
+                              per drafter layer, added to the up projection before the gating product:
+                              W_d((W_u a + b_l) * SiLU(W_g a)).  Needs L_V >= 3. */
+
+/* Weights of SD2_STEER_MLP, device pointers in the configuration's dtype, 16-byte aligned. */
+typedef struct {
+    const void* w_s;       /* [L_D * d_ff_D][d_V]: rows l*d_ff_D .. (l+1)*d_ff_D - 1 give layer l's bias */
+    const void* w_hml;     /* [d_V][3 d_V]: g = W_hml [h; m; l] (columns: h, then m, then l) */
+    const void* ln_gain;   /* [d_V] LayerNorm gain */
+    const void* ln_bias;   /* [d_V] LayerNorm shift */
+    float ln_eps;          /* LayerNorm: (g - mean) / sqrt(var + eps) * gain + shift, population variance */
+} sd2_mlp_steering;
 
 /* Bytes of device workspace sd2_create needs for cfg (0 if cfg is invalid). */
 size_t sd2_workspace_bytes(const sd2_config* cfg);
@@ -101,6 +120,18 @@ size_t sd2_workspace_bytes(const sd2_config* cfg);
 sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
                       const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
                       sd2_handle_t* out);
+
+/*
+ * Create a handle whose drafter is steered by the paper's MLP biases (eq. (2); Sec.
+ * "Verification" and "Drafting"): cfg->steering must be SD2_STEER_MLP.  Everything else is as
+ * sd2_create.  The bias is recomputed at the end of every round from the verifier row whose
+ * logits produced the final token, and used for every drafter token of the next round;
+ * the drafter processes the prompt without steering, and the first round's bias comes from
+ * the verifier at position len-2 (zero when len == 1).
+ */
+sd2_status sd2_create_mlp(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                          const sd2_mlp_steering* steering, void* workspace, size_t workspace_bytes,
+                          void* hip_stream, sd2_handle_t* out);
 
 /*
  * Prefill `batch` sequences (1..max_batch) with their prompts.
@@ -145,7 +176,7 @@ const char* sd2_last_error(sd2_handle_t h);
 /* What sd2_debug_read copies (all host-side, after synchronising the stream). */
 #define SD2_DBG_LOGITS_V 1    /* float [batch][k+1][vocab]: last round's verifier logits */
 #define SD2_DBG_LOGITS_D 2    /* float [batch][k][vocab]: last round's drafter logits (row j drew draft j) */
-#define SD2_DBG_STEER 3       /* float [batch][d_drafter]: current steering vector s */
+#define SD2_DBG_STEER 3       /* float [batch][d_drafter]: current steering vector s (SD2_STEER_INPUT) */
 #define SD2_DBG_OWN_DRAFTS 4  /* int32 [batch][k]: drafts the library drew itself last round */
 #define SD2_DBG_OWN_N 5       /* int32 [batch]: accepted count the library computed itself */
 #define SD2_DBG_OWN_Y 6       /* int32 [batch]: final token the library drew itself */
@@ -159,6 +190,9 @@ const char* sd2_last_error(sd2_handle_t h);
                                  (100 MHz): entry 0 = start of launch j (0: verify pass, 1..k: drafter
                                  steps), entry p+1 = end of its phase p; SD2_ERR_STATE when that path
                                  is unavailable */
+
+#define SD2_DBG_UBIAS 12      /* float [batch][L_D][d_ff_D]: current up-projection biases (SD2_STEER_MLP;
+                                 SD2_ERR_STATE otherwise) */
 
 /* Copy a debug buffer of the last round into host memory dst (bytes must match). */
 sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes);

@@ -16,9 +16,9 @@ P = ctypes.c_void_p
 SD2_OK = 0
 STATUS = {0: "ok", -1: "invalid argument", -2: "capacity", -3: "state", -4: "hip error", -5: "unsupported"}
 DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V, DBG_PATH, \
-    DBG_TRACE = range(1, 12)
+    DBG_TRACE, DBG_UBIAS = range(1, 13)
 
-EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
+EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_create_mlp", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
            "sd2_status_string", "sd2_last_error", "sd2_debug_read", "sd2_profile", "sd2_profile_read"]
 PROF_GEMV, PROF_ATTN, PROF_SAMPLER, PROF_OTHER, PROF_PROGRAM = 1, 2, 3, 4, 5
 
@@ -36,7 +36,14 @@ class Weights(ctypes.Structure):
 class Config(ctypes.Structure):
     _fields_ = [("verifier", Dims), ("drafter", Dims), ("dtype", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("max_batch", ctypes.c_int32), ("max_seq_len", ctypes.c_int32), ("max_new_tokens", ctypes.c_int32),
-                ("temperature", ctypes.c_float), ("seed", ctypes.c_uint64)]
+                ("temperature", ctypes.c_float), ("seed", ctypes.c_uint64), ("steering", ctypes.c_int32)]
+
+
+STEER_INPUT, STEER_MLP = 0, 1
+
+
+class MlpSteering(ctypes.Structure):
+    _fields_ = [("w_s", P), ("w_hml", P), ("ln_gain", P), ("ln_bias", P), ("ln_eps", ctypes.c_float)]
 
 
 _lib = None
@@ -54,6 +61,9 @@ def load():
         lib.sd2_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights), P, P,
                                    ctypes.c_size_t, P, ctypes.POINTER(P)]
         lib.sd2_create.restype = ctypes.c_int32
+        lib.sd2_create_mlp.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights),
+                                       ctypes.POINTER(MlpSteering), P, ctypes.c_size_t, P, ctypes.POINTER(P)]
+        lib.sd2_create_mlp.restype = ctypes.c_int32
         lib.sd2_prefill.argtypes = [P, ctypes.c_int32, P, P, ctypes.c_int32]
         lib.sd2_prefill.restype = ctypes.c_int32
         lib.sd2_round.argtypes = [P, P, P]
@@ -81,14 +91,15 @@ def dims_of(dm) -> Dims:
     return Dims(dm.n_layers, dm.d_model, dm.n_heads, dm.n_kv_heads, dm.d_ff, dm.vocab, dm.rope_theta, dm.rms_eps)
 
 
-def config_of(wl, max_batch=None, max_seq_len=None, max_new_tokens=None, temperature=None, k=None, seed=None):
+def config_of(wl, max_batch=None, max_seq_len=None, max_new_tokens=None, temperature=None, k=None, seed=None,
+              steering=STEER_INPUT):
     return Config(dims_of(wl.verifier), dims_of(wl.drafter), 1 if wl.dtype == "bf16" else 0,
                   wl.k if k is None else k,
                   wl.batch if max_batch is None else max_batch,
                   wl.max_seq_len if max_seq_len is None else max_seq_len,
                   wl.new_tokens if max_new_tokens is None else max_new_tokens,
                   wl.temperature if temperature is None else temperature,
-                  wl.seed if seed is None else seed)
+                  wl.seed if seed is None else seed, steering)
 
 
 class Sd2Error(RuntimeError):
@@ -132,15 +143,19 @@ class DeviceModel:
 
 
 class Engine:
-    """One libsd2 handle.  `stream` is a torch.cuda.Stream (default: the current stream)."""
+    """One libsd2 handle.  `stream` is a torch.cuda.Stream (default: the current stream).
+
+    With `mlp` (a dict of device tensors w_s, w_hml, ln_gain, ln_bias and a float ln_eps) the
+    handle is created by sd2_create_mlp (cfg.steering must be STEER_MLP) and `w_steer` is unused."""
 
     def __init__(self, cfg: Config, verifier: DeviceModel, drafter: DeviceModel, w_steer: torch.Tensor,
-                 stream=None, device="cuda"):
+                 stream=None, device="cuda", mlp=None):
         lib = load()
         self.lib = lib
         self.cfg = cfg
         self.models = (verifier, drafter)
         self.w_steer = w_steer
+        self.mlp = mlp
         self.stream = stream if stream is not None else torch.cuda.current_stream()
         nbytes = lib.sd2_workspace_bytes(ctypes.byref(cfg))
         if nbytes == 0:
@@ -149,9 +164,17 @@ class Engine:
         base = self.workspace.data_ptr()
         off = (-base) % 256
         self.h = P()
-        rc = lib.sd2_create(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
-                            w_steer.data_ptr(), base + off, nbytes, self.stream.cuda_stream, ctypes.byref(self.h))
-        check(rc, None, "sd2_create")
+        if mlp is None:
+            rc = lib.sd2_create(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
+                                w_steer.data_ptr(), base + off, nbytes, self.stream.cuda_stream, ctypes.byref(self.h))
+            check(rc, None, "sd2_create")
+        else:
+            ms = MlpSteering(mlp["w_s"].data_ptr(), mlp["w_hml"].data_ptr(), mlp["ln_gain"].data_ptr(),
+                             mlp["ln_bias"].data_ptr(), float(mlp["ln_eps"]))
+            rc = lib.sd2_create_mlp(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
+                                    ctypes.byref(ms), base + off, nbytes, self.stream.cuda_stream,
+                                    ctypes.byref(self.h))
+            check(rc, None, "sd2_create_mlp")
         self.batch = 0
         k = cfg.k
         self.out_tokens = torch.zeros((cfg.max_batch, k + 1), dtype=torch.int32, device=device)
@@ -198,6 +221,7 @@ class Engine:
             DBG_OWN_Y: ((B,), np.int32), DBG_STATE: ((B, 5), np.int32),
             DBG_HIST: ((B, self.cfg.max_seq_len), np.int32), DBG_HIDDEN_V: ((B, k + 1, dV), np.float32),
             DBG_PATH: ((2,), np.int32), DBG_TRACE: ((33, 1024), np.int64),
+            DBG_UBIAS: ((B, self.cfg.drafter.n_layers, self.cfg.drafter.d_ff), np.float32),
         }
         shp, dt = shapes[what]
         out = np.zeros(shp, dtype=dt)

@@ -79,6 +79,11 @@ struct Workspace {
     int32_t* ws_cnt;
     float* attn_part;
     int32_t* attn_cnt;
+    // MLP steering (null unless cfg.steering == SD2_STEER_MLP)
+    float* taps;            // [3][maxm][d_V] verifier residual after the tap blocks (per-operation path)
+    float* tapsel;          // [max_batch][3 d_V] [h; m; l] of each sequence's steering row
+    float* gsteer;          // [max_batch][d_V] g = W_hml [h; m; l], then its LayerNorm
+    float* ubias;           // [max_batch][L_D][F_D] up-projection biases of the current round
 };
 
 // Per-launch timing entries (HIP events recorded on the engine's stream).
@@ -93,7 +98,11 @@ struct ProfEntry {
 struct Engine {
     sd2_config cfg;
     ModelDev mv, md;
-    const void* w_steer;
+    const void* w_steer;    // SD2_STEER_INPUT: [d_D][d_V]; SD2_STEER_MLP: [L_D*F_D][d_V]
+    bool mlp;               // cfg.steering == SD2_STEER_MLP
+    const void *w_hml, *ln_gain, *ln_bias;
+    float ln_eps;
+    int tap_layer[3];       // 0-based verifier layers after which h, m, l are taken
     Workspace ws;
     int cap, maxm, batch;
     bool prefilled;
@@ -131,10 +140,20 @@ void launch_init_maps(hipStream_t s, Engine& e);
 enum PlanKind { kPlanDraft1 = 0, kPlanDraftJ = 1, kPlanVerify = 2, kPlanPrefill = 3 };
 void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
                        const int32_t* prompt_len, int max_prompt, int chunk);
-void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps);
+// ubias (drafter rounds with MLP steering): this layer's biases, row stride ub_ld, indexed by
+// the row's sequence; null for none.
+void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps, const float* ubias = nullptr,
+                  int ub_ld = 0);
 // Final-norm LM head of `rows` residual rows into Y[out_map[r]] (bf16 path via the projection kernel).
 void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map);
 void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows);
+// MLP steering: copy the verifier residual rows after `layer` to the tap slots taken there.
+void launch_tap_copy(hipStream_t s, Engine& e, int layer, int rows);
+// Prefill: keep the tap rows at position len-2 of every sequence (slots taken after `layer`).
+void launch_prefill_tap(hipStream_t s, Engine& e, int layer, int rows, const int32_t* prompt_len, int max_prompt);
+// Gather [h; m; l] of row in_map[b] from src[3] ([rows][d_V] each) into tapsel, then
+// gsteer = LayerNorm(W_hml tapsel) and ubias = W_s gsteer, for `rows` sequences.
+void launch_mlp_steer(Engine& e, const float* const* src, const int32_t* in_map, int rows);
 enum Epi { kEpiStore = 0, kEpiAdd = 1, kEpiSwiglu = 2, kEpiQkv = 3 };
 
 // One bf16 weight-streaming projection (see wsgemv.hip).
@@ -160,6 +179,8 @@ struct WsCall {
     const float *rcos, *rsin;
     float *qout, *kc, *vc;
     int cap, max_batch, layer;
+    const float* ubias;  // SwiGLU: per-sequence up-projection bias rows (stride ub_ld, row_seq), or null
+    int ub_ld;
 };
 struct WsPlan {
     int KR, S, tiles, NW, steps, Gt;
@@ -172,7 +193,8 @@ int attn_nsplit(int cap);
 size_t attn_groups(int rows, int rps, int H, int Hkv);
 void launch_gemv(Engine* e, hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K,
                  const void* gamma, float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y,
-                 int ldy, const int32_t* out_map);
+                 int ldy, const int32_t* out_map, const float* ubias = nullptr, int ub_ld = 0,
+                 const int32_t* row_seq = nullptr);
 void launch_draft_pick(hipStream_t s, Engine& e, int j);
 void launch_verify_decide(hipStream_t s, Engine& e, int32_t* out_tokens, int32_t* out_counts);
 void launch_prefill_capture(hipStream_t s, Engine& e, int rows, const int32_t* prompt_len, int max_prompt);

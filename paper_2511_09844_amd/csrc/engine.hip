@@ -62,6 +62,15 @@ bool config_ok(const sd2_config* c) {
     if (c->max_new_tokens < 1) return false;
     if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // 8192 = 64 spans of 128
     if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
+    if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP) return false;
+    if (c->steering == SD2_STEER_MLP) {
+        // the low tap is block 3; a steering projection runs on the MFMA kernel when its K is a
+        // multiple of 256 (bf16), else on the vector kernel, which stages a K row of at most 16384
+        const int dV = c->verifier.d_model;
+        if (c->verifier.n_layers < 3) return false;
+        if (3 * dV > 16384 && !(c->dtype == SD2_BF16 && (3 * dV) % 256 == 0)) return false;
+        if (dV > 16384 && !(c->dtype == SD2_BF16 && dV % 256 == 0)) return false;
+    }
     return true;
 }
 
@@ -148,10 +157,22 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                     if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256 * subs);
                 }
         }
+        if (c.steering == SD2_STEER_MLP) {
+            // W_hml (d_V x 3 d_V) and W_s (L_D F_D x d_V) projections
+            int mshapes[2][2] = {{c.verifier.d_model, 3 * c.verifier.d_model},
+                                 {c.drafter.n_layers * c.drafter.d_ff, c.verifier.d_model}};
+            for (int mm = 1; mm <= std::min(B, 16); ++mm)
+                for (auto& sh : mshapes) {
+                    WsPlan p = ws_plan(mm, sh[0], sh[1], kEpiStore);
+                    if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256);
+                }
+        }
         w.ws_part = cv.take<float>(std::max<size_t>(pmax, 1));
         size_t tmax = (size_t)std::max(c.verifier.vocab, c.drafter.vocab) / 16 + 1;
         for (int i = 0; i < 2; ++i)
             tmax = std::max(tmax, (size_t)std::max(dd[i]->d_ff, dd[i]->d_model) / 16 + 1);
+        if (c.steering == SD2_STEER_MLP)
+            tmax = std::max(tmax, (size_t)c.drafter.n_layers * c.drafter.d_ff / 16 + 1);
         w.ws_cnt = cv.take<int32_t>(tmax);
     }
     {
@@ -175,6 +196,13 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
             }
         }
         w.attn_cnt = cv.take<int32_t>(gmax);
+    }
+    if (c.steering == SD2_STEER_MLP) {
+        const size_t dV = c.verifier.d_model;
+        w.taps = cv.take<float>(3 * (size_t)maxm * dV);
+        w.tapsel = cv.take<float>((size_t)B * 3 * dV);
+        w.gsteer = cv.take<float>((size_t)B * dV);
+        w.ubias = cv.take<float>((size_t)B * c.drafter.n_layers * c.drafter.d_ff);
     }
     for (int i = 0; i < 2; ++i) {
         ModelDev* m = ms[i];
@@ -282,22 +310,35 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
         hipError_t err = mk_launch(e, 0);
         if (err != hipSuccess) { e.launch_err = err; return; }
         launch_verify_decide(s, e, out_tokens, out_counts);
-        launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
+        if (e.mlp) launch_mlp_steer(e, e.mk.tap_x, e.ws.steer_map, B);
+        else launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
         return;
     }
+    const int ub_ld = e.md.dm.n_layers * e.md.dm.d_ff;
     for (int j = 1; j <= k; ++j) {
         int rows = j == 1 ? 2 * B : B;
         launch_plan_embed(s, e, e.md, j == 1 ? kPlanDraft1 : kPlanDraftJ, j, rows, nullptr, nullptr, 0, 1);
-        for (int l = 0; l < e.md.dm.n_layers; ++l) launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1);
+        for (int l = 0; l < e.md.dm.n_layers; ++l)
+            launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1, e.mlp ? e.ws.ubias + (size_t)l * e.md.dm.d_ff : nullptr,
+                         ub_ld);
         launch_lm_head(e, e.md, rows, e.ws.logits_d, e.ws.lm_map_d + (size_t)(j - 1) * 2 * e.cfg.max_batch);
         launch_draft_pick(s, e, j);
     }
     int rows = B * (k + 1);
     launch_plan_embed(s, e, e.mv, kPlanVerify, 0, rows, nullptr, nullptr, 0, 1);
-    for (int l = 0; l < e.mv.dm.n_layers; ++l) launch_layer(s, e, e.mv, l, rows, k + 1);
+    for (int l = 0; l < e.mv.dm.n_layers; ++l) {
+        launch_layer(s, e, e.mv, l, rows, k + 1);
+        if (e.mlp) launch_tap_copy(s, e, l, rows);
+    }
     launch_lm_head(e, e.mv, rows, e.ws.logits_v, nullptr);
     launch_verify_decide(s, e, out_tokens, out_counts);
-    launch_steer(e, e.mv.x, e.mv.ss, e.ws.steer_map, B);
+    if (e.mlp) {
+        const size_t slot = (size_t)e.maxm * e.mv.dm.d_model;
+        const float* src[3] = {e.ws.taps, e.ws.taps + slot, e.ws.taps + 2 * slot};
+        launch_mlp_steer(e, src, e.ws.steer_map, B);
+    } else {
+        launch_steer(e, e.mv.x, e.mv.ss, e.ws.steer_map, B);
+    }
 }
 
 void drop_graph(Engine& e) {
@@ -368,12 +409,16 @@ static bool weights_ok(const sd2_weights* w, const sd2_dims& d) {
     return true;
 }
 
-sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
-                      const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
-                      sd2_handle_t* out) {
+static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                              const void* w_steer, const sd2_mlp_steering* mlp, void* workspace,
+                              size_t workspace_bytes, void* hip_stream, sd2_handle_t* out) {
     if (!out) return SD2_ERR_INVALID_ARG;
     *out = nullptr;
     if (!config_ok(cfg)) return SD2_ERR_INVALID_ARG;
+    if ((cfg->steering == SD2_STEER_MLP) != (mlp != nullptr)) return SD2_ERR_INVALID_ARG;
+    if (mlp && (!aligned16(mlp->w_hml) || !aligned16(mlp->ln_gain) || !aligned16(mlp->ln_bias) ||
+                !(mlp->ln_eps >= 0.f)))
+        return SD2_ERR_INVALID_ARG;
     if (!weights_ok(verifier, cfg->verifier) || !weights_ok(drafter, cfg->drafter) || !aligned16(w_steer))
         return SD2_ERR_INVALID_ARG;
     if (!workspace || ((uintptr_t)workspace % kAlign) != 0) return SD2_ERR_INVALID_ARG;
@@ -395,6 +440,20 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
     e->bf16 = cfg->dtype == SD2_BF16;
     e->stream = (hipStream_t)hip_stream;
     e->w_steer = w_steer;
+    e->mlp = mlp != nullptr;
+    if (mlp) {
+        e->w_hml = mlp->w_hml;
+        e->ln_gain = mlp->ln_gain;
+        e->ln_bias = mlp->ln_bias;
+        e->ln_eps = mlp->ln_eps;
+    }
+    {
+        // blocks L-2, floor(L/2) and 3 counted from 1 (high, middle, low)
+        const int L = cfg->verifier.n_layers;
+        e->tap_layer[0] = L - 3;
+        e->tap_layer[1] = L / 2 - 1;
+        e->tap_layer[2] = 2;
+    }
     // Graph replay needs a capturable (non-null) stream; SD2_NO_GRAPH=1 forces eager launches.
     e->use_graph = hip_stream != nullptr && getenv("SD2_NO_GRAPH") == nullptr;
     carve(*cfg, (char*)workspace, &e->ws, &e->mv, &e->md, &e->maxm, &e->mk);
@@ -425,6 +484,23 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
     return SD2_OK;
 }
 
+sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                      const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
+                      sd2_handle_t* out) {
+    return create_impl(cfg, verifier, drafter, w_steer, nullptr, workspace, workspace_bytes, hip_stream, out);
+}
+
+sd2_status sd2_create_mlp(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                          const sd2_mlp_steering* steering, void* workspace, size_t workspace_bytes,
+                          void* hip_stream, sd2_handle_t* out) {
+    if (!steering) {
+        if (out) *out = nullptr;
+        return SD2_ERR_INVALID_ARG;
+    }
+    return create_impl(cfg, verifier, drafter, steering->w_s, steering, workspace, workspace_bytes, hip_stream,
+                       out);
+}
+
 sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, const int32_t* lens,
                        int32_t max_prompt) {
     if (!h) return SD2_ERR_INVALID_ARG;
@@ -440,10 +516,16 @@ sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, con
     if (err != hipSuccess) return hip_fail(e, err, "hipMemsetAsync");
     for (int c = 0; c < nchunks; ++c) {
         launch_plan_embed(s, *e, e->mv, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
-        for (int l = 0; l < e->mv.dm.n_layers; ++l) launch_layer(s, *e, e->mv, l, rows, chunk);
+        for (int l = 0; l < e->mv.dm.n_layers; ++l) {
+            launch_layer(s, *e, e->mv, l, rows, chunk);
+            if (e->mlp) launch_prefill_tap(s, *e, l, rows, lens, max_prompt);
+        }
         launch_prefill_capture(s, *e, rows, lens, max_prompt);
     }
-    launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, nullptr, batch);
+    // the first round's steering from position len-2 (a one-token prompt gets none: the finish
+    // step below clears it)
+    if (e->mlp) launch_mlp_steer(*e, nullptr, nullptr, batch);
+    else launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, nullptr, batch);
     for (int c = 0; c < nchunks; ++c) {
         launch_plan_embed(s, *e, e->md, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
         for (int l = 0; l < e->md.dm.n_layers; ++l) launch_layer(s, *e, e->md, l, rows, chunk);
@@ -551,6 +633,11 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
         case SD2_DBG_LOGITS_V: src = e->ws.logits_v; want = sizeof(float) * (size_t)B * (k + 1) * V; break;
         case SD2_DBG_LOGITS_D: src = e->ws.logits_d; want = sizeof(float) * (size_t)B * k * V; break;
         case SD2_DBG_STEER: src = e->ws.steer; want = sizeof(float) * (size_t)B * e->md.dm.d_model; break;
+        case SD2_DBG_UBIAS:
+            if (!e->mlp) return SD2_ERR_STATE;
+            src = e->ws.ubias;
+            want = sizeof(float) * (size_t)B * e->md.dm.n_layers * e->md.dm.d_ff;
+            break;
         case SD2_DBG_OWN_DRAFTS: src = e->ws.own_drafts; want = sizeof(int32_t) * (size_t)B * k; break;
         case SD2_DBG_OWN_N: src = e->ws.own_n; want = sizeof(int32_t) * (size_t)B; break;
         case SD2_DBG_OWN_Y: src = e->ws.own_y; want = sizeof(int32_t) * (size_t)B; break;

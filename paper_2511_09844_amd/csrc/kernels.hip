@@ -133,7 +133,7 @@ void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, i
     a.t = e.ws.t; a.len_d = e.ws.len_d; a.done = e.ws.done; a.hist = e.ws.hist; a.drafts = e.ws.drafts;
     a.prompt_tok = prompt_tok; a.prompt_len = prompt_len;
     a.steer = e.ws.steer;
-    a.add_steer = (&m == &e.md) && (kind == kPlanDraft1 || kind == kPlanDraftJ);
+    a.add_steer = !e.mlp && (&m == &e.md) && (kind == kPlanDraft1 || kind == kPlanDraftJ);
     a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq; a.x = m.x; a.ss = m.ss; a.embed = m.embed;
     prof_begin(&e, kProfOther, 0.0);
     if (e.bf16) k_plan_embed<uint16_t><<<rows, 256, 0, s>>>(a);
@@ -160,6 +160,9 @@ struct GemvArgs {
     float* Y;
     int ldy;
     const int32_t* out_map;
+    const float* ubias;       // SwiGLU with MLP steering: bias rows per sequence (row_seq), or null
+    int ub_ld;
+    const int32_t* row_seq;
 };
 
 constexpr int kGemvThreads = 256;
@@ -270,9 +273,15 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_vec(GemvArgs a) {
                 int orow = a.out_map ? a.out_map[m0 + m] : m0 + m;
                 if (orow >= 0) {
                     float* yp = a.Y + (size_t)orow * a.ldy + n;
-                    if (a.epi == kEpiStore) *yp = acc0[m];
-                    else if (a.epi == kEpiAdd) *yp += acc0[m];
-                    else *yp = silu(acc0[m]) * acc1[m];
+                    if (a.epi == kEpiStore) {
+                        *yp = acc0[m];
+                    } else if (a.epi == kEpiAdd) {
+                        *yp += acc0[m];
+                    } else {
+                        float up = acc1[m];
+                        if (a.ubias) up += a.ubias[(size_t)a.row_seq[m0 + m] * a.ub_ld + n];
+                        *yp = silu(acc0[m]) * up;
+                    }
                 }
             }
         }
@@ -281,8 +290,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_vec(GemvArgs a) {
 
 void launch_gemv(Engine* e, hipStream_t s, bool bf16, const float* X, const int32_t* in_map, int M, int K,
                  const void* gamma, float eps, const void* const* W, const int* seg_rows, int nseg, int epi, float* Y,
-                 int ldy, const int32_t* out_map) {
+                 int ldy, const int32_t* out_map, const float* ubias, int ub_ld, const int32_t* row_seq) {
     GemvArgs a;
+    a.ubias = ubias; a.ub_ld = ub_ld; a.row_seq = row_seq;
     a.X = X; a.in_map = in_map; a.M = M; a.K = K; a.gamma = gamma; a.eps = eps;
     int off = 0;
     for (int i = 0; i < 3; ++i) {
@@ -374,7 +384,8 @@ static WsCall ws_base(Engine& e, ModelDev& m) {
     return c;
 }
 
-void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps) {
+void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps, const float* ubias,
+                  int ub_ld) {
     const sd2_dims& dm = m.dm;
     const void* const* W = m.layer + (size_t)layer * 9;
     int hd = m.hd, H = dm.n_heads, Hkv = dm.n_kv_heads;
@@ -400,6 +411,7 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, in
         g.X = m.x; g.M = rows; g.K = dm.d_model; g.gamma = W[kFfnNorm]; g.ss = m.ss;
         g.W[0] = W[kWg]; g.W[1] = W[kWu]; g.seg_rows[0] = dm.d_ff; g.seg_rows[1] = dm.d_ff; g.nseg = 2;
         g.mode = kEpiSwiglu; g.Y = e.ws.ffh; g.ldy = dm.d_ff;
+        g.ubias = ubias; g.ub_ld = ub_ld; g.row_seq = e.ws.row_seq;
         launch_wsgemv(&e, s, g);
         // down projection + residual
         WsCall d = ws_base(e, m);
@@ -435,7 +447,7 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, in
         const void* ws[2] = {W[kWg], W[kWu]};
         int rws[2] = {dm.d_ff, dm.d_ff};
         launch_gemv(&e, s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kFfnNorm], dm.rms_eps, ws, rws, 2, kEpiSwiglu,
-                    e.ws.ffh, dm.d_ff, nullptr);
+                    e.ws.ffh, dm.d_ff, nullptr, ubias, ub_ld, e.ws.row_seq);
     }
     {
         const void* ws[1] = {W[kWd]};
@@ -473,6 +485,133 @@ void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_
     int rws[1] = {e.md.dm.d_model};
     launch_gemv(&e, e.stream, e.bf16, X, in_map, rows, e.mv.dm.d_model, e.mv.final_norm, e.mv.dm.rms_eps, ws, rws,
                 1, kEpiStore, e.ws.steer, e.md.dm.d_model, nullptr);
+}
+
+// ===========================================================================
+// MLP steering (eq. (2)): taps of the verifier's residual stream, g = LayerNorm(W_hml [h; m; l]),
+// per-layer up-projection biases W_s g.
+// ===========================================================================
+// Residual rows after `layer` into every tap slot taken there (per-operation verify pass).
+__global__ void k_tap_copy(const float* x, int d, int rows, int maxm, float* taps, int m0, int m1, int m2) {
+    const int r = blockIdx.x;
+    const int mask = m0 | (m1 << 1) | (m2 << 2);
+    for (int sl = 0; sl < 3; ++sl) {
+        if (!((mask >> sl) & 1)) continue;
+        float* dst = taps + ((size_t)sl * maxm + r) * d;
+        for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = x[(size_t)r * d + i];
+    }
+}
+
+void launch_tap_copy(hipStream_t s, Engine& e, int layer, int rows) {
+    const int* tl = e.tap_layer;
+    if (tl[0] != layer && tl[1] != layer && tl[2] != layer) return;
+    prof_begin(&e, kProfOther, 0.0);
+    k_tap_copy<<<rows, 256, 0, s>>>(e.mv.x, e.mv.dm.d_model, rows, e.maxm, e.ws.taps, tl[0] == layer,
+                                    tl[1] == layer, tl[2] == layer);
+    prof_end(&e);
+}
+
+// Prefill: the tap rows at position len-2 of each sequence go straight to its [h; m; l] row.
+__global__ void k_prefill_tap(const int32_t* row_pos, const int32_t* row_seq, const int32_t* prompt_len,
+                              int max_prompt, const float* x, int d, float* tapsel, int batch, int m0, int m1,
+                              int m2) {
+    const int r = blockIdx.x;
+    const int pos = row_pos[r];
+    if (pos < 0) return;
+    const int b = row_seq[r];
+    if (b >= batch || pos != min(prompt_len[b], max_prompt) - 2) return;
+    const int mask = m0 | (m1 << 1) | (m2 << 2);
+    for (int sl = 0; sl < 3; ++sl) {
+        if (!((mask >> sl) & 1)) continue;
+        float* dst = tapsel + ((size_t)b * 3 + sl) * d;
+        for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = x[(size_t)r * d + i];
+    }
+}
+
+void launch_prefill_tap(hipStream_t s, Engine& e, int layer, int rows, const int32_t* prompt_len, int max_prompt) {
+    const int* tl = e.tap_layer;
+    if (tl[0] != layer && tl[1] != layer && tl[2] != layer) return;
+    k_prefill_tap<<<rows, 256, 0, s>>>(e.ws.row_pos, e.ws.row_seq, prompt_len, max_prompt, e.mv.x,
+                                       e.mv.dm.d_model, e.ws.tapsel, e.batch, tl[0] == layer, tl[1] == layer,
+                                       tl[2] == layer);
+}
+
+// [h; m; l] of row in_map[b] (identity when null) of three [rows][d] sources.
+__global__ void k_tap_gather(const float* s0, const float* s1, const float* s2, const int32_t* in_map, int d,
+                             float* tapsel) {
+    const int b = blockIdx.x;
+    const int r = in_map ? in_map[b] : b;
+    const float* src[3] = {s0, s1, s2};
+    for (int sl = 0; sl < 3; ++sl)
+        for (int i = threadIdx.x; i < d; i += blockDim.x)
+            tapsel[((size_t)b * 3 + sl) * d + i] = src[sl][(size_t)r * d + i];
+}
+
+// In-place LayerNorm of rows [rows][d]: (g - mean) / sqrt(var + eps) * gain + shift, population
+// variance, both moments from the row held in LDS (d <= 16384).
+template <typename TW>
+__global__ __launch_bounds__(256) void k_layernorm_rows(float* X, int d, const TW* gain, const TW* shift, float eps) {
+    __shared__ float red[4];
+    __shared__ float stat[2];
+    float* x = X + (size_t)blockIdx.x * d;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x / 64;
+    float sum = 0.0f;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) sum += x[i];
+    sum = wave_sum(sum);
+    if (lane == 0) red[wave] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) stat[0] = (red[0] + red[1] + red[2] + red[3]) / (float)d;
+    __syncthreads();
+    const float mean = stat[0];
+    float sq = 0.0f;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+        const float c = x[i] - mean;
+        sq += c * c;
+    }
+    sq = wave_sum(sq);
+    if (lane == 0) red[wave] = sq;
+    __syncthreads();
+    if (threadIdx.x == 0) stat[1] = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+    __syncthreads();
+    const float inv = stat[1];
+    for (int i = threadIdx.x; i < d; i += blockDim.x)
+        x[i] = (x[i] - mean) * inv * load_scalar<TW>(gain, i) + load_scalar<TW>(shift, i);
+}
+
+// Y[rows][N] = X[rows][K] . W^T: the MFMA projection kernel when it has a plan for the shape,
+// else the vector kernel (small K, or f32 weights).
+static void project_rows(Engine& e, const float* X, int rows, int K, const void* W, int N, float* Y) {
+    if (e.bf16 && ws_plan(rows < 16 ? rows : 16, N, K, kEpiStore).S) {
+        WsCall c = ws_base(e, e.mv);
+        c.X = X; c.M = rows; c.K = K;
+        c.W[0] = W; c.seg_rows[0] = N; c.nseg = 1; c.mode = kEpiStore;
+        c.Y = Y; c.ldy = N;
+        launch_wsgemv(&e, e.stream, c);
+        return;
+    }
+    const void* ws[1] = {W};
+    int rws[1] = {N};
+    launch_gemv(&e, e.stream, e.bf16, X, nullptr, rows, K, nullptr, 0.f, ws, rws, 1, kEpiStore, Y, N, nullptr);
+}
+
+void launch_mlp_steer(Engine& e, const float* const* src, const int32_t* in_map, int rows) {
+    const int dV = e.mv.dm.d_model;
+    const int nb = e.md.dm.n_layers * e.md.dm.d_ff;
+    if (src) {  // else tapsel already holds the rows (prefill)
+        prof_begin(&e, kProfOther, 0.0);
+        k_tap_gather<<<rows, 256, 0, e.stream>>>(src[0], src[1], src[2], in_map, dV, e.ws.tapsel);
+        prof_end(&e);
+    }
+    project_rows(e, e.ws.tapsel, rows, 3 * dV, e.w_hml, dV, e.ws.gsteer);
+    prof_begin(&e, kProfOther, 0.0);
+    if (e.bf16)
+        k_layernorm_rows<uint16_t><<<rows, 256, 0, e.stream>>>(e.ws.gsteer, dV, (const uint16_t*)e.ln_gain,
+                                                               (const uint16_t*)e.ln_bias, e.ln_eps);
+    else
+        k_layernorm_rows<float><<<rows, 256, 0, e.stream>>>(e.ws.gsteer, dV, (const float*)e.ln_gain,
+                                                            (const float*)e.ln_bias, e.ln_eps);
+    prof_end(&e);
+    project_rows(e, e.ws.gsteer, rows, dV, e.w_steer, nb, e.ws.ubias);
 }
 
 // ===========================================================================
@@ -847,15 +986,19 @@ void launch_prefill_capture(hipStream_t s, Engine& e, int rows, const int32_t* p
 
 __global__ void k_prefill_finish(int batch, const int32_t* prompt_tok, const int32_t* prompt_len, int max_prompt,
                                  int32_t* hist, int cap, int32_t* t, int32_t* len_v, int32_t* len_d,
-                                 int32_t* produced, int32_t* done, float* steer, int dD, int vocab) {
+                                 int32_t* produced, int32_t* done, float* steer, int dD, int vocab, float* ubias,
+                                 int nb) {
     int b = blockIdx.x;
     int p = min(max(prompt_len[b], 1), max_prompt);
     for (int i = threadIdx.x; i < p; i += blockDim.x) {
         int tok = prompt_tok[(size_t)b * max_prompt + i];
         hist[(size_t)b * cap + i] = tok < 0 ? 0 : (tok >= vocab ? vocab - 1 : tok);
     }
-    if (p < 2)
+    if (p < 2) {
         for (int i = threadIdx.x; i < dD; i += blockDim.x) steer[(size_t)b * dD + i] = 0.0f;
+        if (ubias)
+            for (int i = threadIdx.x; i < nb; i += blockDim.x) ubias[(size_t)b * nb + i] = 0.0f;
+    }
     if (threadIdx.x == 0) {
         t[b] = p;
         len_v[b] = p - 1;
@@ -869,7 +1012,8 @@ void launch_prefill_finish(hipStream_t s, Engine& e, int batch, const int32_t* p
                            int max_prompt) {
     k_prefill_finish<<<batch, 256, 0, s>>>(batch, prompt_tok, prompt_len, max_prompt, e.ws.hist, e.cap, e.ws.t,
                                            e.ws.len_v, e.ws.len_d, e.ws.produced, e.ws.done, e.ws.steer,
-                                           e.md.dm.d_model, e.mv.dm.vocab);
+                                           e.md.dm.d_model, e.mv.dm.vocab, e.mlp ? e.ws.ubias : nullptr,
+                                           e.md.dm.n_layers * e.md.dm.d_ff);
 }
 
 // Final-norm rows (debug read of the verifier's hidden states).

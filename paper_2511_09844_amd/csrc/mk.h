@@ -34,6 +34,7 @@ struct MkPhase {
     int32_t defer;           // ATTN: leave the span partials unmerged (the next projection merges them)
     int32_t kvsig;           // Q|K|V: count every finished tile in on its KV head's counter
     int32_t kvwait;          // ATTN: wait for the unit's KV head counter instead of a grid barrier
+    int32_t ub_ld;           // SwiGLU: row stride of ubias (per sequence)
     const uint16_t* W[3];
     const float* X;          // activation rows [M][K] (kMkXBuf), or attention partials (kMkXAttn)
     const uint16_t* gamma;   // RMSNorm gain, or null (no norm)
@@ -46,6 +47,7 @@ struct MkPhase {
     float* qout;             // Qkv: queries [M][H*hd]; ATTN: query source
     float* aout;             // ATTN: output [M][H*hd]
     float* apart;            // ATTN: partials [M][H][nsplit][hd+4] (outputs, span max, span sum)
+    const float* ubias;      // SwiGLU: this layer's up-projection bias per sequence (MLP steering), or null
 };
 
 // Launch-wide arguments.
@@ -99,6 +101,7 @@ struct MkState {
     int off[kMkMaxLaunch], n[kMkMaxLaunch];
     double bytes[kMkMaxLaunch];  // weight bytes streamed by each launch
     bool active;
+    const float* tap_x[3]; // verifier launch: residual rows after the steering tap blocks (h, m, l)
     float* final_x;       // verifier launch: final residual rows [M][d_V]
     float* final_ss;      //   and their 16-column sums of squares
     int64_t* trace;       // [kMkMaxLaunch][kMkTracePhases] phase end times of the last profiled round

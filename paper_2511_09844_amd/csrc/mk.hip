@@ -315,6 +315,7 @@ __device__ __forceinline__ float mk_embed_at(const MkArgs& a, const MkRows& rp, 
     return v;
 }
 
+template <bool UB>
 __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, const MkRows& rp, char* smem, float* inv_rms,
                         int* flags, int* last_flag, MkBuf& bf) {
     // descriptor fields (od lives in LDS), uniform
@@ -609,11 +610,22 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                 if (valid && ec == 0) mk_stf(oss_out + (size_t)em * (oldy / 16) + tile, sq);
             }
         } else if (omode == kEpiSwiglu) {
+            // MLP steering: the sequence's bias for this layer joins the up projection (eq. (2));
+            // compiled only into the instance that runs steered drafter steps
+            float ub = 0.f;
+            if constexpr (UB) {
+                const float* oub = mk_uni(od.ubias);
+                if (oub && valid)
+                    ub = mk_ldg(oub + (size_t)rp.seq[em] * mk_uni(od.ub_ld) +
+                                (osubs == 2 ? tile * 16 + ec : tile * 8 + (ec & 7)));
+            }
             if (osubs == 2) {
-                if (valid) mk_stf(oY + (size_t)em * oldy + tile * 16 + ec, silu(v0) * v1);
+                const float up = UB ? v1 + ub : v1;
+                if (valid) mk_stf(oY + (size_t)em * oldy + tile * 16 + ec, silu(v0) * up);
             } else {
                 // column c < 8 holds gate feature 8 tile + c, column c + 8 its up row
-                const float up = __shfl_xor(v0, 8, 16);
+                const float upr = __shfl_xor(v0, 8, 16);
+                const float up = UB ? upr + ub : upr;
                 if (valid && ec < 8) mk_stf(oY + (size_t)em * oldy + tile * 8 + ec, silu(v0) * up);
             }
         } else {  // Q|K|V: rotate-half RoPE on Q and K, cache append of K and V
@@ -1087,8 +1099,10 @@ __device__ __forceinline__ void mk_attn_phase(const MkArgs& a, const MkPhase& od
 }
 
 // One kernel per head dim (64: drafter, 128: verifier), so that each holds one attention
-// instantiation: the code of a launch then stays closer to the instruction cache's size.
-template <int HD>
+// instantiation: the code of a launch then stays closer to the instruction cache's size.  UB:
+// the SwiGLU epilogue adds the MLP-steering bias (drafter steps with that steering only; the
+// other instances carry no code for it).
+template <int HD, bool UB>
 __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ MkPhase op_lds[2];
@@ -1122,7 +1136,7 @@ __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
                 const uint16_t* wp = mk_uptr(a, q, 0, lane & 15, lane >> 4, lane, st);
                 mk_issue<0, kMkPreSteps>(bf, wp, st);
             }
-            mk_gemv(a, o, rp, smem, inv_rms, flags, &last_flag, bf);
+            mk_gemv<UB>(a, o, rp, smem, inv_rms, flags, &last_flag, bf);
         } else if (op == kMkAttn) {
             mk_attn_phase<HD>(a, o, rp, smem, &last_flag, gen, spins, p);
         }
@@ -1198,7 +1212,7 @@ int mk_nsplit(int cap) { return (cap + kMkSpan - 1) / kMkSpan; }
 // Returns false when a shape is not supported.  `lds` receives the largest dynamic LDS.
 bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int rps, int j, int G, Arena& ar,
                const Workspace* ws, std::vector<MkPhase>* out, size_t* lds, int32_t* cnt, float** final_x,
-               float** final_ss, double* bytes_out = nullptr) {
+               float** final_ss, double* bytes_out = nullptr, const float** tap_x = nullptr) {
     double bytes = 0.0;
     const sd2_dims& d = m.dm;
     const int hd = d.d_model / d.n_heads;
@@ -1294,6 +1308,10 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         gu.X = xa;
         gu.Y = hbuf;
         gu.ldy = F;
+        if (!verifier && ws && c.steering == SD2_STEER_MLP) {
+            gu.ubias = ws->ubias + (size_t)l * F;
+            gu.ub_ld = L * F;
+        }
         MkPhase dn{};
         if (!gemv(kEpiAdd, dm, F, nullptr, false, 1, dn)) return false;
         dn.nseg = 1;
@@ -1311,6 +1329,13 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
             out->push_back(dn);
         }
         x_prev = xf;
+        // MLP steering taps: residual after blocks L-2, floor(L/2), 3 (from 1); each layer's
+        // residual has its own buffer, so the rows stay readable after the launch
+        if (tap_x) {
+            const int tl[3] = {L - 3, L / 2 - 1, 2};
+            for (int sl = 0; sl < 3; ++sl)
+                if (tl[sl] == l) tap_x[sl] = xf;
+        }
         if (l == L - 1) {
             if (final_x) *final_x = xf;
             if (final_ss) *final_ss = ss;
@@ -1423,16 +1448,18 @@ bool mk_build(Engine& e, int batch) {
         Arena ar{s.arena, 0};
         s.off[0] = (int)prog.size();
         if (!mk_record(c, e.mv, true, batch * (c.k + 1), c.k + 1, 0, s.G, ar, &e.ws, &prog, &lds, s.cnt, &s.final_x,
-                       &s.final_ss, &s.bytes[0]))
+                       &s.final_ss, &s.bytes[0], s.tap_x))
             return false;
         s.n[0] = (int)prog.size() - s.off[0];
     }
     if ((int)prog.size() > s.prog_cap) return false;
     s.lds = lds;
-    for (const void* fn : {(const void*)k_mk<64>, (const void*)k_mk<128>})
+    for (const void* fn : {(const void*)k_mk<64, false>, (const void*)k_mk<128, false>, (const void*)k_mk<64, true>,
+                           (const void*)k_mk<128, true>})
         if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) return false;
     int occ = 0;
-    for (const void* fn : {(const void*)k_mk<64>, (const void*)k_mk<128>})
+    for (const void* fn : {(const void*)k_mk<64, false>, (const void*)k_mk<128, false>, (const void*)k_mk<64, true>,
+                           (const void*)k_mk<128, true>})
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, kMkThreads, lds) != hipSuccess || occ < 1) return false;
     if (hipMemcpyAsync(s.prog, prog.data(), sizeof(MkPhase) * prog.size(), hipMemcpyHostToDevice, e.stream) !=
         hipSuccess)
@@ -1473,7 +1500,7 @@ hipError_t mk_launch(Engine& e, int j) {
     a.steer = e.ws.steer;
     a.embed = (const uint16_t*)m.embed;
     a.vocab = m.dm.vocab;
-    a.add_steer = ver ? 0 : 1;
+    a.add_steer = ver || e.mlp ? 0 : 1;  // MLP steering biases the up projections instead
     a.kc = m.kc;
     a.vc = m.vc;
     a.rcos = m.rope_cos;
@@ -1491,7 +1518,9 @@ hipError_t mk_launch(Engine& e, int j) {
     void* args[] = {&a};
     ProfEntry* pe = prof_slot(&e, kProfProgram, s.bytes[j]);
     if (pe) (void)hipEventRecord(pe->a, e.stream);
-    const void* fn = m.hd == 64 ? (const void*)k_mk<64> : (const void*)k_mk<128>;
+    const bool ub = !ver && e.mlp;
+    const void* fn = m.hd == 64 ? (ub ? (const void*)k_mk<64, true> : (const void*)k_mk<64, false>)
+                                : (ub ? (const void*)k_mk<128, true> : (const void*)k_mk<128, false>);
     hipError_t err = hipLaunchCooperativeKernel(fn, dim3(s.G), dim3(kMkThreads), args, s.lds, e.stream);
     if (pe) {
         (void)hipEventRecord(pe->b, e.stream);

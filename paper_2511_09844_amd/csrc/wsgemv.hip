@@ -64,6 +64,9 @@ struct WsArgs {
     const float *rcos, *rsin;
     float *qout, *kc, *vc;
     int cap, max_batch, layer;
+    // SwiGLU with MLP steering: up-projection bias of the row's sequence (row_seq), or null
+    const float* ubias;
+    int ub_ld;
 };
 
 // Weight row streamed by lane column n of a tile (segment resolution and the Q|K|V pairing
@@ -108,7 +111,11 @@ __device__ __forceinline__ void tile_epilogue(const WsArgs& a, int tile, const f
         for (int o = 8; o > 0; o >>= 1) sq += __shfl_xor(sq, o, 16);
         if (valid && ec == 0) a.ss_out[(size_t)row * a.tiles + tile] = sq;
     } else if (a.mode == kEpiSwiglu) {
-        if (valid) a.Y[(size_t)row * a.ldy + tile * 16 + ec] = silu(v[0]) * v[SUBS - 1];
+        if (valid) {
+            float up = v[SUBS - 1];
+            if (a.ubias) up += a.ubias[(size_t)a.row_seq[row] * a.ub_ld + tile * 16 + ec];
+            a.Y[(size_t)row * a.ldy + tile * 16 + ec] = silu(v[0]) * up;
+        }
     } else {
         float partner = __shfl_xor(v[0], 8, 16);
         if (!valid) return;
@@ -397,6 +404,7 @@ void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
         a.H = c.H; a.Hkv = c.Hkv; a.hd = c.hd; a.row_pos = c.row_pos; a.row_seq = c.row_seq;
         a.rcos = c.rcos; a.rsin = c.rsin; a.qout = c.qout; a.kc = c.kc; a.vc = c.vc;
         a.cap = c.cap; a.max_batch = c.max_batch; a.layer = c.layer;
+        a.ubias = c.ubias; a.ub_ld = c.ub_ld;
         int subs = c.mode == kEpiSwiglu ? 2 : 1;
         bool launched = false;
         if (p.S) {

@@ -50,21 +50,35 @@ class Stats:
 
 
 def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check_logits=True, log=print,
-               expect_path=None, separate_kernels=False):
+               expect_path=None, separate_kernels=False, mlp=None):
     """Run prefill + rounds on both sides; assert parity; return Stats.
 
     expect_path: 0 (one kernel per operation) or 1 (one persistent launch per drafter step and
-    verify pass) -- the execution path the library must have chosen; separate_kernels forces 0."""
+    verify pass) -- the execution path the library must have chosen; separate_kernels forces 0.
+    mlp: host weights of the MLP steering form (sd2_inputs.mlp_steer_weights); the per-layer
+    up-projection biases are then compared where the steering vector is otherwise."""
     if wv is None:
         wv, wd, ws = si.model_weights(wl, 0), si.model_weights(wl, 1), si.steer_weights(wl)
     tol = TOL[wl.dtype]
     toks, lens = si.prompts(wl)
     seqs = list(range(wl.batch)) if seqs is None else list(seqs)
-    o = oracle.Oracle(wl, wv, wd, ws)
+    o = oracle.Oracle(wl, wv, wd, ws, mlp=mlp)
     o.prefill(toks, lens, seqs)
     dv, dd = device_model(wl, 0, wv), device_model(wl, 1, wd)
-    ws_dev = B.to_device(ws)
-    eng = B.Engine(B.config_of(wl), dv, dd, ws_dev)
+    if mlp is None:
+        ws_dev = B.to_device(ws)
+        eng = B.Engine(B.config_of(wl), dv, dd, ws_dev)
+    else:
+        ws_dev = {key: B.to_device(mlp[key]) for key in ("w_s", "w_hml", "ln_gain", "ln_bias")}
+        ws_dev["ln_eps"] = mlp["ln_eps"]
+        eng = B.Engine(B.config_of(wl, steering=B.STEER_MLP), dv, dd, None, mlp=ws_dev)
+
+    def steer_err(b, dev):
+        # the steering state of sequence b: s (input form) or the per-layer biases (MLP form)
+        ref = o.steer_vec(b) if mlp is None else o.ubias(b)
+        return float(np.abs(dev[b] - ref).max())
+
+    dbg_steer = B.DBG_STEER if mlp is None else B.DBG_UBIAS
     old = os.environ.pop("SD2_NO_MK", None)
     if separate_kernels:
         os.environ["SD2_NO_MK"] = "1"
@@ -79,9 +93,9 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
     if expect_path is not None:
         assert path == expect_path, f"execution path {path}, expected {expect_path}"
     st = Stats()
-    s_gpu = eng.debug(B.DBG_STEER)
+    s_gpu = eng.debug(dbg_steer)
     for b in seqs:
-        err = np.abs(s_gpu[b] - o.steer_vec(b)).max()
+        err = steer_err(b, s_gpu)
         st.max_err_s = max(st.max_err_s, err)
         assert err <= tol, f"prefill steering b={b} err={err}"
     k = wl.k
@@ -105,7 +119,7 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
         if check_logits:
             lv = eng.debug(B.DBG_LOGITS_V)
             ld = eng.debug(B.DBG_LOGITS_D)
-        sg = eng.debug(B.DBG_STEER)
+        sg = eng.debug(dbg_steer)
         state = eng.state()
         for b in live:
             lg = logs[b]
@@ -123,7 +137,7 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
                 st.max_err_v = max(st.max_err_v, ev)
                 st.max_err_d = max(st.max_err_d, ed)
                 assert ev <= tol and ed <= tol, f"{where}: logits err v={ev} d={ed}"
-            es = float(np.abs(sg[b] - o.steer_vec(b)).max())
+            es = steer_err(b, sg)
             st.max_err_s = max(st.max_err_s, es)
             assert es <= tol, f"{where}: steering err {es}"
             # the library's own decisions, where the oracle's margin pins them

@@ -64,3 +64,53 @@ def test_status_strings():
     lib = B.load()
     for code in (0, -1, -2, -3, -4, -5, 7):
         assert lib.sd2_status_string(code)
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structures have the header's sizes and field offsets (gcc on the host)."""
+    prog = tmp_path / "layout.c"
+    prog.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "sd2.h"\n'
+        "int main(void) {\n"
+        '  printf("%zu %zu %zu %zu\\n", sizeof(sd2_config), offsetof(sd2_config, seed),\n'
+        "         offsetof(sd2_config, steering), offsetof(sd2_config, temperature));\n"
+        '  printf("%zu %zu %zu\\n", sizeof(sd2_mlp_steering), offsetof(sd2_mlp_steering, ln_bias),\n'
+        "         offsetof(sd2_mlp_steering, ln_eps));\n"
+        '  printf("%zu %zu\\n", sizeof(sd2_weights), sizeof(sd2_dims));\n'
+        "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    import subprocess
+    subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(prog), "-o", str(exe)])
+    got = [list(map(int, line.split())) for line in subprocess.check_output([str(exe)]).decode().splitlines()]
+    C, M = B.Config, B.MlpSteering
+    assert got[0] == [ctypes.sizeof(C), C.seed.offset, C.steering.offset, C.temperature.offset]
+    assert got[1] == [ctypes.sizeof(M), M.ln_bias.offset, M.ln_eps.offset]
+    assert got[2] == [ctypes.sizeof(B.Weights), ctypes.sizeof(B.Dims)]
+
+
+def test_mlp_steering_configs():
+    """The MLP form needs a verifier of at least 3 layers (block 3 is the low tap) and sizes its
+    extra buffers; an unknown steering form is rejected."""
+    lib = B.load()
+    for wl in si.PRESETS[:4]:
+        base = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl)))
+        mlp = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl, steering=B.STEER_MLP)))
+        dm = wl.drafter
+        assert mlp >= base + wl.batch * dm.n_layers * dm.d_ff * 4
+    c = B.config_of(si.TINY, steering=2)
+    assert lib.sd2_workspace_bytes(ctypes.byref(c)) == 0
+    c = B.config_of(si.TINY, steering=B.STEER_MLP)
+    c.verifier.n_layers = 2
+    assert lib.sd2_workspace_bytes(ctypes.byref(c)) == 0
+
+
+def test_create_mlp_rejects_bad_arguments_without_gpu():
+    lib = B.load()
+    h = B.P()
+    c = B.config_of(si.TINY, steering=B.STEER_MLP)
+    assert lib.sd2_create_mlp(ctypes.byref(c), None, None, None, None, 0, None, ctypes.byref(h)) == -1
+    # the input form's entry point refuses an MLP configuration, and the reverse
+    assert lib.sd2_create(ctypes.byref(c), None, None, None, None, 0, None, ctypes.byref(h)) == -1
+    ms = B.MlpSteering(None, None, None, None, 1e-5)
+    c0 = B.config_of(si.TINY)
+    assert lib.sd2_create_mlp(ctypes.byref(c0), None, None, ctypes.byref(ms), None, 0, None, ctypes.byref(h)) == -1
