@@ -188,6 +188,7 @@ struct WsPlan {
 };
 WsPlan ws_plan(int M, int N, int K, int mode);
 void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c);
+hipError_t wsgemv_setup();  // kernel attributes of the many-row GEMM (once per process and device)
 void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride);
 int attn_nsplit(int cap);
 size_t attn_groups(int rows, int rps, int H, int Hkv);

@@ -465,7 +465,13 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
         dst[i]->lm_head = src[i]->lm_head;
         for (int j = 0; j < dst[i]->dm.n_layers * 9; ++j) dst[i]->layer[j] = src[i]->layers[j];
     }
-    hipError_t err = hipMemsetAsync(workspace, 0, need, e->stream);
+    hipError_t err = wsgemv_setup();
+    if (err != hipSuccess) {
+        sd2_status st = hip_fail(e, err, "hipFuncSetAttribute");
+        delete e;
+        return st;
+    }
+    err = hipMemsetAsync(workspace, 0, need, e->stream);
     if (err != hipSuccess) {
         sd2_status st = hip_fail(e, err, "hipMemsetAsync");
         delete e;

@@ -332,6 +332,164 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
     }
 }
 
+// ===========================================================================
+// Many-row projections (prefill chunks, large batches): an MFMA GEMM.  A workgroup computes 64
+// activation rows (4 groups of 16) against 8 weight sub-tiles of 16 rows (two per wave), walking
+// K in steps of 256 columns: the step's weight fragments are requested first, the activation
+// slice is staged in LDS as hi/lo bf16 planes (gain applied, as in k_wsgemv), then every weight
+// fragment meets all 4 row groups.  Epilogues are k_wsgemv's, per 16-row group.
+// ===========================================================================
+constexpr int kPgRows = 64;           // activation rows per workgroup
+constexpr int kPgTW = 2;              // weight sub-tiles per wave
+constexpr int kPgKC = 256;            // K columns per step
+constexpr int kPgLdk = kPgKC + 8;     // padded LDS row stride (bf16 elements)
+constexpr size_t kPgLds = 2 * kPgRows * kPgLdk * 2;  // hi and lo planes (also holds the 32 KB of results)
+static_assert(kPgLds >= 4 * kPgTW * 4 * 256 * 4, "result staging must fit the activation planes");
+
+template <int SUBS>
+__global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ float inv_rms[kPgRows];
+    __shared__ int src_row[kPgRows];
+    constexpr int NT = 4 * kPgTW / SUBS;  // 16-row output tiles per workgroup
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n = lane & 15, q = lane >> 4;
+    // block -> (n block, m block): workgroups are dealt to the 8 XCDs in turn, so blocks b, b + 8,
+    // ... share an XCD; they take the m blocks of one n block, whose weights then come from that
+    // XCD's L2 after the first read
+    const int xcd = blockIdx.x & 7, r = blockIdx.x >> 3;
+    const int mb = r % nblk_m;
+    const int nb = xcd + 8 * (r / nblk_m);
+    const int tile0 = nb * NT;
+    if (tile0 >= a.tiles) return;  // grid padding (uniform per workgroup)
+    const int m0 = mb * kPgRows;
+    const int M = a.M;
+    if (tid < kPgRows) {
+        const int row = m0 + tid;
+        int src = -1;
+        if (row < M) src = a.in_map ? a.in_map[row] : row;
+        src_row[tid] = src;
+        inv_rms[tid] = 1.0f;
+    }
+    __syncthreads();
+    if (a.gamma) {
+        for (int m = wave; m < kPgRows; m += 4) {
+            const int src = src_row[m];
+            float sm = 0.0f;
+            if (src >= 0)
+                for (int t = lane; t < a.nss; t += 64) sm += a.ss[(size_t)src * a.nss + t];
+            sm = wave_sum(sm);
+            if (lane == 0) inv_rms[m] = rsqrtf(sm / (float)a.K + a.eps);
+        }
+    }
+    // this wave's sub-tiles: SwiGLU waves 0, 1 take gate rows and waves 2, 3 the up rows of the
+    // same features; a tile past the end is read clamped and never written
+    const int sub = SUBS == 2 ? wave >> 1 : 0;
+    const uint16_t* wrow[kPgTW];
+#pragma unroll
+    for (int j = 0; j < kPgTW; ++j) {
+        const int tile = tile0 + (SUBS == 2 ? (wave & 1) * kPgTW : wave * kPgTW) + j;
+        wrow[j] = tile_row(a, min(tile, a.tiles - 1), sub, n) + 16 * q;
+    }
+    uint16_t* xh = (uint16_t*)smem;
+    uint16_t* xl = xh + kPgRows * kPgLdk;
+    floatx4_t acc[kPgTW][4];
+#pragma unroll
+    for (int j = 0; j < kPgTW; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[j][g] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < a.K; k0 += kPgKC) {
+        u32x4_t w[kPgTW][4][2];
+#pragma unroll
+        for (int j = 0; j < kPgTW; ++j)
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) w[j][st][h] = *(const u32x4_t*)(wrow[j] + k0 + st * 64 + 8 * h);
+        // 64 rows x 256 columns of fp32 activations: 16 float4 per thread, row-major
+        float4 xv[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int idx = tid + i * 256;
+            const int m = idx >> 6, kk = (idx & 63) * 4;
+            const int src = src_row[m];
+            xv[i] = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        __syncthreads();  // the previous step's MFMAs have read the planes
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int idx = tid + i * 256;
+            const int m = idx >> 6, kk = (idx & 63) * 4;
+            float gm[4] = {1.f, 1.f, 1.f, 1.f};
+            if (a.gamma) {
+                uint2 gw = *(const uint2*)(a.gamma + k0 + kk);
+                gm[0] = bf16_lo(gw.x); gm[1] = bf16_hi(gw.x); gm[2] = bf16_lo(gw.y); gm[3] = bf16_hi(gw.y);
+            }
+            const float vv[4] = {xv[i].x * gm[0], xv[i].y * gm[1], xv[i].z * gm[2], xv[i].w * gm[3]};
+            uint16_t hi[4], lo[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                hi[e] = f32_to_bf16_rne(vv[e]);
+                lo[e] = f32_to_bf16_rne(vv[e] - bf16_to_f32(hi[e]));
+            }
+            *(uint2*)(xh + m * kPgLdk + kk) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+            *(uint2*)(xl + m * kPgLdk + kk) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int kk = st * 64 + 16 * q + 8 * h;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const bf16x8_t ah = *(const bf16x8_t*)(xh + (g * 16 + n) * kPgLdk + kk);
+                    const bf16x8_t al = *(const bf16x8_t*)(xl + (g * 16 + n) * kPgLdk + kk);
+#pragma unroll
+                    for (int j = 0; j < kPgTW; ++j) {
+                        const bf16x8_t b = __builtin_bit_cast(bf16x8_t, w[j][st][h]);
+                        acc[j][g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b, acc[j][g], 0, 0, 0);
+                        acc[j][g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b, acc[j][g], 0, 0, 0);
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();  // planes free: results go to LDS, slot (wave * TW + j, group g)
+    float* red = (float*)smem;
+#pragma unroll
+    for (int j = 0; j < kPgTW; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[((wave * kPgTW + j) * 4 + g) * 256 + (4 * q + i) * 16 + n] = acc[j][g][i];
+    __syncthreads();
+    // per output tile and row group: element (m, c) at thread 16 m + c; SwiGLU's up value of
+    // local tile lt sits 2 TW slots after its gate value
+    WsArgs ar = a;
+    for (int lt = 0; lt < NT; ++lt) {
+        const int tile = tile0 + lt;
+        if (tile >= a.tiles) break;
+        for (int g = 0; g < 4; ++g) {
+            const int row0 = m0 + g * 16;
+            if (row0 >= M) break;
+            const float sc = inv_rms[g * 16 + (tid >> 4)];
+            float v[2];
+            v[0] = red[(lt * 4 + g) * 256 + tid] * sc;
+            v[1] = SUBS == 2 ? red[((lt + 2 * kPgTW) * 4 + g) * 256 + tid] * sc : v[0];
+            ar.row0 = row0;
+            ar.M = min(16, M - row0);
+            tile_epilogue<SUBS>(ar, tile, v);
+        }
+    }
+}
+
+hipError_t wsgemv_setup() {
+    hipError_t e1 = hipFuncSetAttribute((const void*)k_pgemm<1>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kPgLds);
+    hipError_t e2 = hipFuncSetAttribute((const void*)k_pgemm<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kPgLds);
+    return e1 != hipSuccess ? e1 : e2;
+}
+
 constexpr int kLdsBudget = 160 * 1024 - 2048;
 
 static size_t lds_bytes(int rows, int KR, int NW) {
@@ -382,7 +540,46 @@ WsPlan ws_plan(int M, int N, int K, int mode) {
     return p;
 }
 
+static bool launch_pgemm(Engine* e, hipStream_t s, const WsCall& c) {
+    if (c.K % kPgKC) return false;
+    WsArgs a{};
+    a.X = c.X; a.ldx = c.K; a.in_map = c.in_map; a.M = c.M; a.row0 = 0; a.K = c.K;
+    a.gamma = (const uint16_t*)c.gamma; a.eps = c.eps; a.ss = c.ss; a.nss = c.nss;
+    int tiles = 0;
+    for (int i = 0; i < 3; ++i) {
+        a.W[i] = i < c.nseg ? (const uint16_t*)c.W[i] : nullptr;
+        a.seg_tiles[i] = i < c.nseg ? c.seg_rows[i] / 16 : 0;
+        if (c.mode != kEpiSwiglu) tiles += a.seg_tiles[i];
+    }
+    if (c.mode == kEpiSwiglu) tiles = c.seg_rows[0] / 16;
+    a.nseg = c.nseg; a.mode = c.mode; a.tiles = tiles;
+    a.Y = c.Y; a.ldy = c.ldy; a.out_map = c.out_map; a.ss_out = c.ss_out;
+    a.S = 1;
+    a.H = c.H; a.Hkv = c.Hkv; a.hd = c.hd; a.row_pos = c.row_pos; a.row_seq = c.row_seq;
+    a.rcos = c.rcos; a.rsin = c.rsin; a.qout = c.qout; a.kc = c.kc; a.vc = c.vc;
+    a.cap = c.cap; a.max_batch = c.max_batch; a.layer = c.layer;
+    a.ubias = c.ubias; a.ub_ld = c.ub_ld;
+    const int subs = c.mode == kEpiSwiglu ? 2 : 1;
+    const int nt = 4 * kPgTW / subs;
+    const int nblk_m = (c.M + kPgRows - 1) / kPgRows;
+    const int nblk_n = (tiles + nt - 1) / nt;
+    dim3 grid(8 * nblk_m * ((nblk_n + 7) / 8));
+    const double wbytes = (double)tiles * 16 * subs * c.K * 2.0;
+    ProfEntry* pe = prof_slot(e, kProfGemv, wbytes + (double)c.M * c.K * 4.0 + (double)c.M * tiles * 16 * 4.0);
+    if (subs == 2) {
+        if (pe) hipExtLaunchKernelGGL((k_pgemm<2>), grid, dim3(256), kPgLds, s, pe->a, pe->b, 0, a, nblk_m);
+        else k_pgemm<2><<<grid, 256, kPgLds, s>>>(a, nblk_m);
+    } else {
+        if (pe) hipExtLaunchKernelGGL((k_pgemm<1>), grid, dim3(256), kPgLds, s, pe->a, pe->b, 0, a, nblk_m);
+        else k_pgemm<1><<<grid, 256, kPgLds, s>>>(a, nblk_m);
+    }
+    if (pe) prof_commit(e);
+    return true;
+}
+
 void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
+    // more than one 16-row group: the GEMM (weights read once per 64 rows, not per 16)
+    if (c.M > 16 && launch_pgemm(e, s, c)) return;
     for (int r0 = 0; r0 < c.M; r0 += 16) {
         int M = c.M - r0 < 16 ? c.M - r0 : 16;
         WsArgs a{};
