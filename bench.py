@@ -269,18 +269,21 @@ def main():
         tp = time.time()
         eng.prefill(t_tok, t_len, wl.max_prompt)
         torch.cuda.synchronize()
-        log(f"prefill done in {time.time() - tp:.2f}s")
+        prefill_s = time.time() - tp
+        log(f"prefill done in {prefill_s:.2f}s")
         for _ in range(args.warmup):
             eng.round()
         torch.cuda.synchronize()
         st0 = eng.state()
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record(stream)
-        for _ in range(args.steps):
+        # one event between consecutive rounds: the whole span gives the mean, the gaps the spread
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        evs[0].record(stream)
+        for i in range(args.steps):
             eng.round()
-        ev1.record(stream)
+            evs[i + 1].record(stream)
         torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1)
+        ms = evs[0].elapsed_time(evs[-1])
+        per_round = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
         st1 = eng.state()
         log(f"timed {args.steps} rounds: {ms:.2f} ms")
         # kernel-level timing: HIP events around every launch of the same rounds, recorded into the graph
@@ -366,6 +369,9 @@ def main():
                                f"{wl.verifier.n_kv_heads} F{wl.verifier.d_ff} V{wl.verifier.vocab}",
                    "drafter": f"L{wl.drafter.n_layers} d{wl.drafter.d_model} H{wl.drafter.n_heads}/"
                               f"{wl.drafter.n_kv_heads} F{wl.drafter.d_ff}"},
+        "round_ms_p50": per_round[len(per_round) // 2],
+        "round_ms_p90": per_round[min(len(per_round) - 1, (9 * len(per_round)) // 10)],
+        "prefill_s": prefill_s,
         "block_efficiency": tau,
         "round_bytes": bytes_round,
         "round_hbm_frac": bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS,

@@ -25,9 +25,10 @@ MLP_SMALL = Workload(
     dtype="bf16", k=3, batch=2, prompt=(1, 9), new_tokens=16, temperature=1.0, seed=21)
 
 
-def _run(wl, hml="normal", ln="normal", zero_ws=False, **kw):
+def _run(wl, hml="normal", ln="normal", zero_ws=False, mlp=None, **kw):
     from gpu_harness import parity_run
-    mlp = si.mlp_steer_weights(wl, hml=hml, ln=ln)
+    if mlp is None:
+        mlp = si.mlp_steer_weights(wl, hml=hml, ln=ln)
     if zero_ws:
         mlp["w_s"] = np.zeros_like(mlp["w_s"])
     st = parity_run(wl, mlp=mlp, **kw)
@@ -66,3 +67,20 @@ def test_mlp_steering_f32():
 def test_mlp_steering_zero_ws_persistent():
     """W_s = 0 (the paper's initialisation): every bias is zero and the drafter is unsteered."""
     _run(MLP_MK, zero_ws=True, expect_path=1)
+
+
+@pytest.fixture(scope="module")
+def host_8b_mlp():
+    """Host weights of the 8B-shaped verifier / 1B-shaped drafter and of the MLP steering
+    (W_hml 4096 x 12288, W_s 16 * 8192 x 4096), generated once."""
+    wl = si.LLAMA8B
+    return si.model_weights(wl, 0), si.model_weights(wl, 1), si.mlp_steer_weights(wl)
+
+
+def test_mlp_steering_8b_shapes_short_prompt(host_8b_mlp):
+    """The shapes bench.py --steering mlp times (taps after verifier blocks 30, 16 and 3; a bias
+    of 8192 features in each of the 16 drafter layers) on the persistent launches, T=1, k=5;
+    a 16-token prompt keeps the float64 oracle within seconds."""
+    wl = si.LLAMA8B.with_(prompt=(16, 16), new_tokens=10)
+    wv, wd, mlp = host_8b_mlp
+    _run(wl, wv=wv, wd=wd, mlp=mlp, expect_path=1)
