@@ -68,7 +68,7 @@ def _load():
         lib.oracle_forward.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P]
         lib.oracle_steer.argtypes = [P, P, P]
         lib.oracle_get_ubias.argtypes = [P, ctypes.c_int, P]
-        lib.oracle_forward_mlp.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P, P]
+        lib.oracle_forward_mlp.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P]
         lib.oracle_mlp_steer.argtypes = [P, P, P]
         lib.oracle_philox.argtypes = [P, u32, u32, P]
         lib.oracle_uniform.argtypes = [u32]
@@ -142,7 +142,8 @@ class Oracle:
     ``ws`` is W_s [d_D][d_V]; arrays must stay alive (they are referenced).
     ``mlp`` selects the MLP steering of eq. (2) instead: a dict as returned by
     ``sd2_inputs.mlp_steer_weights`` (w_s [L_D*F_D][d_V], w_hml [d_V][3 d_V],
-    ln_gain, ln_bias, ln_eps); ``ws`` is then ignored.
+    ln_gain, ln_bias, ln_eps; form 2, the bias after every MLP: w_s [d_D][d_V]);
+    ``ws`` is then ignored.
     """
 
     def __init__(self, wl, wv, wd, ws, max_batch=None, cap=None, temperature=None, k=None, max_new=None,
@@ -167,7 +168,7 @@ class Oracle:
             self._ws = mlp["w_s"]
             for key in ("w_s", "w_hml", "ln_gain", "ln_bias"):
                 assert mlp[key].flags["C_CONTIGUOUS"]
-            form = 1
+            form = int(mlp.get("form", 1))
             extra = (mlp["w_hml"].ctypes.data, mlp["ln_gain"].ctypes.data, mlp["ln_bias"].ctypes.data,
                      float(mlp["ln_eps"]))
         self.h = lib.oracle_create(self._dv.ctypes.data, self._rv.ctypes.data, self._dd.ctypes.data,
@@ -259,16 +260,20 @@ class Oracle:
         self.lib.oracle_steer(self.h, h.ctypes.data, s.ctypes.data)
         return s
 
-    def ubias(self, b):
-        """MLP steering: the up-projection biases [L_D][F_D] of sequence b for its next round."""
+    def _bias_shape(self):
         dm = self.wl.drafter
-        out = np.zeros((dm.n_layers, dm.d_ff), dtype=np.float64)
+        return (dm.n_layers, dm.d_ff) if int(self.mlp.get("form", 1)) == 1 else (dm.d_model,)
+
+    def ubias(self, b):
+        """MLP steering: the biases of sequence b for its next round: per-layer up-projection
+        biases [L_D][F_D] (form 1) or the bias after every MLP [d_D] (form 2)."""
+        out = np.zeros(self._bias_shape(), dtype=np.float64)
         self.lib.oracle_get_ubias(self.h, b, out.ctypes.data)
         return out
 
-    def forward_mlp(self, which, toks, ubias=None, taps=False):
-        """Whole-sequence forward with optional up-projection biases [L][F] on every row; returns
-        (hF [n][d], logits [n][V], taps [n][3][d] or None) in float64."""
+    def forward_mlp(self, which, toks, ubias=None, taps=False, obias=None):
+        """Whole-sequence forward with optional up-projection biases [L][F] and a bias after every
+        MLP [d] on every row; returns (hF [n][d], logits [n][V], taps [n][3][d] or None) in float64."""
         dm = self.wl.verifier if which == 0 else self.wl.drafter
         toks = np.ascontiguousarray(toks, dtype=np.int32)
         n = len(toks)
@@ -280,14 +285,18 @@ class Oracle:
             ubias = np.ascontiguousarray(ubias, dtype=np.float64)
             assert ubias.shape == (dm.n_layers, dm.d_ff)
             ub = ubias.ctypes.data
-        self.lib.oracle_forward_mlp(self.h, which, toks.ctypes.data, n, ub, tp.ctypes.data if taps else None,
+        ob = None
+        if obias is not None:
+            obias = np.ascontiguousarray(obias, dtype=np.float64)
+            assert obias.shape == (dm.d_model,)
+            ob = obias.ctypes.data
+        self.lib.oracle_forward_mlp(self.h, which, toks.ctypes.data, n, ub, ob, tp.ctypes.data if taps else None,
                                     hF.ctypes.data, lg.ctypes.data)
         return hF, lg, tp
 
     def mlp_steer(self, z):
-        """ub = W_s LayerNorm(W_hml z) for z = [h; m; l] (3 d_V); returns [L_D][F_D]."""
-        dm = self.wl.drafter
+        """ub = W_s LayerNorm(W_hml z) for z = [h; m; l] (3 d_V); returns [L_D][F_D] (form 2: [d_D])."""
         z = np.ascontiguousarray(z, dtype=np.float64).reshape(-1)
-        ub = np.zeros((dm.n_layers, dm.d_ff), dtype=np.float64)
+        ub = np.zeros(self._bias_shape(), dtype=np.float64)
         self.lib.oracle_mlp_steer(self.h, z.ctypes.data, ub.ctypes.data)
         return ub

@@ -44,6 +44,9 @@
  *     W_s), added to the up projection before the gating product:
  *     W_d((W_u a + b_l) * SiLU(W_g a)).  The bias is computed once per round
  *     and used for every drafter token processed in that round.
+ *   - the ablation "Inv. bias after MLP" (Sec. "Ablation", the simplest of the
+ *     three steering mechanisms compared there): the same g, and one bias
+ *     W_s g of d_model values added to the output of every drafter MLP.
  *   - greedy regime (T = 0): argmax drafts, accept iff the draft equals the
  *     verifier's argmax, final token = verifier argmax (Sec. "Decoding
  *     Parameters").
@@ -191,13 +194,15 @@ static void tap_layers(int L, int out[3]) {
  * whose cache holds positions 0..pos0-1.  `add` (d doubles, may be NULL) is
  * added to every input embedding (the steering injection).  `ubias` (NULL for
  * none) holds one bias of d_ff values per layer, added to the up projection
- * before the gating product (eq. (2)).  `taps` (NULL for none) receives, per
+ * before the gating product (eq. (2)); `obias` (d values, NULL for none) is
+ * added to the output of every layer's MLP.  `taps` (NULL for none) receives, per
  * row, the residual stream after the three tap blocks: taps[m][3][d].  Writes
  * the final-norm hidden state of every row to hF[m][d] and, when
  * logits != NULL, the logits of every row to logits[m][vocab].
  */
 static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32_t* toks,
-                          const double* add, const double* ubias, double* taps, double* hF, double* logits) {
+                          const double* add, const double* ubias, const double* obias, double* taps, double* hF,
+                          double* logits) {
     const odims* dm = &M->dm;
     int d = dm->d_model, H = dm->n_heads, Hkv = dm->n_kv_heads, F = dm->d_ff;
     int hd = d / H, group = H / Hkv;
@@ -271,7 +276,7 @@ static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32
             gate[i] = silu(gate[i]) * u;
         }
         matmul_rows(M->bf16, Wl[W_DOWN], d, F, gate, m, proj);
-        for (size_t i = 0; i < (size_t)m * d; ++i) x[i] += proj[i];
+        for (size_t i = 0; i < (size_t)m * d; ++i) x[i] += proj[i] + (obias ? obias[i % d] : 0.0);
         if (taps) {
             int tl[3];
             tap_layers(dm->n_layers, tl);
@@ -415,10 +420,11 @@ void oracle_accept_final(int k, int V, float T, uint64_t seed, int t, int b, con
 typedef struct {
     omodel V, D;
     const void* w_s;           /* form 0: [d_D][d_V]; form 1: [L_D*F_D][d_V]; storage type of the models */
-    int form;                  /* 0: input-embedding steering; 1: MLP steering (eq. (2)) */
+    int form;                  /* 0: input-embedding steering; 1: MLP steering (eq. (2)); 2: bias after the MLP */
     const void *w_hml, *ln_gain, *ln_bias;   /* form 1: W_hml [d_V][3 d_V], LayerNorm gain and shift [d_V] */
     double ln_eps;
-    double* ub;                /* form 1: [max_batch][L_D*F_D] up-projection biases of the current round */
+    double* ub;                /* form 1: [max_batch][L_D*F_D] up-projection biases; form 2: [max_batch][d_D] */
+    int nb;                    /* bias values per sequence */
     int k, max_batch, cap, max_new;
     float temperature;
     uint64_t seed;
@@ -446,7 +452,7 @@ ostate* oracle_create(const int32_t* dims_v, const double* rope_eps_v, const int
                       uint64_t seed, int form, const void* w_hml, const void* ln_gain, const void* ln_bias,
                       double ln_eps) {
     /* MLP steering taps decoder block 3: the verifier needs at least three layers */
-    if (form != 0 && (form != 1 || dims_v[0] < 3 || !w_hml || !ln_gain || !ln_bias)) return NULL;
+    if (form != 0 && ((form != 1 && form != 2) || dims_v[0] < 3 || !w_hml || !ln_gain || !ln_bias)) return NULL;
     ostate* st = calloc(1, sizeof(ostate));
     omodel* ms[2] = {&st->V, &st->D};
     const int32_t* dims[2] = {dims_v, dims_d};
@@ -467,8 +473,8 @@ ostate* oracle_create(const int32_t* dims_v, const double* rope_eps_v, const int
     st->w_s = w_s;
     st->form = form;
     st->w_hml = w_hml; st->ln_gain = ln_gain; st->ln_bias = ln_bias; st->ln_eps = ln_eps;
-    if (form == 1)
-        st->ub = calloc((size_t)max_batch * st->D.dm.n_layers * st->D.dm.d_ff, sizeof(double));
+    st->nb = form == 1 ? st->D.dm.n_layers * st->D.dm.d_ff : (form == 2 ? st->D.dm.d_model : 0);
+    if (form != 0) st->ub = calloc((size_t)max_batch * st->nb, sizeof(double));
     st->k = k; st->max_batch = max_batch; st->cap = cap; st->max_new = max_new;
     st->temperature = temperature; st->seed = seed;
     st->hist = calloc((size_t)max_batch * cap, sizeof(int32_t));
@@ -501,11 +507,12 @@ static void steer(const ostate* st, const double* h, double* s) {
     matmul_rows(st->V.bf16, st->w_s, st->D.dm.d_model, st->V.dm.d_model, h, 1, s);
 }
 
-/* MLP steering (eq. (2)): g = LayerNorm(W_hml [h; m; l]), then the per-layer
- * up-projection biases ub = W_s g ([L_D*F_D]).  z holds [h; m; l] (3 d_V). */
+/* MLP steering (eq. (2)): g = LayerNorm(W_hml [h; m; l]), then the biases
+ * ub = W_s g: per-layer up-projection biases [L_D*F_D] (form 1) or the one
+ * bias after every MLP [d_D] (form 2).  z holds [h; m; l] (3 d_V). */
 static void mlp_steer(const ostate* st, const double* z, double* ub) {
     int dV = st->V.dm.d_model;
-    int nb = st->D.dm.n_layers * st->D.dm.d_ff;
+    int nb = st->nb;
     double* g = malloc((size_t)dV * sizeof(double));
     matmul_rows(st->V.bf16, st->w_hml, dV, 3 * dV, z, 1, g);
     double mean = 0.0;
@@ -538,21 +545,21 @@ int oracle_prefill_one(ostate* st, int b, const int32_t* prompt, int p) {
     memcpy(st->hist + (size_t)b * st->cap, prompt, (size_t)p * sizeof(int32_t));
     double* s = st->s + (size_t)b * dD;
     for (int i = 0; i < dD; ++i) s[i] = 0.0;
-    size_t nb = (size_t)st->D.dm.n_layers * st->D.dm.d_ff;
-    double* ub = st->form == 1 ? st->ub + (size_t)b * nb : NULL;
+    size_t nb = (size_t)st->nb;
+    double* ub = st->form != 0 ? st->ub + (size_t)b * nb : NULL;
     if (ub)
         for (size_t i = 0; i < nb; ++i) ub[i] = 0.0;
     if (p >= 2) {
         double* hF = malloc((size_t)(p - 1) * dV * sizeof(double));
         double* taps = ub ? malloc((size_t)(p - 1) * 3 * dV * sizeof(double)) : NULL;
-        forward_block(&st->V, &st->kv_v[b], 0, p - 1, prompt, NULL, NULL, taps, hF, NULL);
+        forward_block(&st->V, &st->kv_v[b], 0, p - 1, prompt, NULL, NULL, NULL, taps, hF, NULL);
         if (ub) mlp_steer(st, taps + (size_t)(p - 2) * 3 * dV, ub);
         else steer(st, hF + (size_t)(p - 2) * dV, s);
         free(hF);
         free(taps);
         /* the drafter processes the prompt without steering */
         double* hD = malloc((size_t)(p - 1) * dD * sizeof(double));
-        forward_block(&st->D, &st->kv_d[b], 0, p - 1, prompt, NULL, NULL, NULL, hD, NULL);
+        forward_block(&st->D, &st->kv_d[b], 0, p - 1, prompt, NULL, NULL, NULL, NULL, hD, NULL);
         free(hD);
     }
     st->t[b] = p;
@@ -581,7 +588,7 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
     int32_t* hist = st->hist + (size_t)b * st->cap;
     int t = st->t[b];
     double* s = st->s + (size_t)b * dD;
-    double* ub = st->form == 1 ? st->ub + (size_t)b * st->D.dm.n_layers * st->D.dm.d_ff : NULL;
+    double* ub = st->form != 0 ? st->ub + (size_t)b * st->nb : NULL;
     lg->active = 1;
     lg->t_start = t;
 
@@ -604,7 +611,8 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
             m = 1;
             in = &drafts[j - 2];
         }
-        forward_block(&st->D, &st->kv_d[b], pos0, m, in, ub ? NULL : s, ub, NULL, hD, dl);
+        forward_block(&st->D, &st->kv_d[b], pos0, m, in, ub ? NULL : s, st->form == 1 ? ub : NULL,
+                      st->form == 2 ? ub : NULL, NULL, hD, dl);
         float* q = qlog + (size_t)(j - 1) * V;
         for (int v = 0; v < V; ++v) q[v] = (float)dl[(size_t)(m - 1) * V + v];
         float margin;
@@ -620,7 +628,7 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
     double* hF = malloc((size_t)(k + 1) * dV * sizeof(double));
     double* vl = malloc((size_t)(k + 1) * V * sizeof(double));
     double* taps = ub ? malloc((size_t)(k + 1) * 3 * dV * sizeof(double)) : NULL;
-    forward_block(&st->V, &st->kv_v[b], t - 1, k + 1, blk, NULL, NULL, taps, hF, vl);
+    forward_block(&st->V, &st->kv_v[b], t - 1, k + 1, blk, NULL, NULL, NULL, taps, hF, vl);
     for (size_t i = 0; i < (size_t)(k + 1) * V; ++i) plog[i] = (float)vl[i];
 
     /* ---- accept / reject, final token ---- */
@@ -667,10 +675,9 @@ void oracle_set_steer(ostate* st, int b, const double* in) {
     memcpy(st->s + (size_t)b * st->D.dm.d_model, in, (size_t)st->D.dm.d_model * sizeof(double));
 }
 
-/* Form 1: the up-projection biases [L_D*F_D] of sequence b for its next round. */
+/* Forms 1 and 2: the biases of sequence b for its next round ([L_D*F_D] or [d_D]). */
 void oracle_get_ubias(const ostate* st, int b, double* out) {
-    size_t nb = (size_t)st->D.dm.n_layers * st->D.dm.d_ff;
-    memcpy(out, st->ub + (size_t)b * nb, nb * sizeof(double));
+    memcpy(out, st->ub + (size_t)b * st->nb, (size_t)st->nb * sizeof(double));
 }
 
 void oracle_get_hist(const ostate* st, int b, int32_t* out, int n) {
@@ -692,11 +699,11 @@ void oracle_forward(const ostate* st, int which, const int32_t* toks, int n, con
     const omodel* M = which == 0 ? &st->V : &st->D;
     okv kv = kv_alloc(&M->dm, n);
     if (!add) {
-        forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, hF, logits);
+        forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, NULL, hF, logits);
     } else {
         int d = M->dm.d_model;
         for (int i = 0; i < n; ++i)
-            forward_block(M, &kv, i, 1, toks + i, add + (size_t)i * d, NULL, NULL, hF + (size_t)i * d,
+            forward_block(M, &kv, i, 1, toks + i, add + (size_t)i * d, NULL, NULL, NULL, hF + (size_t)i * d,
                           logits ? logits + (size_t)i * M->dm.vocab : NULL);
     }
     free(kv.k);
@@ -708,18 +715,18 @@ void oracle_steer(const ostate* st, const double* h, double* s) { steer(st, h, s
 
 /*
  * Whole-sequence forward with the MLP-steering pieces exposed: optional
- * per-layer up-projection biases ubias[L][d_ff] (NULL for none) applied to
- * every row, and the three steering taps of every row, taps[n][3][d] (NULL for
- * none).  Outputs as oracle_forward.
+ * per-layer up-projection biases ubias[L][d_ff] and a bias after every MLP
+ * obias[d] (NULL for none) applied to every row, and the three steering taps
+ * of every row, taps[n][3][d] (NULL for none).  Outputs as oracle_forward.
  */
-void oracle_forward_mlp(const ostate* st, int which, const int32_t* toks, int n, const double* ubias, double* taps,
-                        double* hF, double* logits) {
+void oracle_forward_mlp(const ostate* st, int which, const int32_t* toks, int n, const double* ubias,
+                        const double* obias, double* taps, double* hF, double* logits) {
     const omodel* M = which == 0 ? &st->V : &st->D;
     okv kv = kv_alloc(&M->dm, n);
-    forward_block(M, &kv, 0, n, toks, NULL, ubias, taps, hF, logits);
+    forward_block(M, &kv, 0, n, toks, NULL, ubias, obias, taps, hF, logits);
     free(kv.k);
     free(kv.v);
 }
 
-/* MLP steering on its own: ub = W_s LayerNorm(W_hml z), z = [h; m; l]. */
+/* MLP steering on its own: ub = W_s LayerNorm(W_hml z), z = [h; m; l] (form 1 or 2 sizes). */
 void oracle_mlp_steer(const ostate* st, const double* z, double* ub) { mlp_steer(st, z, ub); }

@@ -130,13 +130,16 @@ def steer_weights(wl: Workload) -> np.ndarray:
     return normal((wl.drafter.d_model, wl.verifier.d_model), wl.dtype, wl.seed, tensor_id(2, 0, "w_s"))
 
 
-def mlp_steer_weights(wl: Workload, hml: str = "normal", ln: str = "normal", ln_eps: float = 1e-5) -> dict:
-    """Weights of the MLP steering form: W_s [L_D*F_D][d_V] (one d_ff block per drafter layer),
+def mlp_steer_weights(wl: Workload, hml: str = "normal", ln: str = "normal", ln_eps: float = 1e-5,
+                      form: int = 1) -> dict:
+    """Weights of the MLP steering forms: W_s [L_D*F_D][d_V] (form 1: one d_ff block per drafter
+    layer) or [d_D][d_V] (form 2: one bias after every MLP),
     W_hml [d_V][3 d_V] ("normal" draws, or "identity" for [I I I], which maps [h; m; l] to
     h + m + l), LayerNorm gain and shift [d_V] ("normal": 1 + N(0, 0.02) and N(0, 0.02); "unit":
     ones and zeros)."""
     dV, dD = wl.verifier.d_model, wl.drafter
-    w_s = normal((dD.n_layers * dD.d_ff, dV), wl.dtype, wl.seed, (3 << 20) | 1)
+    rows = dD.n_layers * dD.d_ff if form == 1 else dD.d_model
+    w_s = normal((rows, dV), wl.dtype, wl.seed, (3 << 20) | (1 if form == 1 else 5))
     if hml == "identity":
         eye = np.eye(dV, dtype=np.float32)
         w = np.concatenate([eye, eye, eye], axis=1)
@@ -152,7 +155,8 @@ def mlp_steer_weights(wl: Workload, hml: str = "normal", ln: str = "normal", ln_
             if wl.dtype == "bf16" else g32
         shift = normal((dV,), wl.dtype, wl.seed, (3 << 20) | 4)
     return {"w_s": np.ascontiguousarray(w_s), "w_hml": np.ascontiguousarray(w_hml),
-            "ln_gain": np.ascontiguousarray(gain), "ln_bias": np.ascontiguousarray(shift), "ln_eps": ln_eps}
+            "ln_gain": np.ascontiguousarray(gain), "ln_bias": np.ascontiguousarray(shift), "ln_eps": ln_eps,
+            "form": form}
 
 
 def prompt_lens(wl: Workload) -> np.ndarray:

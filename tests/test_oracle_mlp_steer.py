@@ -11,7 +11,9 @@ What the paper fixes and these tests check:
     keep the bias of the stage that processed them (Sec. "Drafting");
   - W_s = 0 (the paper's initialisation) leaves the drafter unchanged, and
     W_hml = [I I I] maps the three activations to their sum (initialisation);
-  - greedy speculative decoding still reproduces the verifier's greedy decode.
+  - greedy speculative decoding still reproduces the verifier's greedy decode;
+  - the ablation "Inv. bias after MLP" (Sec. "Ablation"): the same g, and one bias
+    W_s g added to the output of every drafter MLP.
 Each check compares with the independent PyTorch float64 reference
 (``torch_ref``: library LayerNorm, attention and SiLU) or with an invariant.
 """
@@ -29,9 +31,9 @@ MLP8 = Workload(
     dtype="bf16", k=3, batch=2, prompt=(5, 9), new_tokens=16, temperature=1.0, seed=21)
 
 
-def _oracle(wl, hml="normal", ln="normal", zero_ws=False, **kw):
+def _oracle(wl, hml="normal", ln="normal", zero_ws=False, form=1, **kw):
     wv, wd = si.model_weights(wl, 0), si.model_weights(wl, 1)
-    mlp = si.mlp_steer_weights(wl, hml=hml, ln=ln)
+    mlp = si.mlp_steer_weights(wl, hml=hml, ln=ln, form=form)
     if zero_ws:
         mlp["w_s"] = np.zeros_like(mlp["w_s"])
     return oracle.Oracle(wl, wv, wd, None, mlp=mlp, **kw), wv, wd, mlp
@@ -192,3 +194,67 @@ def test_two_layer_verifier_is_rejected():
     wl = MLP8.with_(verifier=Dims(2, 128, 4, 2, 256, 256, 5e5))
     with pytest.raises(ValueError):
         _oracle(wl)
+
+
+def test_bias_after_mlp_forward_matches_torch():
+    wl = MLP8
+    o, _, wd, _ = _oracle(wl, form=2)
+    rng = np.random.default_rng(7)
+    ob = rng.normal(0, 0.3, size=(wl.drafter.d_model,))
+    toks = np.array([7, 8, 9, 10, 11], dtype=np.int32)
+    _, lg, _ = o.forward_mlp(1, toks, obias=ob)
+    _, rl = torch_ref.forward(wl.drafter, wd, wl.dtype, toks, obias=ob)
+    assert np.abs(lg - rl).max() < 1e-9 * max(1.0, np.abs(rl).max())
+    _, plain = o.forward(1, toks)
+    assert np.abs(lg - plain).max() > 1e-3
+
+
+def test_bias_after_mlp_round_against_torch():
+    """Form 2 over whole generations: the bias after each round is W_s LayerNorm(W_hml [h; m; l])
+    of the last committed input, and every drafter row carries the bias of the round that
+    processed it (a forward with per-position biases after every MLP)."""
+    wl = MLP8
+    o, wv, wd, mlp = _oracle(wl, form=2)
+    b = 1
+    toks, lens = si.prompts(wl)
+    o.prefill(toks, lens, [b])
+    p = int(lens[b])
+    dD = wl.drafter.d_model
+    bias_of_pos = {i: np.zeros(dD) for i in range(p - 1)}
+    rounds = 0
+    while not o.state(b)["done"]:
+        before = o.state(b)
+        ob = o.ubias(b)
+        t, ld = before["t"], before["len_d"]
+        _, _, tp = torch_ref.forward(wl.verifier, wv, wl.dtype, o.hist(b, t - 1), taps=True)
+        ref_b = torch_ref.mlp_steer(tp[-1], mlp, wl.dtype, wl.drafter.n_layers, wl.drafter.d_ff)
+        assert ob.shape == (dD,) and np.abs(ob - ref_b).max() < 1e-9 * np.abs(ref_b).max()
+        out, lg, dumps = o.round_one(b, dump=True)
+        for pos in range(ld, t + wl.k - 1):
+            bias_of_pos[pos] = ob
+        seq = list(o.hist(b, t)) + list(lg.drafts[: wl.k - 1])
+        rows = np.stack([bias_of_pos[i] for i in range(len(seq))])
+        _, ref = torch_ref.forward(wl.drafter, wd, wl.dtype, seq, obias=rows)
+        assert np.abs(dumps["logits_d"] - ref[t - 1 : t + wl.k - 1]).max() < 1e-5
+        for pos in list(bias_of_pos):
+            if pos >= o.state(b)["len_d"]:
+                del bias_of_pos[pos]
+        rounds += 1
+    assert rounds > 3
+
+
+def test_bias_after_mlp_greedy_matches_verifier_greedy_decode():
+    wl = MLP8.with_(temperature=0.0, new_tokens=20)
+    o, _, _, _ = _oracle(wl, form=2)
+    toks, lens = si.prompts(wl)
+    o.prefill(toks, lens)
+    outs = {b: [] for b in range(wl.batch)}
+    while any(not o.state(b)["done"] for b in range(wl.batch)):
+        for b in range(wl.batch):
+            if not o.state(b)["done"]:
+                outs[b].extend(o.round_one(b)[0].tolist())
+    for b in range(wl.batch):
+        p = int(lens[b])
+        seq = np.array(list(toks[b, :p]) + outs[b], dtype=np.int32)
+        _, lg = o.forward(0, seq[:-1])
+        assert list(lg[p - 1 :].astype(np.float32).argmax(axis=1)) == outs[b]

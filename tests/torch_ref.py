@@ -37,11 +37,12 @@ def tap_blocks(L):
     return [L - 2, L // 2, 3]
 
 
-def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False):
+def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False, obias=None):
     """Causal forward of a whole sequence; returns (final-norm hidden [T][d], logits [T][V]).
 
     ubias: up-projection biases added before the gating product, [L][F] for every row or
-    [T][L][F] per row.  taps=True also returns the residual stream after the tap blocks,
+    [T][L][F] per row.  obias: a bias added to every layer's MLP output, [d] or [T][d] per row.
+    taps=True also returns the residual stream after the tap blocks,
     [T][3][d]."""
     T = len(toks)
     d, H, Hkv, hd = dm.d_model, dm.n_heads, dm.n_kv_heads, dm.head_dim
@@ -73,6 +74,8 @@ def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False):
         if ub is not None:
             up = up + (ub[li] if ub.dim() == 2 else ub[:, li, :])
         x = x + (F.silu(n2 @ _t(wg, dtype).T) * up) @ _t(wd, dtype).T
+        if obias is not None:
+            x = x + torch.as_tensor(np.asarray(obias), dtype=torch.float64)
         outs.append(x)
     hF = norm(x, w["final_norm"])
     logits = (hF @ _t(w["lm_head"], dtype).T).numpy()
@@ -83,9 +86,11 @@ def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False):
 
 
 def mlp_steer(z, mlp, dtype, n_layers, d_ff):
-    """Per-layer up-projection biases [L][F] from z = [h; m; l]: W_s LayerNorm(W_hml z)."""
+    """Biases from z = [h; m; l]: W_s LayerNorm(W_hml z), per-layer up-projection biases [L][F]
+    (form 1) or the one bias after every MLP [d_D] (form 2)."""
     zt = torch.as_tensor(np.asarray(z, dtype=np.float64)).reshape(-1)
     g = _t(mlp["w_hml"], dtype) @ zt
     g = F.layer_norm(g, (g.shape[0],), weight=_t(mlp["ln_gain"], dtype), bias=_t(mlp["ln_bias"], dtype),
                      eps=mlp["ln_eps"])
-    return (_t(mlp["w_s"], dtype) @ g).reshape(n_layers, d_ff).numpy()
+    out = _t(mlp["w_s"], dtype) @ g
+    return (out.reshape(n_layers, d_ff) if int(mlp.get("form", 1)) == 1 else out).numpy()
