@@ -44,6 +44,8 @@ def steer_weight_bytes(wl, es, steering="input"):
     dV = wl.verifier.d_model
     if steering == "mlp":
         return (3 * dV * dV + wl.drafter.n_layers * wl.drafter.d_ff * dV) * es
+    if steering == "mlp-out":
+        return (3 * dV * dV + wl.drafter.d_model * dV) * es
     return wl.drafter.d_model * dV * es
 
 
@@ -196,9 +198,10 @@ def main():
     ap.add_argument("--prof-rounds", type=int, default=3)
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--steering", choices=["input", "mlp"], default="input",
+    ap.add_argument("--steering", choices=["input", "mlp", "mlp-out"], default="input",
                     help="input: s = W_s h added to the drafter's input embeddings; mlp: the paper's eq. (2) "
-                         "per-layer up-projection biases from three verifier layers (no CPU baseline)")
+                         "per-layer up-projection biases from three verifier layers; mlp-out: its ablation "
+                         "with one bias after every drafter MLP (no CPU baseline for either)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the rounds, copy one 1 GiB buffer (a plain copy of known size, the reference "
                          "point for scaling hardware traffic counters)")
@@ -247,8 +250,8 @@ def main():
         del items
         log(f"model {which} generated and uploaded ({time.time() - t0:.1f}s)")
     mlp_dev = None
-    if args.steering == "mlp":
-        mlp = si.mlp_steer_weights(wl)
+    if args.steering != "input":
+        mlp = si.mlp_steer_weights(wl, form=1 if args.steering == "mlp" else 2)
         mlp_dev = {key: B.to_device(mlp[key], dev) for key in ("w_s", "w_hml", "ln_gain", "ln_bias")}
         mlp_dev["ln_eps"] = mlp["ln_eps"]
         del mlp
@@ -260,7 +263,7 @@ def main():
     toks, lens = si.prompts(wl)
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
-        steer_form = B.STEER_MLP if mlp_dev is not None else B.STEER_INPUT
+        steer_form = {"input": B.STEER_INPUT, "mlp": B.STEER_MLP, "mlp-out": B.STEER_MLP_OUT}[args.steering]
         eng = B.Engine(B.config_of(wl, steering=steer_form), models[0], models[1], ws_dev, stream=stream,
                        device=dev, mlp=mlp_dev)
         t_tok = torch.from_numpy(toks).to(dev)

@@ -94,10 +94,14 @@ typedef struct {
                               from 1; high, middle, low; training details) and one bias b_l = W_s^(l) g
                               per drafter layer, added to the up projection before the gating product:
                               W_d((W_u a + b_l) * SiLU(W_g a)).  Needs L_V >= 3. */
+#define SD2_STEER_MLP_OUT 2 /* the paper's ablation "Inv. bias after MLP" (Sec. Ablation): the same g,
+                              and one bias b = W_s g of d_D values added to the output of every
+                              drafter MLP (x += W_d(...) + b).  Needs L_V >= 3. */
 
 /* Weights of SD2_STEER_MLP, device pointers in the configuration's dtype, 16-byte aligned. */
 typedef struct {
-    const void* w_s;       /* [L_D * d_ff_D][d_V]: rows l*d_ff_D .. (l+1)*d_ff_D - 1 give layer l's bias */
+    const void* w_s;       /* SD2_STEER_MLP: [L_D * d_ff_D][d_V], rows l*d_ff_D .. (l+1)*d_ff_D - 1 give
+                              layer l's bias; SD2_STEER_MLP_OUT: [d_D][d_V] */
     const void* w_hml;     /* [d_V][3 d_V]: g = W_hml [h; m; l] (columns: h, then m, then l) */
     const void* ln_gain;   /* [d_V] LayerNorm gain */
     const void* ln_bias;   /* [d_V] LayerNorm shift */
@@ -123,7 +127,8 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
 
 /*
  * Create a handle whose drafter is steered by the paper's MLP biases (eq. (2); Sec.
- * "Verification" and "Drafting"): cfg->steering must be SD2_STEER_MLP.  Everything else is as
+ * "Verification" and "Drafting"): cfg->steering must be SD2_STEER_MLP (or SD2_STEER_MLP_OUT, the
+ * ablation with one bias after every MLP).  Everything else is as
  * sd2_create.  The bias is recomputed at the end of every round from the verifier row whose
  * logits produced the final token, and used for every drafter token of the next round;
  * the drafter processes the prompt without steering, and the first round's bias comes from
@@ -191,8 +196,9 @@ const char* sd2_last_error(sd2_handle_t h);
                                  steps), entry p+1 = end of its phase p; SD2_ERR_STATE when that path
                                  is unavailable */
 
-#define SD2_DBG_UBIAS 12      /* float [batch][L_D][d_ff_D]: current up-projection biases (SD2_STEER_MLP;
-                                 SD2_ERR_STATE otherwise) */
+#define SD2_DBG_UBIAS 12      /* float [batch][L_D][d_ff_D]: current up-projection biases (SD2_STEER_MLP),
+                                 float [batch][d_D]: the bias after every MLP (SD2_STEER_MLP_OUT);
+                                 SD2_ERR_STATE for SD2_STEER_INPUT */
 
 /* Copy a debug buffer of the last round into host memory dst (bytes must match). */
 sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes);

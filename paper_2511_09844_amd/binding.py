@@ -39,7 +39,7 @@ class Config(ctypes.Structure):
                 ("temperature", ctypes.c_float), ("seed", ctypes.c_uint64), ("steering", ctypes.c_int32)]
 
 
-STEER_INPUT, STEER_MLP = 0, 1
+STEER_INPUT, STEER_MLP, STEER_MLP_OUT = 0, 1, 2
 
 
 class MlpSteering(ctypes.Structure):
@@ -146,7 +146,8 @@ class Engine:
     """One libsd2 handle.  `stream` is a torch.cuda.Stream (default: the current stream).
 
     With `mlp` (a dict of device tensors w_s, w_hml, ln_gain, ln_bias and a float ln_eps) the
-    handle is created by sd2_create_mlp (cfg.steering must be STEER_MLP) and `w_steer` is unused."""
+    handle is created by sd2_create_mlp (cfg.steering STEER_MLP or STEER_MLP_OUT) and `w_steer` is
+    unused."""
 
     def __init__(self, cfg: Config, verifier: DeviceModel, drafter: DeviceModel, w_steer: torch.Tensor,
                  stream=None, device="cuda", mlp=None):
@@ -221,7 +222,8 @@ class Engine:
             DBG_OWN_Y: ((B,), np.int32), DBG_STATE: ((B, 5), np.int32),
             DBG_HIST: ((B, self.cfg.max_seq_len), np.int32), DBG_HIDDEN_V: ((B, k + 1, dV), np.float32),
             DBG_PATH: ((2,), np.int32), DBG_TRACE: ((33, 1024), np.int64),
-            DBG_UBIAS: ((B, self.cfg.drafter.n_layers, self.cfg.drafter.d_ff), np.float32),
+            DBG_UBIAS: (((B, self.cfg.drafter.n_layers, self.cfg.drafter.d_ff) if self.cfg.steering == STEER_MLP
+                         else (B, self.cfg.drafter.d_model)), np.float32),
         }
         shp, dt = shapes[what]
         out = np.zeros(shp, dtype=dt)

@@ -83,7 +83,7 @@ struct Workspace {
     float* taps;            // [3][maxm][d_V] verifier residual after the tap blocks (per-operation path)
     float* tapsel;          // [max_batch][3 d_V] [h; m; l] of each sequence's steering row
     float* gsteer;          // [max_batch][d_V] g = W_hml [h; m; l], then its LayerNorm
-    float* ubias;           // [max_batch][L_D][F_D] up-projection biases of the current round
+    float* ubias;           // [max_batch][nbias] biases of the current round (L_D x F_D, or d_D)
 };
 
 // Per-launch timing entries (HIP events recorded on the engine's stream).
@@ -99,7 +99,9 @@ struct Engine {
     sd2_config cfg;
     ModelDev mv, md;
     const void* w_steer;    // SD2_STEER_INPUT: [d_D][d_V]; SD2_STEER_MLP: [L_D*F_D][d_V]
-    bool mlp;               // cfg.steering == SD2_STEER_MLP
+    bool mlp;               // cfg.steering is SD2_STEER_MLP or SD2_STEER_MLP_OUT (taps, W_hml, LayerNorm)
+    bool bias_after;        // SD2_STEER_MLP_OUT: the bias joins every drafter MLP's output
+    int nbias;              // bias values per sequence: L_D*F_D or d_D
     const void *w_hml, *ln_gain, *ln_bias;
     float ln_eps;
     int tap_layer[3];       // 0-based verifier layers after which h, m, l are taken
@@ -141,9 +143,10 @@ enum PlanKind { kPlanDraft1 = 0, kPlanDraftJ = 1, kPlanVerify = 2, kPlanPrefill 
 void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
                        const int32_t* prompt_len, int max_prompt, int chunk);
 // ubias (drafter rounds with MLP steering): this layer's biases, row stride ub_ld, indexed by
-// the row's sequence; null for none.
+// the row's sequence, added to the up projection, or to the MLP output when bias_after; null
+// for none.
 void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps, const float* ubias = nullptr,
-                  int ub_ld = 0);
+                  int ub_ld = 0, bool bias_after = false);
 // Final-norm LM head of `rows` residual rows into Y[out_map[r]] (bf16 path via the projection kernel).
 void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map);
 void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows);
@@ -179,7 +182,8 @@ struct WsCall {
     const float *rcos, *rsin;
     float *qout, *kc, *vc;
     int cap, max_batch, layer;
-    const float* ubias;  // SwiGLU: per-sequence up-projection bias rows (stride ub_ld, row_seq), or null
+    const float* ubias;  // per-sequence bias rows (stride ub_ld, row_seq): SwiGLU adds them to up, Add
+                         // to the output; or null
     int ub_ld;
 };
 struct WsPlan {

@@ -62,8 +62,9 @@ bool config_ok(const sd2_config* c) {
     if (c->max_new_tokens < 1) return false;
     if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // 8192 = 64 spans of 128
     if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
-    if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP) return false;
-    if (c->steering == SD2_STEER_MLP) {
+    if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP && c->steering != SD2_STEER_MLP_OUT)
+        return false;
+    if (c->steering != SD2_STEER_INPUT) {
         // the low tap is block 3; a steering projection runs on the MFMA kernel when its K is a
         // multiple of 256 (bf16), else on the vector kernel, which stages a K row of at most 16384
         const int dV = c->verifier.d_model;
@@ -72,6 +73,11 @@ bool config_ok(const sd2_config* c) {
         if (dV > 16384 && !(c->dtype == SD2_BF16 && dV % 256 == 0)) return false;
     }
     return true;
+}
+
+// MLP steering: bias values per sequence (per-layer up-projection biases, or one after-MLP bias)
+int bias_len(const sd2_config& c) {
+    return c.steering == SD2_STEER_MLP ? c.drafter.n_layers * c.drafter.d_ff : c.drafter.d_model;
 }
 
 int max_rows(const sd2_config& c) {
@@ -157,10 +163,9 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                     if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256 * subs);
                 }
         }
-        if (c.steering == SD2_STEER_MLP) {
-            // W_hml (d_V x 3 d_V) and W_s (L_D F_D x d_V) projections
-            int mshapes[2][2] = {{c.verifier.d_model, 3 * c.verifier.d_model},
-                                 {c.drafter.n_layers * c.drafter.d_ff, c.verifier.d_model}};
+        if (c.steering != SD2_STEER_INPUT) {
+            // W_hml (d_V x 3 d_V) and W_s (bias values x d_V) projections
+            int mshapes[2][2] = {{c.verifier.d_model, 3 * c.verifier.d_model}, {bias_len(c), c.verifier.d_model}};
             for (int mm = 1; mm <= std::min(B, 16); ++mm)
                 for (auto& sh : mshapes) {
                     WsPlan p = ws_plan(mm, sh[0], sh[1], kEpiStore);
@@ -171,8 +176,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         size_t tmax = (size_t)std::max(c.verifier.vocab, c.drafter.vocab) / 16 + 1;
         for (int i = 0; i < 2; ++i)
             tmax = std::max(tmax, (size_t)std::max(dd[i]->d_ff, dd[i]->d_model) / 16 + 1);
-        if (c.steering == SD2_STEER_MLP)
-            tmax = std::max(tmax, (size_t)c.drafter.n_layers * c.drafter.d_ff / 16 + 1);
+        if (c.steering != SD2_STEER_INPUT) tmax = std::max(tmax, (size_t)bias_len(c) / 16 + 1);
         w.ws_cnt = cv.take<int32_t>(tmax);
     }
     {
@@ -197,12 +201,12 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         }
         w.attn_cnt = cv.take<int32_t>(gmax);
     }
-    if (c.steering == SD2_STEER_MLP) {
+    if (c.steering != SD2_STEER_INPUT) {
         const size_t dV = c.verifier.d_model;
         w.taps = cv.take<float>(3 * (size_t)maxm * dV);
         w.tapsel = cv.take<float>((size_t)B * 3 * dV);
         w.gsteer = cv.take<float>((size_t)B * dV);
-        w.ubias = cv.take<float>((size_t)B * c.drafter.n_layers * c.drafter.d_ff);
+        w.ubias = cv.take<float>((size_t)B * bias_len(c));
     }
     for (int i = 0; i < 2; ++i) {
         ModelDev* m = ms[i];
@@ -314,13 +318,14 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
         else launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
         return;
     }
-    const int ub_ld = e.md.dm.n_layers * e.md.dm.d_ff;
+    const int ub_ld = e.nbias;
     for (int j = 1; j <= k; ++j) {
         int rows = j == 1 ? 2 * B : B;
         launch_plan_embed(s, e, e.md, j == 1 ? kPlanDraft1 : kPlanDraftJ, j, rows, nullptr, nullptr, 0, 1);
         for (int l = 0; l < e.md.dm.n_layers; ++l)
-            launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1, e.mlp ? e.ws.ubias + (size_t)l * e.md.dm.d_ff : nullptr,
-                         ub_ld);
+            launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1,
+                         !e.mlp ? nullptr : e.ws.ubias + (e.bias_after ? 0 : (size_t)l * e.md.dm.d_ff), ub_ld,
+                         e.bias_after);
         launch_lm_head(e, e.md, rows, e.ws.logits_d, e.ws.lm_map_d + (size_t)(j - 1) * 2 * e.cfg.max_batch);
         launch_draft_pick(s, e, j);
     }
@@ -415,7 +420,7 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     if (!out) return SD2_ERR_INVALID_ARG;
     *out = nullptr;
     if (!config_ok(cfg)) return SD2_ERR_INVALID_ARG;
-    if ((cfg->steering == SD2_STEER_MLP) != (mlp != nullptr)) return SD2_ERR_INVALID_ARG;
+    if ((cfg->steering != SD2_STEER_INPUT) != (mlp != nullptr)) return SD2_ERR_INVALID_ARG;
     if (mlp && (!aligned16(mlp->w_hml) || !aligned16(mlp->ln_gain) || !aligned16(mlp->ln_bias) ||
                 !(mlp->ln_eps >= 0.f)))
         return SD2_ERR_INVALID_ARG;
@@ -441,6 +446,8 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     e->stream = (hipStream_t)hip_stream;
     e->w_steer = w_steer;
     e->mlp = mlp != nullptr;
+    e->bias_after = cfg->steering == SD2_STEER_MLP_OUT;
+    e->nbias = bias_len(*cfg);
     if (mlp) {
         e->w_hml = mlp->w_hml;
         e->ln_gain = mlp->ln_gain;
@@ -642,7 +649,7 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
         case SD2_DBG_UBIAS:
             if (!e->mlp) return SD2_ERR_STATE;
             src = e->ws.ubias;
-            want = sizeof(float) * (size_t)B * e->md.dm.n_layers * e->md.dm.d_ff;
+            want = sizeof(float) * (size_t)B * e->nbias;
             break;
         case SD2_DBG_OWN_DRAFTS: src = e->ws.own_drafts; want = sizeof(int32_t) * (size_t)B * k; break;
         case SD2_DBG_OWN_N: src = e->ws.own_n; want = sizeof(int32_t) * (size_t)B; break;

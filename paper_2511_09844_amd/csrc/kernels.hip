@@ -160,7 +160,8 @@ struct GemvArgs {
     float* Y;
     int ldy;
     const int32_t* out_map;
-    const float* ubias;       // SwiGLU with MLP steering: bias rows per sequence (row_seq), or null
+    const float* ubias;       // MLP steering: bias rows per sequence (row_seq), added to up (SwiGLU) or
+                              // to the output (Add), or null
     int ub_ld;
     const int32_t* row_seq;
 };
@@ -276,7 +277,9 @@ __global__ __launch_bounds__(kGemvThreads) void k_gemv_vec(GemvArgs a) {
                     if (a.epi == kEpiStore) {
                         *yp = acc0[m];
                     } else if (a.epi == kEpiAdd) {
-                        *yp += acc0[m];
+                        float add = acc0[m];
+                        if (a.ubias) add += a.ubias[(size_t)a.row_seq[m0 + m] * a.ub_ld + n];
+                        *yp += add;
                     } else {
                         float up = acc1[m];
                         if (a.ubias) up += a.ubias[(size_t)a.row_seq[m0 + m] * a.ub_ld + n];
@@ -385,7 +388,9 @@ static WsCall ws_base(Engine& e, ModelDev& m) {
 }
 
 void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps, const float* ubias,
-                  int ub_ld) {
+                  int ub_ld, bool bias_after) {
+    const float* up_bias = bias_after ? nullptr : ubias;
+    const float* out_bias = bias_after ? ubias : nullptr;
     const sd2_dims& dm = m.dm;
     const void* const* W = m.layer + (size_t)layer * 9;
     int hd = m.hd, H = dm.n_heads, Hkv = dm.n_kv_heads;
@@ -411,12 +416,13 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, in
         g.X = m.x; g.M = rows; g.K = dm.d_model; g.gamma = W[kFfnNorm]; g.ss = m.ss;
         g.W[0] = W[kWg]; g.W[1] = W[kWu]; g.seg_rows[0] = dm.d_ff; g.seg_rows[1] = dm.d_ff; g.nseg = 2;
         g.mode = kEpiSwiglu; g.Y = e.ws.ffh; g.ldy = dm.d_ff;
-        g.ubias = ubias; g.ub_ld = ub_ld; g.row_seq = e.ws.row_seq;
+        g.ubias = up_bias; g.ub_ld = ub_ld; g.row_seq = e.ws.row_seq;
         launch_wsgemv(&e, s, g);
         // down projection + residual
         WsCall d = ws_base(e, m);
         d.X = e.ws.ffh; d.M = rows; d.K = dm.d_ff; d.W[0] = W[kWd]; d.seg_rows[0] = dm.d_model; d.nseg = 1;
         d.mode = kEpiAdd; d.Y = m.x; d.ldy = dm.d_model; d.ss_out = m.ss;
+        d.ubias = out_bias; d.ub_ld = ub_ld; d.row_seq = e.ws.row_seq;
         launch_wsgemv(&e, s, d);
         return;
     }
@@ -447,13 +453,13 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, in
         const void* ws[2] = {W[kWg], W[kWu]};
         int rws[2] = {dm.d_ff, dm.d_ff};
         launch_gemv(&e, s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kFfnNorm], dm.rms_eps, ws, rws, 2, kEpiSwiglu,
-                    e.ws.ffh, dm.d_ff, nullptr, ubias, ub_ld, e.ws.row_seq);
+                    e.ws.ffh, dm.d_ff, nullptr, up_bias, ub_ld, e.ws.row_seq);
     }
     {
         const void* ws[1] = {W[kWd]};
         int rws[1] = {dm.d_model};
         launch_gemv(&e, s, e.bf16, e.ws.ffh, nullptr, rows, dm.d_ff, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x,
-                    dm.d_model, nullptr);
+                    dm.d_model, nullptr, out_bias, ub_ld, e.ws.row_seq);
     }
 }
 
@@ -596,7 +602,7 @@ static void project_rows(Engine& e, const float* X, int rows, int K, const void*
 
 void launch_mlp_steer(Engine& e, const float* const* src, const int32_t* in_map, int rows) {
     const int dV = e.mv.dm.d_model;
-    const int nb = e.md.dm.n_layers * e.md.dm.d_ff;
+    const int nb = e.nbias;
     if (src) {  // else tapsel already holds the rows (prefill)
         prof_begin(&e, kProfOther, 0.0);
         k_tap_gather<<<rows, 256, 0, e.stream>>>(src[0], src[1], src[2], in_map, dV, e.ws.tapsel);
@@ -1013,7 +1019,7 @@ void launch_prefill_finish(hipStream_t s, Engine& e, int batch, const int32_t* p
     k_prefill_finish<<<batch, 256, 0, s>>>(batch, prompt_tok, prompt_len, max_prompt, e.ws.hist, e.cap, e.ws.t,
                                            e.ws.len_v, e.ws.len_d, e.ws.produced, e.ws.done, e.ws.steer,
                                            e.md.dm.d_model, e.mv.dm.vocab, e.mlp ? e.ws.ubias : nullptr,
-                                           e.md.dm.n_layers * e.md.dm.d_ff);
+                                           e.nbias);
 }
 
 // Final-norm rows (debug read of the verifier's hidden states).

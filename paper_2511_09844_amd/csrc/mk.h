@@ -34,7 +34,7 @@ struct MkPhase {
     int32_t defer;           // ATTN: leave the span partials unmerged (the next projection merges them)
     int32_t kvsig;           // Q|K|V: count every finished tile in on its KV head's counter
     int32_t kvwait;          // ATTN: wait for the unit's KV head counter instead of a grid barrier
-    int32_t ub_ld;           // SwiGLU: row stride of ubias (per sequence)
+    int32_t ub_ld;           // row stride of ubias (per sequence)
     const uint16_t* W[3];
     const float* X;          // activation rows [M][K] (kMkXBuf), or attention partials (kMkXAttn)
     const uint16_t* gamma;   // RMSNorm gain, or null (no norm)
@@ -47,7 +47,8 @@ struct MkPhase {
     float* qout;             // Qkv: queries [M][H*hd]; ATTN: query source
     float* aout;             // ATTN: output [M][H*hd]
     float* apart;            // ATTN: partials [M][H][nsplit][hd+4] (outputs, span max, span sum)
-    const float* ubias;      // SwiGLU: this layer's up-projection bias per sequence (MLP steering), or null
+    const float* ubias;      // MLP steering, per sequence: SwiGLU, this layer's up-projection bias; Add (down
+                             // projection), the bias after the MLP; or null
 };
 
 // Launch-wide arguments.

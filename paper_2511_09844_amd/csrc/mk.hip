@@ -601,6 +601,11 @@ __device__ __forceinline__ void mk_gemv(const MkArgs& a, const MkPhase& od, cons
                                    : jt < kPreTiles ? (jt == 0 ? pre0[0] : pre0[1])
                                                     : mk_ldg(oxres + (size_t)em * oldy + col);
                 nv = res0 + v0;
+                if constexpr (UB) {
+                    // steering bias after the MLP (the down projection's phase carries it)
+                    const float* oub = mk_uni(od.ubias);
+                    if (oub) nv += mk_ldg(oub + (size_t)rp.seq[em] * mk_uni(od.ub_ld) + col);
+                }
                 mk_stf(oY + (size_t)em * oldy + col, nv);
             }
             if (oss_out) {
@@ -1100,8 +1105,9 @@ __device__ __forceinline__ void mk_attn_phase(const MkArgs& a, const MkPhase& od
 
 // One kernel per head dim (64: drafter, 128: verifier), so that each holds one attention
 // instantiation: the code of a launch then stays closer to the instruction cache's size.  UB:
-// the SwiGLU epilogue adds the MLP-steering bias (drafter steps with that steering only; the
-// other instances carry no code for it).
+// the epilogues add the MLP-steering biases (to up in SwiGLU phases, or after the MLP in the down
+// projection's phase; drafter steps with that steering only: the other instances carry no code
+// for it).
 template <int HD, bool UB>
 __global__ __launch_bounds__(kMkThreads) void k_mk(MkArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1321,6 +1327,10 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
         dn.Y = xf;
         dn.ldy = dm;
         dn.ss_out = ss;
+        if (!verifier && ws && c.steering == SD2_STEER_MLP_OUT) {
+            dn.ubias = ws->ubias;
+            dn.ub_ld = dm;
+        }
         if (out) {
             out->push_back(qkv);
             out->push_back(at);

@@ -64,7 +64,8 @@ struct WsArgs {
     const float *rcos, *rsin;
     float *qout, *kc, *vc;
     int cap, max_batch, layer;
-    // SwiGLU with MLP steering: up-projection bias of the row's sequence (row_seq), or null
+    // MLP steering: bias of the row's sequence (row_seq), added to up (SwiGLU) or to the output
+    // (Add), or null
     const float* ubias;
     int ub_ld;
 };
@@ -104,6 +105,7 @@ __device__ __forceinline__ void tile_epilogue(const WsArgs& a, int tile, const f
         if (valid) {
             float* yp = a.Y + (size_t)row * a.ldy + tile * 16 + ec;
             nv = *yp + v[0];
+            if (a.ubias) nv += a.ubias[(size_t)a.row_seq[row] * a.ub_ld + tile * 16 + ec];
             *yp = nv;
         }
         float sq = nv * nv;

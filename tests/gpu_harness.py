@@ -71,7 +71,8 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
     else:
         ws_dev = {key: B.to_device(mlp[key]) for key in ("w_s", "w_hml", "ln_gain", "ln_bias")}
         ws_dev["ln_eps"] = mlp["ln_eps"]
-        eng = B.Engine(B.config_of(wl, steering=B.STEER_MLP), dv, dd, None, mlp=ws_dev)
+        form = B.STEER_MLP if int(mlp.get("form", 1)) == 1 else B.STEER_MLP_OUT
+        eng = B.Engine(B.config_of(wl, steering=form), dv, dd, None, mlp=ws_dev)
 
     def steer_err(b, dev):
         # the steering state of sequence b: s (input form) or the per-layer biases (MLP form)

@@ -97,7 +97,11 @@ def test_mlp_steering_configs():
         mlp = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl, steering=B.STEER_MLP)))
         dm = wl.drafter
         assert mlp >= base + wl.batch * dm.n_layers * dm.d_ff * 4
-    c = B.config_of(si.TINY, steering=2)
+    for wl in si.PRESETS[:4]:
+        base = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl)))
+        after = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl, steering=B.STEER_MLP_OUT)))
+        assert after >= base + wl.batch * wl.drafter.d_model * 4
+    c = B.config_of(si.TINY, steering=3)
     assert lib.sd2_workspace_bytes(ctypes.byref(c)) == 0
     c = B.config_of(si.TINY, steering=B.STEER_MLP)
     c.verifier.n_layers = 2

@@ -1,4 +1,5 @@
-"""GPU rounds with the paper's MLP steering (eq. (2)) vs the CPU oracle, through the C ABI.
+"""GPU rounds with the paper's MLP steering (eq. (2)) and its bias-after-MLP ablation vs the CPU
+oracle, through the C ABI.
 
 Every round compares logits, the per-layer up-projection biases W_s LayerNorm(W_hml [h; m; l])
 of every sequence (tolerance of the dtype), emitted tokens, counts and cache lengths (exact),
@@ -25,10 +26,10 @@ MLP_SMALL = Workload(
     dtype="bf16", k=3, batch=2, prompt=(1, 9), new_tokens=16, temperature=1.0, seed=21)
 
 
-def _run(wl, hml="normal", ln="normal", zero_ws=False, mlp=None, **kw):
+def _run(wl, hml="normal", ln="normal", zero_ws=False, mlp=None, form=1, **kw):
     from gpu_harness import parity_run
     if mlp is None:
-        mlp = si.mlp_steer_weights(wl, hml=hml, ln=ln)
+        mlp = si.mlp_steer_weights(wl, hml=hml, ln=ln, form=form)
     if zero_ws:
         mlp["w_s"] = np.zeros_like(mlp["w_s"])
     st = parity_run(wl, mlp=mlp, **kw)
@@ -67,6 +68,20 @@ def test_mlp_steering_f32():
 def test_mlp_steering_zero_ws_persistent():
     """W_s = 0 (the paper's initialisation): every bias is zero and the drafter is unsteered."""
     _run(MLP_MK, zero_ws=True, expect_path=1)
+
+
+def test_bias_after_mlp_persistent_path():
+    """The ablation with one bias W_s g after every drafter MLP (added in the down projection's
+    residual epilogue)."""
+    _run(MLP_MK, form=2, expect_path=1)
+
+
+def test_bias_after_mlp_separate_kernels():
+    _run(MLP_MK, form=2, separate_kernels=True, expect_path=0)
+
+
+def test_bias_after_mlp_f32():
+    _run(si.TINY.with_(new_tokens=16), form=2, expect_path=0)
 
 
 @pytest.fixture(scope="module")
