@@ -240,6 +240,16 @@ static size_t attn_lds(int hd) {
                             (size_t)kAttnQT * kAttnCL);
 }
 
+// Query heads per workgroup: all heads of a KV group (each K/V row then read once for all of
+// them) once the groups alone fill the chip and one tile holds all rows, or for long row blocks
+// (prefill chunks: tiles of 32/G rows); else one head per workgroup (more workgroups).
+int attn_heads_per_wg(int nseq, int rps, int H, int Hkv) {
+    const int G = H / Hkv;
+    if (G > kAttnQT) return 1;
+    if ((nseq * Hkv >= 128 && rps * G <= kAttnQT) || rps >= 64) return G;
+    return 1;
+}
+
 void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride) {
     const sd2_dims& dm = m.dm;
     AttnArgs a;
@@ -248,8 +258,7 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
     a.layer = layer;
     int nseq = rows / rps;
     int G = dm.n_heads / dm.n_kv_heads;
-    // all heads of a group per workgroup once the groups alone fill the chip and fit a tile
-    a.hp = (nseq * dm.n_kv_heads >= 128 && G <= kAttnQT && rps * G <= kAttnQT) ? G : 1;  // as attn_groups
+    a.hp = attn_heads_per_wg(nseq, rps, dm.n_heads, dm.n_kv_heads);
     int rows_per_tile = kAttnQT / a.hp;
     a.nrt = (rps + rows_per_tile - 1) / rows_per_tile;
     a.ngrp = nseq * dm.n_kv_heads * a.nrt;
@@ -273,7 +282,7 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
 // Workgroups of the split-free attention grid for a launch shape (arrival counters needed).
 size_t attn_groups(int rows, int rps, int H, int Hkv) {
     int nseq = rows / rps, G = H / Hkv;
-    int hp = (nseq * Hkv >= 128 && G <= kAttnQT && rps * G <= kAttnQT) ? G : 1;
+    int hp = attn_heads_per_wg(nseq, rps, H, Hkv);
     int rows_per_tile = kAttnQT / hp;
     int nrt = (rps + rows_per_tile - 1) / rows_per_tile;
     int ngrp = nseq * Hkv * nrt;
