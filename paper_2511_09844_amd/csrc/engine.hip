@@ -37,8 +37,9 @@ bool dims_ok(const sd2_dims& d) {
     int hd = d.d_model / d.n_heads;
     if (hd != 32 && hd != 64 && hd != 128) return false;
     if (d.d_model % 64 || (d.n_heads * hd) % 64 || d.d_ff % 64) return false;
-    // every GEMV input row must fit the 64 KiB of LDS a workgroup stages it in
-    if (d.d_model > 16384 || d.d_ff > 16384) return false;
+    // the residual row is at most 16384 wide; d_ff has no further limit for bf16 weights (the
+    // projection kernels split K into ranges); f32 weights: see config_ok
+    if (d.d_model > 16384 || d.d_ff > 65536) return false;
     if (!(d.rope_theta > 0.f) || !(d.rms_eps >= 0.f)) return false;
     return true;
 }
@@ -57,6 +58,8 @@ bool config_ok(const sd2_config* c) {
     if (c->dtype == SD2_BF16 && (!bf16_dims_ok(c->verifier) || !bf16_dims_ok(c->drafter))) return false;
     if (c->verifier.vocab != c->drafter.vocab) return false;
     if (c->dtype != SD2_F32 && c->dtype != SD2_BF16) return false;
+    // f32 weights use the vector projection kernel, which stages a whole input row in 64 KB of LDS
+    if (c->dtype == SD2_F32 && (c->verifier.d_ff > 16384 || c->drafter.d_ff > 16384)) return false;
     if (c->k < 1 || c->k > kMaxK) return false;
     if (c->max_batch < 1 || c->max_batch > 256) return false;
     if (c->max_new_tokens < 1) return false;

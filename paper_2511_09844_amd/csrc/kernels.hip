@@ -554,7 +554,7 @@ __global__ void k_tap_gather(const float* s0, const float* s1, const float* s2, 
 }
 
 // In-place LayerNorm of rows [rows][d]: (g - mean) / sqrt(var + eps) * gain + shift, population
-// variance, both moments from the row held in LDS (d <= 16384).
+// variance; one workgroup per row, two passes over it (mean, then centred squares).
 template <typename TW>
 __global__ __launch_bounds__(256) void k_layernorm_rows(float* X, int d, const TW* gain, const TW* shift, float eps) {
     __shared__ float red[4];

@@ -72,3 +72,13 @@ def test_parity_8b_batched_ragged_sampled_sequences(host_8b):
     wl = si.LLAMA8B_BATCHED.with_(prompt=(6, 30), new_tokens=5)
     wv, wd, ws = host_8b
     _run(wl, wv=wv, wd=wd, ws=ws, seqs=[0, 11])
+
+
+def test_parity_70b_width_two_layers():
+    """The 70B shape's verifier layer width (d 8192, 64 query / 8 KV heads, F 28672: down
+    projection K beyond 16384, split into K ranges) on two layers, with the 1B-shaped drafter,
+    k = 8, batch 2 (18 verifier rows: the many-row GEMM and the per-operation path)."""
+    from sd2_inputs.configs import Dims
+    wl = si.LLAMA70B.with_(verifier=Dims(2, 8192, 64, 8, 28672, 128256, 5e5), batch=2, prompt=(7, 12),
+                           new_tokens=9)
+    _run(wl)
