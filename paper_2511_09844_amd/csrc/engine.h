@@ -77,6 +77,7 @@ struct Workspace {
     // split-K partial tiles of the projection kernel; attention partials per position span
     float* ws_part;
     int32_t* ws_cnt;
+    size_t ws_part_n, ws_cnt_n;  // their capacities (floats, counters)
     float* attn_part;
     int32_t* attn_cnt;
     // MLP steering (null unless cfg.steering == SD2_STEER_MLP)
@@ -192,7 +193,8 @@ struct WsPlan {
 };
 WsPlan ws_plan(int M, int N, int K, int mode);
 void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c);
-hipError_t wsgemv_setup();  // kernel attributes of the many-row GEMM (once per process and device)
+hipError_t wsgemv_setup();
+int pg_split(int M, int N, int K, int subs);  // K ranges of the many-row GEMM for a shape  // kernel attributes of the many-row GEMM (once per process and device)
 void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride);
 int attn_nsplit(int cap);
 size_t attn_groups(int rows, int rps, int H, int Hkv);

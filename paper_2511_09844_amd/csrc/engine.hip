@@ -147,7 +147,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
     w.forced_on = cv.take<int32_t>(1);
     // projection split-K partials: the largest tiles*S*256*subs over every projection shape
     {
-        size_t pmax = 0;
+        size_t pmax = 0, pg_cnt = 0;
         const sd2_dims* dd[2] = {&c.verifier, &c.drafter};
         int mmax = std::min(maxm, 16);
         for (int i = 0; i < 2; ++i) {
@@ -175,12 +175,35 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                     if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256);
                 }
         }
+        // many-row GEMM with K ranges: [tile][m block][range][subs][4 x 256] partials
+        for (int i = 0; i < 2; ++i) {
+            const sd2_dims& d = *dd[i];
+            int hd = d.d_model / d.n_heads;
+            int shapes[5][3] = {{(d.n_heads + 2 * d.n_kv_heads) * hd, d.d_model, 1},
+                                {d.d_model, d.n_heads * hd, 1},
+                                {d.d_ff, d.d_model, 2},
+                                {d.d_model, d.d_ff, 1},
+                                {d.vocab, d.d_model, 1}};
+            // the split depends on the rows only through their number of 64-row blocks
+            for (int nbm = 1; nbm <= (maxm + 63) / 64; ++nbm)
+                for (auto& sh : shapes) {
+                    int S = pg_split(nbm * 64, sh[0], sh[1], sh[2]);
+                    size_t nblkm = (size_t)nbm;
+                    if (S > 1) {
+                        pmax = std::max(pmax, nblkm * (sh[0] / 16) * S * sh[2] * 1024);
+                        pg_cnt = std::max(pg_cnt, nblkm * (sh[0] / 16));
+                    }
+                }
+        }
         w.ws_part = cv.take<float>(std::max<size_t>(pmax, 1));
+        w.ws_part_n = std::max<size_t>(pmax, 1);
         size_t tmax = (size_t)std::max(c.verifier.vocab, c.drafter.vocab) / 16 + 1;
         for (int i = 0; i < 2; ++i)
             tmax = std::max(tmax, (size_t)std::max(dd[i]->d_ff, dd[i]->d_model) / 16 + 1);
         if (c.steering != SD2_STEER_INPUT) tmax = std::max(tmax, (size_t)bias_len(c) / 16 + 1);
+        tmax = std::max(tmax, pg_cnt);
         w.ws_cnt = cv.take<int32_t>(tmax);
+        w.ws_cnt_n = tmax;
     }
     {
         size_t amax = 0;

@@ -90,11 +90,12 @@ __device__ __forceinline__ const uint16_t* tile_row(const WsArgs& a, int tile, i
 // Epilogue of one finished 16x16 tile; element (m, c) is held by thread t = 16m + c of the
 // first 256 threads.  `v` holds the value per sub-tile.
 template <int SUBS>
-__device__ __forceinline__ void tile_epilogue(const WsArgs& a, int tile, const float* v) {
+// Rows row0 .. row0 + nrows - 1 of the launch (at most 16).
+__device__ __forceinline__ void tile_epilogue(const WsArgs& a, int tile, const float* v, int row0, int nrows) {
     const int tid = threadIdx.x;
     const int em = tid >> 4, ec = tid & 15;
-    const bool valid = em < a.M;
-    const int row = a.row0 + em;
+    const bool valid = em < nrows;
+    const int row = row0 + em;
     if (a.mode == kEpiStore) {
         if (valid) {
             int orow = a.out_map ? a.out_map[row] : row;
@@ -289,7 +290,7 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
             stash = x;
         } else if (a.S == 1) {
             float v[2] = {SUBS == 2 ? stash : x, x};
-            if (tid < 256) tile_epilogue<SUBS>(a, tile, v);
+            if (tid < 256) tile_epilogue<SUBS>(a, tile, v, a.row0, a.M);
         } else {
             // K split over S workgroups: the last to finish this tile adds the partials in order
             float* pt = a.part + (size_t)tile * a.S * SUBS * 256;
@@ -318,7 +319,7 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
                     }
                 }
                 if (SUBS == 1) v[1] = v[0];
-                tile_epilogue<SUBS>(a, tile, v);
+                tile_epilogue<SUBS>(a, tile, v, a.row0, a.M);
             }
         }
         __syncthreads();
@@ -348,18 +349,35 @@ constexpr int kPgLdk = kPgKC + 8;     // padded LDS row stride (bf16 elements)
 constexpr size_t kPgLds = 2 * kPgRows * kPgLdk * 2;  // hi and lo planes (also holds the 32 KB of results)
 static_assert(kPgLds >= 4 * kPgTW * 4 * 256 * 4, "result staging must fit the activation planes");
 
+// K ranges for a many-row projection: split while the grid stays within 2 workgroups per CU and
+// every range keeps at least 1024 columns (a multiple of 256).  Shared by the launch and the
+// workspace sizing.
+int pg_split(int M, int N, int K, int subs) {
+    const int nt = 4 * kPgTW / subs;
+    const int nblk_m = (M + kPgRows - 1) / kPgRows;
+    const int nblk_n = (N / 16 + nt - 1) / nt;
+    const int blocks = 8 * nblk_m * ((nblk_n + 7) / 8);
+    int S = 1;
+    while (blocks * S * 2 <= 512 && (K / (S * 2)) % 256 == 0 && K / (S * 2) >= 1024 && K % (S * 2) == 0) S *= 2;
+    return S;
+}
+
 template <int SUBS>
-__global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m) {
+__global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ float inv_rms[kPgRows];
     __shared__ int src_row[kPgRows];
+    __shared__ int last_flag;
     constexpr int NT = 4 * kPgTW / SUBS;  // 16-row output tiles per workgroup
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = lane & 15, q = lane >> 4;
     // block -> (n block, m block): workgroups are dealt to the 8 XCDs in turn, so blocks b, b + 8,
     // ... share an XCD; they take the m blocks of one n block, whose weights then come from that
     // XCD's L2 after the first read
-    const int xcd = blockIdx.x & 7, r = blockIdx.x >> 3;
+    // K range s of a.S (blocks of one range are contiguous); within it, as for S = 1
+    const int s = blockIdx.x / nbs;
+    const int bb = blockIdx.x % nbs;
+    const int xcd = bb & 7, r = bb >> 3;
     const int mb = r % nblk_m;
     const int nb = xcd + 8 * (r / nblk_m);
     const int tile0 = nb * NT;
@@ -400,7 +418,8 @@ __global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m) {
     for (int j = 0; j < kPgTW; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) acc[j][g] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < a.K; k0 += kPgKC) {
+    const int KS = a.K / a.S;
+    for (int k0 = s * KS; k0 < (s + 1) * KS; k0 += kPgKC) {
         u32x4_t w[kPgTW][4][2];
 #pragma unroll
         for (int j = 0; j < kPgTW; ++j)
@@ -467,21 +486,39 @@ __global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m) {
             for (int i = 0; i < 4; ++i) red[((wave * kPgTW + j) * 4 + g) * 256 + (4 * q + i) * 16 + n] = acc[j][g][i];
     __syncthreads();
     // per output tile and row group: element (m, c) at thread 16 m + c; SwiGLU's up value of
-    // local tile lt sits 2 TW slots after its gate value
-    WsArgs ar = a;
+    // local tile lt sits 2 TW slots after its gate value.  With K ranges, each range stores its
+    // sums of (tile, m block) and the last to arrive adds the S partials in range order.
     for (int lt = 0; lt < NT; ++lt) {
         const int tile = tile0 + lt;
         if (tile >= a.tiles) break;
+        float* pt = nullptr;
+        if (a.S > 1) {
+            pt = a.part + (size_t)(tile * nblk_m + mb) * a.S * SUBS * 1024;
+#pragma unroll
+            for (int sub = 0; sub < SUBS; ++sub)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    store_through(pt + ((size_t)s * SUBS + sub) * 1024 + g * 256 + tid,
+                                  red[((lt + sub * 2 * kPgTW) * 4 + g) * 256 + tid]);
+            if (!arrive_last(a.cnt + tile * nblk_m + mb, a.S, &last_flag)) continue;
+        }
         for (int g = 0; g < 4; ++g) {
             const int row0 = m0 + g * 16;
             if (row0 >= M) break;
             const float sc = inv_rms[g * 16 + (tid >> 4)];
-            float v[2];
-            v[0] = red[(lt * 4 + g) * 256 + tid] * sc;
-            v[1] = SUBS == 2 ? red[((lt + 2 * kPgTW) * 4 + g) * 256 + tid] * sc : v[0];
-            ar.row0 = row0;
-            ar.M = min(16, M - row0);
-            tile_epilogue<SUBS>(ar, tile, v);
+            float v[2] = {0.f, 0.f};
+            if (a.S > 1) {
+                for (int s0 = 0; s0 < a.S; ++s0) {
+                    v[0] += pt[((size_t)s0 * SUBS) * 1024 + g * 256 + tid];
+                    if (SUBS == 2) v[1] += pt[((size_t)s0 * SUBS + 1) * 1024 + g * 256 + tid];
+                }
+            } else {
+                v[0] = red[(lt * 4 + g) * 256 + tid];
+                if (SUBS == 2) v[1] = red[((lt + 2 * kPgTW) * 4 + g) * 256 + tid];
+            }
+            v[0] *= sc;
+            v[1] = SUBS == 2 ? v[1] * sc : v[0];
+            tile_epilogue<SUBS>(a, tile, v, row0, min(16, M - row0));
         }
     }
 }
@@ -556,7 +593,16 @@ static bool launch_pgemm(Engine* e, hipStream_t s, const WsCall& c) {
     if (c.mode == kEpiSwiglu) tiles = c.seg_rows[0] / 16;
     a.nseg = c.nseg; a.mode = c.mode; a.tiles = tiles;
     a.Y = c.Y; a.ldy = c.ldy; a.out_map = c.out_map; a.ss_out = c.ss_out;
-    a.S = 1;
+    const int subs0 = c.mode == kEpiSwiglu ? 2 : 1;
+    a.S = pg_split(c.M, tiles * 16, c.K, subs0);
+    {
+        // partials and counters must fit the workspace; else no K split
+        const size_t nblkm = (size_t)(c.M + kPgRows - 1) / kPgRows;
+        if (a.S > 1 && (nblkm * tiles * a.S * subs0 * 1024 > e->ws.ws_part_n || nblkm * tiles > e->ws.ws_cnt_n))
+            a.S = 1;
+    }
+    a.part = c.part;
+    a.cnt = c.cnt;
     a.H = c.H; a.Hkv = c.Hkv; a.hd = c.hd; a.row_pos = c.row_pos; a.row_seq = c.row_seq;
     a.rcos = c.rcos; a.rsin = c.rsin; a.qout = c.qout; a.kc = c.kc; a.vc = c.vc;
     a.cap = c.cap; a.max_batch = c.max_batch; a.layer = c.layer;
@@ -565,15 +611,16 @@ static bool launch_pgemm(Engine* e, hipStream_t s, const WsCall& c) {
     const int nt = 4 * kPgTW / subs;
     const int nblk_m = (c.M + kPgRows - 1) / kPgRows;
     const int nblk_n = (tiles + nt - 1) / nt;
-    dim3 grid(8 * nblk_m * ((nblk_n + 7) / 8));
+    const int nbs = 8 * nblk_m * ((nblk_n + 7) / 8);
+    dim3 grid(nbs * a.S);
     const double wbytes = (double)tiles * 16 * subs * c.K * 2.0;
     ProfEntry* pe = prof_slot(e, kProfGemv, wbytes + (double)c.M * c.K * 4.0 + (double)c.M * tiles * 16 * 4.0);
     if (subs == 2) {
-        if (pe) hipExtLaunchKernelGGL((k_pgemm<2>), grid, dim3(256), kPgLds, s, pe->a, pe->b, 0, a, nblk_m);
-        else k_pgemm<2><<<grid, 256, kPgLds, s>>>(a, nblk_m);
+        if (pe) hipExtLaunchKernelGGL((k_pgemm<2>), grid, dim3(256), kPgLds, s, pe->a, pe->b, 0, a, nblk_m, nbs);
+        else k_pgemm<2><<<grid, 256, kPgLds, s>>>(a, nblk_m, nbs);
     } else {
-        if (pe) hipExtLaunchKernelGGL((k_pgemm<1>), grid, dim3(256), kPgLds, s, pe->a, pe->b, 0, a, nblk_m);
-        else k_pgemm<1><<<grid, 256, kPgLds, s>>>(a, nblk_m);
+        if (pe) hipExtLaunchKernelGGL((k_pgemm<1>), grid, dim3(256), kPgLds, s, pe->a, pe->b, 0, a, nblk_m, nbs);
+        else k_pgemm<1><<<grid, 256, kPgLds, s>>>(a, nblk_m, nbs);
     }
     if (pe) prof_commit(e);
     return true;
