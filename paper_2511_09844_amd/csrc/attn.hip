@@ -240,14 +240,14 @@ static size_t attn_lds(int hd) {
                             (size_t)kAttnQT * kAttnCL);
 }
 
-// Query heads per workgroup: all heads of a KV group (each K/V row then read once for all of
-// them) once the groups alone fill the chip and one tile holds all rows, or for long row blocks
-// (prefill chunks: tiles of 32/G rows); else one head per workgroup (more workgroups).
+// Query heads per workgroup: all heads of a KV group, so that each K/V row is read once for all
+// of them (rows are then tiled 32/G at a time); one head per workgroup only for groups wider
+// than a tile.
 int attn_heads_per_wg(int nseq, int rps, int H, int Hkv) {
+    (void)nseq;
+    (void)rps;
     const int G = H / Hkv;
-    if (G > kAttnQT) return 1;
-    if ((nseq * Hkv >= 128 && rps * G <= kAttnQT) || rps >= 64) return G;
-    return 1;
+    return G > kAttnQT ? 1 : G;
 }
 
 void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int rps, const float* q, int q_stride) {
