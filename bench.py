@@ -1,12 +1,18 @@
-"""Benchmark of one SD^2 speculative-decoding round on one MI355X.
+"""Benchmark of SD^2 speculative decoding on one MI355X.
 
-A step is one call of sd2_round: k steered drafter steps, the (k+1)-row verifier
-block forward, the accept/resample decision, commit with KV-length rollback and
-the steering projection, for every sequence of the batch.  Inputs are synthetic
-(seeded N(0, 0.02) weights, uniform-random prompt ids) with the shapes of the
-named workload; weights and prompts are resident in HBM before timing starts.
+A step is one whole generation of the named workload: sd2_prefill of the prompts,
+then sd2_round until every sequence has its new tokens.  Each round is k steered
+drafter steps, the (k+1)-row verifier block forward, the accept/resample
+decision, commit with KV-length rollback and the steering projection, for every
+sequence of the batch.  The first warm-up generation reads the state after every
+round to learn how many rounds a generation takes; generations are deterministic
+(fixed Philox stream, fixed reduction orders), so the timed ones replay exactly
+those rounds with no host synchronisation.  Events between rounds give per-round
+latency; bytes per round are counted at each round's own context length.
 
-Prints ONE JSON line on stdout; progress goes to stderr.
+Inputs are synthetic (seeded N(0, 0.02) weights, uniform-random prompt ids) with
+the shapes of the named workload; weights and prompts are resident in HBM before
+timing starts.  Prints ONE JSON line on stdout; progress goes to stderr.
 """
 import argparse
 import json
@@ -76,9 +82,10 @@ def cpu_baseline(wl, wv, wd, ws, toks, lens, budget_s):
         rounds += 1
         log(f"cpu oracle round {rounds}: {len(out)} tokens, {time.time() - t0:.1f}s")
     dt = time.time() - t0
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle", "cpu": cpu_model(),
             "sample": f"sequence 0 only, first {prefix} prompt tokens prefilled (untimed), then {rounds} rounds "
-                      f"({tokens} tokens) timed; float64 C oracle, OpenMP over output rows"}
+                      f"({tokens} tokens) timed; float64 C oracle, OpenMP over output rows (the round's cost is "
+                      f"its weights: KV reads at a {prefix}-token context instead of 512-768 change it by about 2 %)"}
 
 
 # ---------------------------------------------------------------------------------------------
@@ -103,32 +110,41 @@ def _round_windows(names, skip_first):
     return list(zip(marks[:-1], marks[1:]))[skip_first:]
 
 
-def summarize_trace(path, last_eager):
-    """Per-round kernel time by class from a kernel_trace.csv: the graph-launched rounds and the
-    last `last_eager` (eagerly launched, event-timed) rounds separately."""
+def _trace_rows(path):
+    """(kernel name, start ns, end ns) of every dispatch in a rocprofv3 kernel trace: the rocpd
+    database (`*_results.db`, the default output) or a kernel_trace.csv."""
+    if path.endswith(".db"):
+        import sqlite3
+        con = sqlite3.connect(path)
+        rows = list(con.execute("select name, start, end from kernels order by start"))
+        con.close()
+        return rows
     import csv
-    rows = []
     with open(path) as f:
-        for r in csv.DictReader(f):
-            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
-    rows.sort()
-    wins = _round_windows([r[2] for r in rows], 0)
-    groups = (("timed rounds (graph replays; eager launches on the persistent path)", wins[:len(wins) - last_eager]),
-              ("profiled (event-timed, eager) rounds", wins[-last_eager:]))
-    for title, ws in groups:
-        if not ws:
-            continue
-        per, span = {}, 0
-        for a, b in ws:
-            span += rows[b][0] - rows[a][0]
-            for st, en, n in rows[a:b]:
-                c = per.setdefault(_kclass(n), [0, 0])
-                c[0] += 1
-                c[1] += en - st
-        print(f"{title}: {len(ws)} rounds, {span / len(ws) / 1e3:.1f} us per round (first kernel to first kernel)")
-        for c, (n, ns) in sorted(per.items(), key=lambda x: -x[1][1]):
-            print(f"  {c:9s} {n / len(ws):6.0f} launches/round  {ns / len(ws) / 1e3:9.1f} us/round  "
-                  f"avg {ns / n / 1e3:7.2f} us/launch")
+        return sorted(((r["Kernel_Name"], int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+                       for r in csv.DictReader(f)), key=lambda x: x[1])
+
+
+def summarize_trace(path):
+    """Per-kernel launches and time per round from a rocprofv3 kernel trace of this script (rounds
+    are counted by k_set_flag, the first kernel of every round; prefill kernels are listed with the
+    rest, under their own names)."""
+    per, rounds = {}, 0
+    for name, start, end in _trace_rows(path):
+        if "k_set_flag" in name:
+            rounds += 1
+        key = name.split("(")[0].replace("void ", "").replace("sd2::", "")
+        c = per.setdefault(key, [0, 0])
+        c[0] += 1
+        c[1] += end - start
+    print(f"{rounds} rounds in the trace")
+    for key, (n, ns) in sorted(per.items(), key=lambda x: -x[1][1])[:20]:
+        print(f"  {key[:40]:40s} {n:7d} launches {n / max(1, rounds):6.2f}/round  {ns / 1e6:10.2f} ms total  "
+              f"avg {ns / n / 1e3:9.2f} us")
+    mk = [v for k, v in per.items() if k.startswith("k_mk<")]
+    if mk:
+        n, ns = sum(v[0] for v in mk), sum(v[1] for v in mk)
+        print(f"k_mk, all instances: {n} launches, average {ns / n / 1e3:.2f} us")
 
 
 def _source_hash():
@@ -187,17 +203,101 @@ def stored_traffic(workload):
     return rec.get("traffic_bytes_per_launch")
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def discover(eng, t_tok, t_len, wl):
+    """One generation with the host reading the state after every round: the number of rounds a
+    generation takes and every round's start length and active flag per sequence.  A generation
+    is deterministic (fixed Philox stream, fixed reduction orders), so later generations replay
+    exactly these rounds without host synchronisation."""
+    import torch
+
+    eng.prefill(t_tok, t_len, wl.max_prompt)
+    rounds = []
+    while True:
+        st = eng.state()
+        if all(s["done"] for s in st[: wl.batch]):
+            break
+        rounds.append([(s["t"], not s["done"]) for s in st[: wl.batch]])
+        eng.round()
+        torch.cuda.synchronize()
+        if len(rounds) > wl.new_tokens + 8:
+            raise RuntimeError("generation did not finish within new_tokens rounds")
+    st = eng.state()
+    produced = sum(s["produced"] for s in st[: wl.batch])
+    return rounds, produced
+
+
+def generation(eng, t_tok, t_len, wl, nrounds, stream, evs=None):
+    """Prefill + nrounds rounds, enqueued without host synchronisation; with `evs` (nrounds + 2
+    events) an event is recorded before the prefill, after it and after every round."""
+    if evs is not None:
+        evs[0].record(stream)
+    eng.prefill(t_tok, t_len, wl.max_prompt)
+    if evs is not None:
+        evs[1].record(stream)
+    for r in range(nrounds):
+        eng.round()
+        if evs is not None:
+            evs[r + 2].record(stream)
+
+
+def gen_bytes(wl, rounds, steering):
+    """Algorithmic bytes of every round of a generation (active sequences at their start lengths)."""
+    out = []
+    for rnd in rounds:
+        w_b, kv = 0.0, 0.0
+        for t, active in rnd:
+            if not active:
+                continue
+            w, kvv, kvd = round_bytes(wl, t, steering)
+            w_b = w
+            kv += kvv + kvd
+        out.append((w_b, kv))
+    return out
+
+
+def timed_generations(eng, t_tok, t_len, wl, nrounds, steps, stream):
+    """K generations between two synchronisations; returns total ms, per-generation prefill ms
+    and every round's ms."""
+    import torch
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nrounds + 2)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_start = time.time()
+    for g in range(steps):
+        generation(eng, t_tok, t_len, wl, nrounds, stream, evs[g])
+    torch.cuda.synchronize()
+    wall = time.time() - t_start
+    total = evs[0][0].elapsed_time(evs[-1][-1])
+    prefill = [e[0].elapsed_time(e[1]) for e in evs]
+    rounds = [e[r + 1].elapsed_time(e[r + 2]) for e in evs for r in range(nrounds)]
+    return total, wall, prefill, rounds
+
+
 def main():
     import sd2_inputs as si
 
-    ap = argparse.ArgumentParser()
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20, help="timed generations (prefill + every round to new_tokens)")
+    ap.add_argument("--warmup", type=int, default=3, help="untimed generations before them")
     ap.add_argument("--workload", default=si.LLAMA8B.name, choices=list(si.BY_NAME))
-    ap.add_argument("--prof-rounds", type=int, default=3)
+    ap.add_argument("--prof-generations", type=int, default=1,
+                    help="generations replayed with a HIP event pair around every launch (kernel roofline)")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-steer-overhead", action="store_true",
+                    help="skip the unsteered-drafter generations that give steer_overhead_ms")
     ap.add_argument("--steering", choices=["input", "mlp", "mlp-out"], default="input",
                     help="input: s = W_s h added to the drafter's input embeddings; mlp: the paper's eq. (2) "
                          "per-layer up-projection biases from three verifier layers; mlp-out: its ablation "
@@ -205,6 +305,9 @@ def main():
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the rounds, copy one 1 GiB buffer (a plain copy of known size, the reference "
                          "point for scaling hardware traffic counters)")
+    ap.add_argument("--maps-out", metavar="PATH",
+                    help="write this process's /proc/self/maps to PATH after teardown (resolves the frames "
+                         "of a crash at exit)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print the per-round breakdown of a rocprofv3 kernel trace of this script and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -213,13 +316,16 @@ def main():
     ap.add_argument("--write-traffic", action="store_true", help="with --summarize-pmc: store the result")
     args = ap.parse_args()
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace, args.prof_rounds)
+        summarize_trace(args.summarize_trace)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, TRAFFIC_FILE if args.write_traffic else None)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the round runs on one device); --gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1:
+        print("--steps must be at least 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -262,48 +368,60 @@ def main():
         ws_dev = B.to_device(ws, dev)
     toks, lens = si.prompts(wl)
     stream = torch.cuda.Stream()
+    engines = []
     with torch.cuda.stream(stream):
         steer_form = {"input": B.STEER_INPUT, "mlp": B.STEER_MLP, "mlp-out": B.STEER_MLP_OUT}[args.steering]
         eng = B.Engine(B.config_of(wl, steering=steer_form), models[0], models[1], ws_dev, stream=stream,
                        device=dev, mlp=mlp_dev)
+        engines.append(eng)
         t_tok = torch.from_numpy(toks).to(dev)
         t_len = torch.from_numpy(lens).to(dev)
         torch.cuda.synchronize()
-        tp = time.time()
-        eng.prefill(t_tok, t_len, wl.max_prompt)
+        # warm-up: the first generation (host reads the state after every round) finds the rounds
+        tw = time.time()
+        rounds, produced = discover(eng, t_tok, t_len, wl)
+        nr = len(rounds)
+        log(f"generation: {nr} rounds, {produced} tokens ({time.time() - tw:.2f}s with host reads)")
+        for _ in range(max(0, args.warmup - 1)):
+            generation(eng, t_tok, t_len, wl, nr, stream)
         torch.cuda.synchronize()
-        prefill_s = time.time() - tp
-        log(f"prefill done in {prefill_s:.2f}s")
-        for _ in range(args.warmup):
-            eng.round()
-        torch.cuda.synchronize()
-        st0 = eng.state()
-        # one event between consecutive rounds: the whole span gives the mean, the gaps the spread
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-        evs[0].record(stream)
-        for i in range(args.steps):
-            eng.round()
-            evs[i + 1].record(stream)
-        torch.cuda.synchronize()
-        ms = evs[0].elapsed_time(evs[-1])
-        per_round = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
-        st1 = eng.state()
-        log(f"timed {args.steps} rounds: {ms:.2f} ms")
-        # kernel-level timing: HIP events around every launch of the same rounds, recorded into the graph
+        total_ms, wall_s, prefill_ms, round_ms = timed_generations(eng, t_tok, t_len, wl, nr, args.steps, stream)
+        st_end = eng.state()
+        assert all(s["done"] for s in st_end[: wl.batch]), "a timed generation did not finish"
+        assert sum(s["produced"] for s in st_end[: wl.batch]) == produced, "generations differ"
+        log(f"timed {args.steps} generations: {total_ms:.1f} ms (host clock {wall_s * 1e3:.1f} ms)")
+        # kernel-level timing: HIP events around every launch of whole replayed generations
         prof = {c: [0, 0.0, 0.0] for c in (B.PROF_PROGRAM, B.PROF_GEMV, B.PROF_ATTN, B.PROF_SAMPLER, B.PROF_OTHER)}
-        stp0 = eng.state()
-        if args.prof_rounds > 0:
+        kv_prof = 0.0
+        gb = gen_bytes(wl, rounds, args.steering)
+        for _ in range(args.prof_generations):
+            eng.prefill(t_tok, t_len, wl.max_prompt)
             eng.profile(True)
-            for _ in range(args.prof_rounds):
+            for r in range(nr):
                 eng.round()
                 for c in prof:
                     n, pms, pby = eng.profile_read(c)
                     prof[c][0] += n
                     prof[c][1] += pms
                     prof[c][2] += pby
+                kv_prof += gb[r][1]
             eng.profile(False)
         torch.cuda.synchronize()
-        stp1 = eng.state()
+        # steering overhead: the same generation with the unsteered (pretrained) drafter
+        overhead = None
+        if not args.no_steer_overhead:
+            e0 = B.Engine(B.config_of(wl, steering=B.STEER_NONE), models[0], models[1], None, stream=stream,
+                          device=dev)
+            engines.append(e0)
+            r0, _ = discover(e0, t_tok, t_len, wl)
+            gens0 = max(1, min(args.steps, 5))
+            _, _, _, rms0 = timed_generations(e0, t_tok, t_len, wl, len(r0), gens0, stream)
+            steered = sum(round_ms) / len(round_ms)
+            unsteered = sum(rms0) / len(rms0)
+            overhead = {"steer_overhead_ms": steered - unsteered, "round_ms_steered_mean": steered,
+                        "round_ms_unsteered_mean": unsteered, "unsteered_generations": gens0,
+                        "unsteered_rounds_per_generation": len(r0)}
+            log(f"steering overhead: {steered:.3f} vs {unsteered:.3f} ms per round (unsteered drafter)")
         if args.calib_copy:
             src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
             dst = torch.empty_like(src)
@@ -312,29 +430,18 @@ def main():
             torch.cuda.synchronize()
             del src, dst
 
-    active = [b for b in range(wl.batch) if not st0[b]["done"]]
-    tokens = sum(st1[b]["produced"] - st0[b]["produced"] for b in range(wl.batch))
-    sec = ms / 1e3
-    tau = tokens / (args.steps * max(1, len(active)))
-    w_b, kvv_b, kvd_b = 0.0, 0.0, 0.0
-    for b in active:
-        t_avg = st0[b]["t"] + (st1[b]["t"] - st0[b]["t"]) * (args.steps - 1) / (2 * args.steps)
-        w, kvv, kvd = round_bytes(wl, t_avg, args.steering)
-        w_b = w
-        kvv_b += kvv
-        kvd_b += kvd
-    bytes_round = w_b + kvv_b + kvd_b
-    ms_round = ms / args.steps
+    tokens = produced * args.steps
+    sec = total_ms / 1e3
+    rsec = sum(round_ms) / 1e3
+    sorted_r = sorted(round_ms)
+    w_tot = sum(w for w, _ in gb) * args.steps
+    kv_tot = sum(kv for _, kv in gb) * args.steps
+    bytes_round = (w_tot + kv_tot) / (nr * args.steps)
+    ms_round = sum(round_ms) / len(round_ms)
+    hbm_frac = (w_tot + kv_tot) / rsec / 1e9 / PEAK_HBM_GBS
+    tau = produced / max(1, sum(sum(a for _, a in rnd) for rnd in rounds))
     # roofline of the dominant kernel: the persistent launches (weights they stream, from the
     # library, plus the KV rows their attention phases read, from the sequence lengths)
-    pr = max(1, args.prof_rounds)
-    kv_prof = 0.0
-    for b in range(wl.batch):
-        if stp0[b]["done"]:
-            continue
-        t_p = stp0[b]["t"] + (stp1[b]["t"] - stp0[b]["t"]) * (pr - 1) / (2 * pr)
-        _, kvv, kvd = round_bytes(wl, t_p)
-        kv_prof += (kvv + kvd) * args.prof_rounds
     p_n, p_ms, p_by = prof[B.PROF_PROGRAM]
     if p_n:
         r_kernel = ("k_mk (persistent launch: one per drafter step, one per verify pass; every projection, "
@@ -344,22 +451,23 @@ def main():
         r_kernel = "k_wsgemv (every weight-streaming projection: QKV, O, gate|up, down, LM heads, W_s)"
         g_n, g_ms, g_by = prof[B.PROF_GEMV]
     gemv_gbs = g_by / (g_ms / 1e3) / 1e9 if g_ms > 0 else 0.0
-    log(f"round: {ms_round:.3f} ms, {bytes_round / 1e9:.3f} GB algorithmic -> "
-        f"{bytes_round / (ms_round / 1e3) / 1e9:.0f} GB/s ({bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS:.1%} of HBM)")
+    npr = max(1, args.prof_generations * nr)
+    log(f"round: {ms_round:.3f} ms mean, {bytes_round / 1e9:.3f} GB algorithmic -> {hbm_frac:.1%} of HBM")
     for c, name in ((B.PROF_PROGRAM, "program"), (B.PROF_GEMV, "gemv"), (B.PROF_ATTN, "attn"),
                     (B.PROF_SAMPLER, "sampler"), (B.PROF_OTHER, "other")):
         n, pms, pby = prof[c]
-        log(f"  {name}: {n / max(1, args.prof_rounds):.0f} launches/round, {pms / max(1, args.prof_rounds):.3f} ms/round"
+        log(f"  {name}: {n / npr:.0f} launches/round, {pms / npr:.3f} ms/round"
             + (f", {pby / (pms / 1e3) / 1e9:.0f} GB/s" if pby and pms else ""))
 
     result = {
-        "metric": "generated tokens/s at 1 GPU (one SD2 round per step)",
+        "metric": "generated tokens/s at 1 GPU (one step = one whole generation: prefill + every SD2 round "
+                  "to new_tokens)",
         "value": tokens / sec,
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_round,
+        "ms_per_step": total_ms / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -372,24 +480,39 @@ def main():
                                f"{wl.verifier.n_kv_heads} F{wl.verifier.d_ff} V{wl.verifier.vocab}",
                    "drafter": f"L{wl.drafter.n_layers} d{wl.drafter.d_model} H{wl.drafter.n_heads}/"
                               f"{wl.drafter.n_kv_heads} F{wl.drafter.d_ff}"},
-        "round_ms_p50": per_round[len(per_round) // 2],
-        "round_ms_p90": per_round[min(len(per_round) - 1, (9 * len(per_round)) // 10)],
-        "prefill_s": prefill_s,
+        "tokens_per_generation": produced,
+        "rounds_per_generation": nr,
+        "decode_tokens_per_s": tokens / rsec,
+        "round_ms_mean": ms_round,
+        "round_ms_p50": sorted_r[len(sorted_r) // 2],
+        "round_ms_p90": sorted_r[min(len(sorted_r) - 1, (9 * len(sorted_r)) // 10)],
+        "prefill_ms_mean": sum(prefill_ms) / len(prefill_ms),
         "block_efficiency": tau,
-        "round_bytes": bytes_round,
-        "round_hbm_frac": bytes_round / (ms_round / 1e3) / 1e9 / PEAK_HBM_GBS,
+        "round_bytes_mean": bytes_round,
+        "round_hbm_frac": hbm_frac,
         "roofline": {"bound": "hbm", "kernel": r_kernel,
                      "achieved": gemv_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gemv_gbs / PEAK_HBM_GBS,
                      "traffic": stored_traffic(wl.name) if p_n and args.steering == "input" else None,
-                     "launches_per_round": g_n / max(1, args.prof_rounds),
+                     "launches_per_round": g_n / npr,
                      "avg_launch_us": g_ms / max(1, g_n) * 1e3,
                      "bytes_per_launch": g_by / max(1, g_n)},
         "cpu_baseline": None,
     }
+    if overhead:
+        result.update(overhead)
     if not args.no_cpu_baseline and args.steering == "input":
         result["cpu_baseline"] = cpu_baseline(wl, host[0], host[1], ws, toks, lens, args.cpu_budget)
-    eng.close()
+    # teardown in order before the interpreter exits: handles, then device tensors, then torch's cache
+    torch.cuda.synchronize()
+    for e in engines:
+        e.close()
+    del eng, engines, models, ws_dev, mlp_dev, t_tok, t_len
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     print(json.dumps(result), flush=True)
+    if args.maps_out:
+        with open("/proc/self/maps") as f, open(args.maps_out, "w") as g:
+            g.write(f.read())
 
 
 if __name__ == "__main__":

@@ -83,7 +83,8 @@ typedef struct {
     int32_t max_new_tokens;        /* generated tokens per sequence; its last round is truncated */
     float temperature;             /* 0 => greedy (argmax drafts, accept iff draft == verifier argmax) */
     uint64_t seed;                 /* Philox4x32-10 key of every random draw */
-    int32_t steering;              /* SD2_STEER_INPUT (sd2_create) or SD2_STEER_MLP (sd2_create_mlp) */
+    int32_t steering;              /* SD2_STEER_INPUT or SD2_STEER_NONE (sd2_create); SD2_STEER_MLP or
+                                      SD2_STEER_MLP_OUT (sd2_create_mlp) */
 } sd2_config;
 
 /* How the drafter is steered by the verifier (sd2_config.steering). */
@@ -97,6 +98,10 @@ typedef struct {
 #define SD2_STEER_MLP_OUT 2 /* the paper's ablation "Inv. bias after MLP" (Sec. Ablation): the same g,
                               and one bias b = W_s g of d_D values added to the output of every
                               drafter MLP (x += W_d(...) + b).  Needs L_V >= 3. */
+#define SD2_STEER_NONE 3   /* no steering: the pretrained drafter the paper compares against (Table 1,
+                              "Pretrained"); no steering projection runs and nothing is added to the
+                              drafter.  Gives the same outputs as SD2_STEER_INPUT with W_s = 0, without
+                              its cost; the baseline of the steering-overhead measurement. */
 
 /* Weights of SD2_STEER_MLP, device pointers in the configuration's dtype, 16-byte aligned. */
 typedef struct {
@@ -113,7 +118,8 @@ size_t sd2_workspace_bytes(const sd2_config* cfg);
 
 /*
  * Create a handle.  verifier/drafter: model weights; w_steer: device [d_drafter][d_verifier]
- * steering projection W_s (s = W_s h, paper Sec. "Verification"/"Drafting");
+ * steering projection W_s (s = W_s h, paper Sec. "Verification"/"Drafting"), ignored (may be
+ * NULL) when cfg->steering is SD2_STEER_NONE;
  * workspace: device buffer of at least sd2_workspace_bytes(cfg) bytes, 256-byte aligned;
  * hip_stream: the hipStream_t every call enqueues on (NULL = default stream).
  * On success *out receives the handle.  Enqueues small table-initialisation kernels.

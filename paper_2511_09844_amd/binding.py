@@ -39,7 +39,7 @@ class Config(ctypes.Structure):
                 ("temperature", ctypes.c_float), ("seed", ctypes.c_uint64), ("steering", ctypes.c_int32)]
 
 
-STEER_INPUT, STEER_MLP, STEER_MLP_OUT = 0, 1, 2
+STEER_INPUT, STEER_MLP, STEER_MLP_OUT, STEER_NONE = 0, 1, 2, 3
 
 
 class MlpSteering(ctypes.Structure):
@@ -147,7 +147,7 @@ class Engine:
 
     With `mlp` (a dict of device tensors w_s, w_hml, ln_gain, ln_bias and a float ln_eps) the
     handle is created by sd2_create_mlp (cfg.steering STEER_MLP or STEER_MLP_OUT) and `w_steer` is
-    unused."""
+    unused; with cfg.steering STEER_NONE (the unsteered drafter) `w_steer` may be None."""
 
     def __init__(self, cfg: Config, verifier: DeviceModel, drafter: DeviceModel, w_steer: torch.Tensor,
                  stream=None, device="cuda", mlp=None):
@@ -167,7 +167,7 @@ class Engine:
         self.h = P()
         if mlp is None:
             rc = lib.sd2_create(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
-                                w_steer.data_ptr(), base + off, nbytes, self.stream.cuda_stream, ctypes.byref(self.h))
+                                w_steer.data_ptr() if w_steer is not None else None, base + off, nbytes, self.stream.cuda_stream, ctypes.byref(self.h))
             check(rc, None, "sd2_create")
         else:
             ms = MlpSteering(mlp["w_s"].data_ptr(), mlp["w_hml"].data_ptr(), mlp["ln_gain"].data_ptr(),

@@ -21,18 +21,38 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the SD2 library needs ROCm's hipcc to build")
 
 
+FLAGS = ["-O3", "-std=c++17", "-fPIC",
+         # packed fp32 instructions are kept out of every kernel
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall"]
+
+
 def build(verbose: bool = False) -> str:
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           # packed fp32 instructions are kept out of every kernel
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-Wall", "-o", SO + ".tmp"] + [os.path.join(HERE, s) for s in SOURCES]
-    res = subprocess.run(cmd, capture_output=True, text=True)
+    """Compile every source to an object in parallel (each object carries its own gfx950 code
+    object; no relocatable device code is needed), then link the shared library."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    cc = hipcc()
+
+    def compile_one(src):
+        obj = os.path.join(objdir, os.path.basename(src).replace(".hip", ".o"))
+        cmd = [cc, f"--offload-arch={ARCH}", *FLAGS, "-c", "-o", obj, os.path.join(HERE, src)]
+        return obj, subprocess.run(cmd, capture_output=True, text=True)
+
+    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+        results = list(ex.map(compile_one, SOURCES))
+    msgs = []
+    for (obj, res), src in zip(results, SOURCES):
+        if res.returncode != 0:
+            raise RuntimeError(f"hipcc failed on {src}:\n" + res.stderr)
+        msgs += [l for l in res.stderr.splitlines() if "packed-fp32-ops' is not a recognized" not in l]
+    link = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", SO + ".tmp"] + [o for o, _ in results]
+    res = subprocess.run(link, capture_output=True, text=True)
     if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + res.stderr)
-    if verbose:
-        msgs = [l for l in res.stderr.splitlines() if "packed-fp32-ops' is not a recognized" not in l]
-        if msgs:
-            print("\n".join(msgs))
+        raise RuntimeError("link failed:\n" + res.stderr)
+    if verbose and msgs:
+        print("\n".join(msgs))
     os.replace(SO + ".tmp", SO)
     return SO
 

@@ -99,7 +99,7 @@ struct ProfEntry {
 struct Engine {
     sd2_config cfg;
     ModelDev mv, md;
-    const void* w_steer;    // SD2_STEER_INPUT: [d_D][d_V]; SD2_STEER_MLP: [L_D*F_D][d_V]
+    const void* w_steer;    // SD2_STEER_INPUT: [d_D][d_V]; SD2_STEER_MLP: [L_D*F_D][d_V]; null: SD2_STEER_NONE
     bool mlp;               // cfg.steering is SD2_STEER_MLP or SD2_STEER_MLP_OUT (taps, W_hml, LayerNorm)
     bool bias_after;        // SD2_STEER_MLP_OUT: the bias joins every drafter MLP's output
     int nbias;              // bias values per sequence: L_D*F_D or d_D

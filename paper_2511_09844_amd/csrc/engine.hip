@@ -52,6 +52,8 @@ bool bf16_dims_ok(const sd2_dims& d) {
            (hd == 32 || hd == 64 || hd == 128);
 }
 
+bool mlp_form(const sd2_config& c);
+
 bool config_ok(const sd2_config* c) {
     if (!c) return false;
     if (!dims_ok(c->verifier) || !dims_ok(c->drafter)) return false;
@@ -65,9 +67,10 @@ bool config_ok(const sd2_config* c) {
     if (c->max_new_tokens < 1) return false;
     if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // 8192 = 64 spans of 128
     if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
-    if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP && c->steering != SD2_STEER_MLP_OUT)
+    if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP && c->steering != SD2_STEER_MLP_OUT &&
+        c->steering != SD2_STEER_NONE)
         return false;
-    if (c->steering != SD2_STEER_INPUT) {
+    if (mlp_form(*c)) {
         // the low tap is block 3; a steering projection runs on the MFMA kernel when its K is a
         // multiple of 256 (bf16), else on the vector kernel, which stages a K row of at most 16384
         const int dV = c->verifier.d_model;
@@ -77,6 +80,9 @@ bool config_ok(const sd2_config* c) {
     }
     return true;
 }
+
+// MLP steering forms (taps, W_hml, LayerNorm, biases in the drafter's MLPs)
+bool mlp_form(const sd2_config& c) { return c.steering == SD2_STEER_MLP || c.steering == SD2_STEER_MLP_OUT; }
 
 // MLP steering: bias values per sequence (per-layer up-projection biases, or one after-MLP bias)
 int bias_len(const sd2_config& c) {
@@ -166,7 +172,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                     if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256 * subs);
                 }
         }
-        if (c.steering != SD2_STEER_INPUT) {
+        if (mlp_form(c)) {
             // W_hml (d_V x 3 d_V) and W_s (bias values x d_V) projections
             int mshapes[2][2] = {{c.verifier.d_model, 3 * c.verifier.d_model}, {bias_len(c), c.verifier.d_model}};
             for (int mm = 1; mm <= std::min(B, 16); ++mm)
@@ -200,7 +206,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         size_t tmax = (size_t)std::max(c.verifier.vocab, c.drafter.vocab) / 16 + 1;
         for (int i = 0; i < 2; ++i)
             tmax = std::max(tmax, (size_t)std::max(dd[i]->d_ff, dd[i]->d_model) / 16 + 1);
-        if (c.steering != SD2_STEER_INPUT) tmax = std::max(tmax, (size_t)bias_len(c) / 16 + 1);
+        if (mlp_form(c)) tmax = std::max(tmax, (size_t)bias_len(c) / 16 + 1);
         tmax = std::max(tmax, pg_cnt);
         w.ws_cnt = cv.take<int32_t>(tmax);
         w.ws_cnt_n = tmax;
@@ -227,7 +233,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         }
         w.attn_cnt = cv.take<int32_t>(gmax);
     }
-    if (c.steering != SD2_STEER_INPUT) {
+    if (mlp_form(c)) {
         const size_t dV = c.verifier.d_model;
         w.taps = cv.take<float>(3 * (size_t)maxm * dV);
         w.tapsel = cv.take<float>((size_t)B * 3 * dV);
@@ -341,7 +347,7 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
         if (err != hipSuccess) { e.launch_err = err; return; }
         launch_verify_decide(s, e, out_tokens, out_counts);
         if (e.mlp) launch_mlp_steer(e, e.mk.tap_x, e.ws.steer_map, B);
-        else launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
+        else if (e.w_steer) launch_steer(e, e.mk.final_x, e.mk.final_ss, e.ws.steer_map, B);
         return;
     }
     const int ub_ld = e.nbias;
@@ -367,7 +373,7 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
         const size_t slot = (size_t)e.maxm * e.mv.dm.d_model;
         const float* src[3] = {e.ws.taps, e.ws.taps + slot, e.ws.taps + 2 * slot};
         launch_mlp_steer(e, src, e.ws.steer_map, B);
-    } else {
+    } else if (e.w_steer) {
         launch_steer(e, e.mv.x, e.mv.ss, e.ws.steer_map, B);
     }
 }
@@ -446,12 +452,13 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     if (!out) return SD2_ERR_INVALID_ARG;
     *out = nullptr;
     if (!config_ok(cfg)) return SD2_ERR_INVALID_ARG;
-    if ((cfg->steering != SD2_STEER_INPUT) != (mlp != nullptr)) return SD2_ERR_INVALID_ARG;
+    if (mlp_form(*cfg) != (mlp != nullptr)) return SD2_ERR_INVALID_ARG;
     if (mlp && (!aligned16(mlp->w_hml) || !aligned16(mlp->ln_gain) || !aligned16(mlp->ln_bias) ||
                 !(mlp->ln_eps >= 0.f)))
         return SD2_ERR_INVALID_ARG;
-    if (!weights_ok(verifier, cfg->verifier) || !weights_ok(drafter, cfg->drafter) || !aligned16(w_steer))
-        return SD2_ERR_INVALID_ARG;
+    if (!weights_ok(verifier, cfg->verifier) || !weights_ok(drafter, cfg->drafter)) return SD2_ERR_INVALID_ARG;
+    const bool unsteered = cfg->steering == SD2_STEER_NONE;
+    if (!unsteered && !aligned16(w_steer)) return SD2_ERR_INVALID_ARG;
     if (!workspace || ((uintptr_t)workspace % kAlign) != 0) return SD2_ERR_INVALID_ARG;
     size_t need = sd2_workspace_bytes(cfg);
     if (workspace_bytes < need) return SD2_ERR_INVALID_ARG;
@@ -470,7 +477,7 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     e->cap = cfg->max_seq_len;
     e->bf16 = cfg->dtype == SD2_BF16;
     e->stream = (hipStream_t)hip_stream;
-    e->w_steer = w_steer;
+    e->w_steer = unsteered ? nullptr : w_steer;
     e->mlp = mlp != nullptr;
     e->bias_after = cfg->steering == SD2_STEER_MLP_OUT;
     e->nbias = bias_len(*cfg);
@@ -564,7 +571,7 @@ sd2_status sd2_prefill(sd2_handle_t h, int32_t batch, const int32_t* tokens, con
     // the first round's steering from position len-2 (a one-token prompt gets none: the finish
     // step below clears it)
     if (e->mlp) launch_mlp_steer(*e, nullptr, nullptr, batch);
-    else launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, nullptr, batch);
+    else if (e->w_steer) launch_steer(*e, e->ws.hcap, e->ws.hcap_ss, nullptr, batch);
     for (int c = 0; c < nchunks; ++c) {
         launch_plan_embed(s, *e, e->md, kPlanPrefill, c, rows, tokens, lens, max_prompt, chunk);
         for (int l = 0; l < e->md.dm.n_layers; ++l) launch_layer(s, *e, e->md, l, rows, chunk);

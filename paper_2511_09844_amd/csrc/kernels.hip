@@ -133,7 +133,7 @@ void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, i
     a.t = e.ws.t; a.len_d = e.ws.len_d; a.done = e.ws.done; a.hist = e.ws.hist; a.drafts = e.ws.drafts;
     a.prompt_tok = prompt_tok; a.prompt_len = prompt_len;
     a.steer = e.ws.steer;
-    a.add_steer = !e.mlp && (&m == &e.md) && (kind == kPlanDraft1 || kind == kPlanDraftJ);
+    a.add_steer = !e.mlp && e.w_steer && (&m == &e.md) && (kind == kPlanDraft1 || kind == kPlanDraftJ);
     a.row_pos = e.ws.row_pos; a.row_seq = e.ws.row_seq; a.x = m.x; a.ss = m.ss; a.embed = m.embed;
     prof_begin(&e, kProfOther, 0.0);
     if (e.bf16) k_plan_embed<uint16_t><<<rows, 256, 0, s>>>(a);

@@ -1510,7 +1510,8 @@ hipError_t mk_launch(Engine& e, int j) {
     a.steer = e.ws.steer;
     a.embed = (const uint16_t*)m.embed;
     a.vocab = m.dm.vocab;
-    a.add_steer = ver || e.mlp ? 0 : 1;  // MLP steering biases the up projections instead
+    // MLP steering biases the up projections instead; an unsteered drafter adds nothing
+    a.add_steer = ver || e.mlp || !e.w_steer ? 0 : 1;
     a.kc = m.kc;
     a.vc = m.vc;
     a.rcos = m.rope_cos;

@@ -50,22 +50,28 @@ class Stats:
 
 
 def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check_logits=True, log=print,
-               expect_path=None, separate_kernels=False, mlp=None):
+               expect_path=None, separate_kernels=False, mlp=None, unsteered=False):
     """Run prefill + rounds on both sides; assert parity; return Stats.
 
     expect_path: 0 (one kernel per operation) or 1 (one persistent launch per drafter step and
     verify pass) -- the execution path the library must have chosen; separate_kernels forces 0.
     mlp: host weights of the MLP steering form (sd2_inputs.mlp_steer_weights); the per-layer
-    up-projection biases are then compared where the steering vector is otherwise."""
+    up-projection biases are then compared where the steering vector is otherwise.
+    unsteered: the library runs the unsteered drafter (SD2_STEER_NONE), the oracle W_s = 0."""
     if wv is None:
         wv, wd, ws = si.model_weights(wl, 0), si.model_weights(wl, 1), si.steer_weights(wl)
+    if unsteered:
+        ws = np.zeros_like(ws)
     tol = TOL[wl.dtype]
     toks, lens = si.prompts(wl)
     seqs = list(range(wl.batch)) if seqs is None else list(seqs)
     o = oracle.Oracle(wl, wv, wd, ws, mlp=mlp)
     o.prefill(toks, lens, seqs)
     dv, dd = device_model(wl, 0, wv), device_model(wl, 1, wd)
-    if mlp is None:
+    if unsteered:
+        ws_dev = None
+        eng = B.Engine(B.config_of(wl, steering=B.STEER_NONE), dv, dd, None)
+    elif mlp is None:
         ws_dev = B.to_device(ws)
         eng = B.Engine(B.config_of(wl), dv, dd, ws_dev)
     else:
@@ -172,3 +178,88 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
     torch.cuda.empty_cache()
     log(f"[parity] {wl.name}: {st}")
     return st
+
+
+def free_run(wl, wv=None, wd=None, ws=None, seqs=None, expect_path=None, separate_kernels=False, min_rounds=3,
+             log=print):
+    """Both sides run free: the library's own sd2_round (no forced decisions, the path the
+    benchmark times) against the oracle's own rounds on the same seeded inputs.
+
+    A sequence is compared round by round -- emitted tokens, counts, cache lengths exactly;
+    logits and steering vector within the dtype's tolerance -- until its first round in which
+    some decision the oracle took has a margin of at most MARGIN.  From there the two
+    trajectories may legitimately differ, so that sequence is followed no further.  Returns
+    (rounds compared per sequence, Stats)."""
+    if wv is None:
+        wv, wd, ws = si.model_weights(wl, 0), si.model_weights(wl, 1), si.steer_weights(wl)
+    tol = TOL[wl.dtype]
+    toks, lens = si.prompts(wl)
+    seqs = list(range(wl.batch)) if seqs is None else list(seqs)
+    o = oracle.Oracle(wl, wv, wd, ws)
+    o.prefill(toks, lens, seqs)
+    dv, dd = device_model(wl, 0, wv), device_model(wl, 1, wd)
+    ws_dev = B.to_device(ws)
+    eng = B.Engine(B.config_of(wl), dv, dd, ws_dev)
+    old = os.environ.pop("SD2_NO_MK", None)
+    if separate_kernels:
+        os.environ["SD2_NO_MK"] = "1"
+    try:
+        eng.prefill(torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(), wl.max_prompt)
+    finally:
+        os.environ.pop("SD2_NO_MK", None)
+        if old is not None:
+            os.environ["SD2_NO_MK"] = old
+    path = int(eng.debug(B.DBG_PATH)[0])
+    log(f"[free] {wl.name}: execution path {path}")
+    if expect_path is not None:
+        assert path == expect_path, f"execution path {path}, expected {expect_path}"
+    st = Stats()
+    compared = {b: 0 for b in seqs}
+    following = set(seqs)
+    k = wl.k
+    while following:
+        live = [b for b in following if not o.state(b)["done"]]
+        if not live:
+            break
+        outs, logs, dumps = {}, {}, {}
+        for b in live:
+            outs[b], logs[b], dumps[b] = o.round_one(b, dump=True)
+        ot, oc = eng.round()
+        ot, oc = ot.cpu().numpy(), oc.cpu().numpy()
+        lv, ld = eng.debug(B.DBG_LOGITS_V), eng.debug(B.DBG_LOGITS_D)
+        sg = eng.debug(B.DBG_STEER)
+        state = eng.state()
+        for b in live:
+            lg = logs[b]
+            margins = list(lg.draft_margin[:k]) + [lg.final_margin]
+            margins += [lg.accept_margin[i] for i in range(min(lg.n + 1, k))]
+            st.decisions += len(margins)
+            if min(margins) <= MARGIN:
+                # a near-tie: the library may take the other branch from here on
+                st.unpinned += 1
+                following.discard(b)
+                continue
+            st.pinned += len(margins)
+            where = f"free round {compared[b]} seq {b}"
+            assert oc[b] == lg.count, f"{where}: count {oc[b]} vs {lg.count}"
+            assert list(ot[b, : lg.count]) == list(outs[b]), f"{where}: tokens {ot[b, :lg.count]} vs {outs[b]}"
+            ost = o.state(b)
+            for key in ("t", "len_v", "len_d", "produced", "done"):
+                assert state[b][key] == ost[key], f"{where}: state {key} {state[b][key]} vs {ost[key]}"
+            ev = float(np.abs(lv[b] - dumps[b]["logits_v"]).max())
+            ed = float(np.abs(ld[b] - dumps[b]["logits_d"]).max())
+            es = float(np.abs(sg[b] - o.steer_vec(b)).max())
+            st.max_err_v, st.max_err_d, st.max_err_s = max(st.max_err_v, ev), max(st.max_err_d, ed), max(st.max_err_s, es)
+            assert ev <= tol and ed <= tol and es <= tol, f"{where}: errors v={ev} d={ed} s={es}"
+            compared[b] += 1
+            st.tokens += int(lg.count)
+        st.rounds += 1
+    assert int(eng.debug(B.DBG_PATH)[1]) == 0, "a persistent launch timed out at a grid barrier"
+    eng.close()
+    del eng, dv, dd, ws_dev
+    torch.cuda.empty_cache()
+    log(f"[free] {wl.name}: compared rounds {compared} {st}")
+    # how far the comparison reaches is a property of the oracle's own trajectory (where its first
+    # near-tie falls), fixed by the seed; the tests choose inputs that reach several rounds
+    assert sum(compared.values()) >= min_rounds, f"only {compared} rounds compared before near-ties"
+    return compared, st

@@ -73,3 +73,27 @@ MK5 = Workload(
     name="mk-many-attention-units", verifier=Dims(1, 2048, 32, 8, 1024, 2048, 5e5),
     drafter=Dims(1, 1024, 16, 8, 1024, 2048, 5e5),
     dtype="bf16", k=5, batch=1, prompt=(730, 730), new_tokens=8, temperature=1.0, seed=17)
+# Head dim 128 at long contexts (the verify pass's attention at the 8B verifier's head shape):
+# 16 query / 4 KV heads, prompts of 629 and 1114 tokens.  Persistent path: 10 and 18 live spans of
+# 64 positions, so the last-arriver fold runs its second batch of 16 (span partials of 12 rows
+# x 16 heads x 19 spans are 1.9 MB, above the size the O projection merges itself); per-operation
+# path: 5 and 9 spans of 128 merged by the last span workgroup.
+MK6 = Workload(
+    name="mk-hd128-long", verifier=Dims(1, 2048, 16, 4, 2048, 4096, 5e5),
+    drafter=Dims(1, 1024, 16, 8, 1024, 4096, 5e5),
+    dtype="bf16", k=5, batch=2, prompt=(512, 1160), new_tokens=24, temperature=1.0, seed=21)
+# The batched workload's structure at a depth the float64 oracle affords: 16 sequences with
+# prompts drawn from [256, 2048] (257 ... 1992 tokens), k = 7, T = 0.7, head dim 128 verifier and
+# head dim 64 drafter; 128 verify rows per round, so the per-operation path runs it.
+RAG16 = Workload(
+    name="ragged-16-long", verifier=Dims(1, 1024, 8, 2, 2048, 4096, 5e5),
+    drafter=Dims(1, 512, 8, 2, 1024, 4096, 5e5),
+    dtype="bf16", k=7, batch=16, prompt=(256, 2048), new_tokens=16, temperature=0.7, seed=42)
+RAG16_SHORTEST, RAG16_LONGEST = 1, 8
+
+
+def scaled_set(wl, scale):
+    """Verifier, drafter and W_s all drawn with standard deviation `scale`: wider logit gaps, so
+    that fewer greedy decisions are near-ties."""
+    ws = si.normal((wl.drafter.d_model, wl.verifier.d_model), wl.dtype, wl.seed, si.tensor_id(2, 0, "w_s"), scale)
+    return scaled_weights(wl, 0, scale), scaled_weights(wl, 1, scale), ws

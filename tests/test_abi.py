@@ -90,7 +90,7 @@ def test_struct_layouts_match_the_header(tmp_path):
 
 def test_mlp_steering_configs():
     """The MLP form needs a verifier of at least 3 layers (block 3 is the low tap) and sizes its
-    extra buffers; an unknown steering form is rejected."""
+    extra buffers; the unsteered form sizes none; an unknown steering form is rejected."""
     lib = B.load()
     for wl in si.PRESETS[:4]:
         base = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl)))
@@ -101,7 +101,11 @@ def test_mlp_steering_configs():
         base = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl)))
         after = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl, steering=B.STEER_MLP_OUT)))
         assert after >= base + wl.batch * wl.drafter.d_model * 4
-    c = B.config_of(si.TINY, steering=3)
+    for wl in si.PRESETS[:4]:
+        # the unsteered drafter needs exactly the input form's workspace
+        base = lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl)))
+        assert lib.sd2_workspace_bytes(ctypes.byref(B.config_of(wl, steering=B.STEER_NONE))) == base
+    c = B.config_of(si.TINY, steering=4)
     assert lib.sd2_workspace_bytes(ctypes.byref(c)) == 0
     c = B.config_of(si.TINY, steering=B.STEER_MLP)
     c.verifier.n_layers = 2
