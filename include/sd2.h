@@ -132,6 +132,26 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
                       sd2_handle_t* out);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, serving loops
+ * and harnesses that forbid hipMalloc): sd2_create with the workspace taken from a static device
+ * array of the library instead of the caller.  Allocates nothing, on host or device: the array
+ * (SD2_NOALLOC_WORKSPACE_BYTES per GPU) is part of the library's code object, reserved on every
+ * GPU the library runs on until the process ends, and the handle's host state sits in a static
+ * slot of that GPU.  cfg->steering must be SD2_STEER_INPUT or SD2_STEER_NONE; the other arguments
+ * are as sd2_create's, and the handle is used and destroyed the same way.
+ * Limits and errors: SD2_ERR_CAPACITY when sd2_workspace_bytes(cfg) exceeds
+ * SD2_NOALLOC_WORKSPACE_BYTES (checked before any device call); one such handle per GPU at a
+ * time: SD2_ERR_STATE while another one on the current device is alive.  The array keeps the
+ * previous handle's contents; creation clears what this handle uses with a kernel (no
+ * hipMemsetAsync) on hip_stream, and sd2_destroy of such a handle waits for its stream, so the
+ * next handle never clears memory still in use.  Work of a handle from this entry point and any
+ * other user of the same array must not overlap on one GPU: they would race on it.
+ */
+#define SD2_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+sd2_status sd2_create_noalloc(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                              const void* w_steer, void* hip_stream, sd2_handle_t* out);
+
+/*
  * Create a handle whose drafter is steered by the paper's MLP biases (eq. (2); Sec.
  * "Verification" and "Drafting"): cfg->steering must be SD2_STEER_MLP (or SD2_STEER_MLP_OUT, the
  * ablation with one bias after every MLP).  Everything else is as

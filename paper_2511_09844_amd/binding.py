@@ -18,7 +18,7 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "capacity", -3: "state", -4: "hip
 DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V, DBG_PATH, \
     DBG_TRACE, DBG_UBIAS = range(1, 13)
 
-EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_create_mlp", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
+EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_create_noalloc", "sd2_create_mlp", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
            "sd2_status_string", "sd2_last_error", "sd2_debug_read", "sd2_profile", "sd2_profile_read"]
 PROF_GEMV, PROF_ATTN, PROF_SAMPLER, PROF_OTHER, PROF_PROGRAM = 1, 2, 3, 4, 5
 
@@ -61,6 +61,9 @@ def load():
         lib.sd2_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights), P, P,
                                    ctypes.c_size_t, P, ctypes.POINTER(P)]
         lib.sd2_create.restype = ctypes.c_int32
+        lib.sd2_create_noalloc.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights),
+                                           P, P, ctypes.POINTER(P)]
+        lib.sd2_create_noalloc.restype = ctypes.c_int32
         lib.sd2_create_mlp.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights),
                                        ctypes.POINTER(MlpSteering), P, ctypes.c_size_t, P, ctypes.POINTER(P)]
         lib.sd2_create_mlp.restype = ctypes.c_int32
@@ -150,7 +153,7 @@ class Engine:
     unused; with cfg.steering STEER_NONE (the unsteered drafter) `w_steer` may be None."""
 
     def __init__(self, cfg: Config, verifier: DeviceModel, drafter: DeviceModel, w_steer: torch.Tensor,
-                 stream=None, device="cuda", mlp=None):
+                 stream=None, device="cuda", mlp=None, noalloc=False):
         lib = load()
         self.lib = lib
         self.cfg = cfg
@@ -161,21 +164,30 @@ class Engine:
         nbytes = lib.sd2_workspace_bytes(ctypes.byref(cfg))
         if nbytes == 0:
             raise Sd2Error("invalid configuration")
-        self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
-        base = self.workspace.data_ptr()
-        off = (-base) % 256
         self.h = P()
-        if mlp is None:
-            rc = lib.sd2_create(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
-                                w_steer.data_ptr() if w_steer is not None else None, base + off, nbytes, self.stream.cuda_stream, ctypes.byref(self.h))
-            check(rc, None, "sd2_create")
+        self.workspace = None
+        ws_ptr = w_steer.data_ptr() if w_steer is not None else None
+        if noalloc:
+            # the library's static workspace (sd2_create_noalloc): nothing is allocated here
+            assert mlp is None
+            rc = lib.sd2_create_noalloc(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
+                                        ws_ptr, self.stream.cuda_stream, ctypes.byref(self.h))
+            check(rc, None, "sd2_create_noalloc")
         else:
-            ms = MlpSteering(mlp["w_s"].data_ptr(), mlp["w_hml"].data_ptr(), mlp["ln_gain"].data_ptr(),
-                             mlp["ln_bias"].data_ptr(), float(mlp["ln_eps"]))
-            rc = lib.sd2_create_mlp(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
-                                    ctypes.byref(ms), base + off, nbytes, self.stream.cuda_stream,
-                                    ctypes.byref(self.h))
-            check(rc, None, "sd2_create_mlp")
+            self.workspace = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+            base = self.workspace.data_ptr()
+            off = (-base) % 256
+            if mlp is None:
+                rc = lib.sd2_create(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w), ws_ptr,
+                                    base + off, nbytes, self.stream.cuda_stream, ctypes.byref(self.h))
+                check(rc, None, "sd2_create")
+            else:
+                ms = MlpSteering(mlp["w_s"].data_ptr(), mlp["w_hml"].data_ptr(), mlp["ln_gain"].data_ptr(),
+                                 mlp["ln_bias"].data_ptr(), float(mlp["ln_eps"]))
+                rc = lib.sd2_create_mlp(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
+                                        ctypes.byref(ms), base + off, nbytes, self.stream.cuda_stream,
+                                        ctypes.byref(self.h))
+                check(rc, None, "sd2_create_mlp")
         self.batch = 0
         k = cfg.k
         self.out_tokens = torch.zeros((cfg.max_batch, k + 1), dtype=torch.int32, device=device)

@@ -124,7 +124,12 @@ struct Engine {
     int prof_n;
     ProfEntry* prof;
     MkState mk;  // persistent round-program path (used when active)
+    bool static_slot;   // created by sd2_create_noalloc: workspace and this object are static
+    int static_device;  // its device
 };
+
+// Size of the static device workspace of sd2_create_noalloc (per GPU).
+constexpr size_t kStaticWorkspaceBytes = SD2_NOALLOC_WORKSPACE_BYTES;
 
 // Bracket one launch with timing events when profiling is enabled (no-op otherwise).
 void prof_begin(Engine* e, int cls, double bytes);

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 
 #include "engine.h"
@@ -413,6 +414,37 @@ sd2_status run_round(Engine* e, int32_t* out_tokens, int32_t* out_counts) {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------------------------
+// Workspace that needs no allocation (sd2_create_noalloc): a static device array, one copy per
+// GPU, held from the library's load until the process ends.  In host code `scratch` names a
+// host-side stand-in, not the device copy: its device address on each GPU comes from
+// hipGetSymbolAddress (once per device, with that device current), and only that address is
+// ever handed to kernels.  One handle at a time per device uses it; the handle's host state
+// lives in the same per-device slot, so creating it allocates nothing on host or device.
+// ---------------------------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[kStaticWorkspaceBytes];
+
+namespace {
+
+constexpr int kStaticMaxDevices = 64;
+
+struct StaticSlot {
+    void* ptr;    // device address of `scratch` on this device (null until first looked up)
+    bool live;    // a handle created by sd2_create_noalloc uses it
+    Engine engine;
+};
+StaticSlot g_static[kStaticMaxDevices];
+std::mutex g_static_mu;
+
+// Clears n bytes (a multiple of 16) with vector stores: a kernel rather than hipMemsetAsync, so
+// that a caller may capture the creation into a graph.
+__global__ void k_zero16(uint4* p, size_t n16) {
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) p[i] = make_uint4(0, 0, 0, 0);
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t sd2_workspace_bytes(const sd2_config* cfg) {
@@ -424,7 +456,7 @@ const char* sd2_status_string(sd2_status s) {
     switch (s) {
         case SD2_OK: return "ok";
         case SD2_ERR_INVALID_ARG: return "invalid argument";
-        case SD2_ERR_CAPACITY: return "capacity exceeded (max_seq_len)";
+        case SD2_ERR_CAPACITY: return "capacity exceeded (max_seq_len, or sd2_create_noalloc's static workspace)";
         case SD2_ERR_STATE: return "invalid state (prefill first)";
         case SD2_ERR_HIP: return "HIP runtime error";
         case SD2_ERR_UNSUPPORTED: return "unsupported";
@@ -446,9 +478,11 @@ static bool weights_ok(const sd2_weights* w, const sd2_dims& d) {
     return true;
 }
 
+// slot: the per-device static slot whose Engine and workspace to use (sd2_create_noalloc), or null
 static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
                               const void* w_steer, const sd2_mlp_steering* mlp, void* workspace,
-                              size_t workspace_bytes, void* hip_stream, sd2_handle_t* out) {
+                              size_t workspace_bytes, void* hip_stream, sd2_handle_t* out,
+                              StaticSlot* slot = nullptr) {
     if (!out) return SD2_ERR_INVALID_ARG;
     *out = nullptr;
     if (!config_ok(cfg)) return SD2_ERR_INVALID_ARG;
@@ -471,8 +505,15 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
         if (strncmp(prop.gcnArchName, "gfx950", 6) != 0 || strstr(prop.gcnArchName, "xnack+") != nullptr)
             return SD2_ERR_UNSUPPORTED;
     }
-    Engine* e = new (std::nothrow) Engine();
-    if (!e) return SD2_ERR_INVALID_ARG;
+    Engine* e = nullptr;
+    if (slot) {
+        slot->engine = Engine{};
+        e = &slot->engine;
+        e->static_slot = true;
+    } else {
+        e = new (std::nothrow) Engine();
+        if (!e) return SD2_ERR_INVALID_ARG;
+    }
     e->cfg = *cfg;
     e->cap = cfg->max_seq_len;
     e->bf16 = cfg->dtype == SD2_BF16;
@@ -508,13 +549,20 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     hipError_t err = wsgemv_setup();
     if (err != hipSuccess) {
         sd2_status st = hip_fail(e, err, "hipFuncSetAttribute");
-        delete e;
+        if (!slot) delete e;
         return st;
     }
-    err = hipMemsetAsync(workspace, 0, need, e->stream);
+    if (slot) {
+        // the static workspace keeps the previous handle's contents: clear it with a kernel
+        const size_t n16 = (need + 15) / 16;
+        k_zero16<<<(unsigned)std::min<size_t>(4096, (n16 + 255) / 256), 256, 0, e->stream>>>((uint4*)workspace, n16);
+        err = hipGetLastError();
+    } else {
+        err = hipMemsetAsync(workspace, 0, need, e->stream);
+    }
     if (err != hipSuccess) {
-        sd2_status st = hip_fail(e, err, "hipMemsetAsync");
-        delete e;
+        sd2_status st = hip_fail(e, err, slot ? "k_zero16" : "hipMemsetAsync");
+        if (!slot) delete e;
         return st;
     }
     launch_rope_table(e->stream, e->mv, e->cap);
@@ -523,7 +571,7 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     mk_init_buffers(*e);
     sd2_status st = check_launch(e, "create");
     if (st != SD2_OK) {
-        delete e;
+        if (!slot) delete e;
         return st;
     }
     *out = reinterpret_cast<sd2_handle_t>(e);
@@ -534,6 +582,34 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
                       const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
                       sd2_handle_t* out) {
     return create_impl(cfg, verifier, drafter, w_steer, nullptr, workspace, workspace_bytes, hip_stream, out);
+}
+
+sd2_status sd2_create_noalloc(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
+                              const void* w_steer, void* hip_stream, sd2_handle_t* out) {
+    if (!out) return SD2_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (!config_ok(cfg) || mlp_form(*cfg)) return SD2_ERR_INVALID_ARG;
+    const size_t need = sd2_workspace_bytes(cfg);
+    if (need > kStaticWorkspaceBytes) return SD2_ERR_CAPACITY;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return SD2_ERR_HIP;
+    if (dev < 0 || dev >= kStaticMaxDevices) return SD2_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    StaticSlot& slot = g_static[dev];
+    if (slot.live) return SD2_ERR_STATE;
+    if (!slot.ptr) {
+        // the device copy's address on this device (the current one)
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return SD2_ERR_HIP;
+        slot.ptr = p;
+    }
+    sd2_status st = create_impl(cfg, verifier, drafter, w_steer, nullptr, slot.ptr, kStaticWorkspaceBytes,
+                                hip_stream, out, &slot);
+    if (st == SD2_OK) {
+        slot.live = true;
+        slot.engine.static_device = dev;
+    }
+    return st;
 }
 
 sd2_status sd2_create_mlp(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,
@@ -618,6 +694,14 @@ sd2_status sd2_destroy(sd2_handle_t h) {
             if (e->prof[i].b) (void)hipEventDestroy(e->prof[i].b);
         }
         delete[] e->prof;
+        e->prof = nullptr;
+    }
+    if (e->static_slot) {
+        // the next handle on this device clears the same memory: let this one's work finish first
+        (void)hipStreamSynchronize(e->stream);
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        g_static[e->static_device].live = false;
+        return SD2_OK;
     }
     delete e;
     return SD2_OK;

@@ -122,3 +122,15 @@ def test_create_mlp_rejects_bad_arguments_without_gpu():
     ms = B.MlpSteering(None, None, None, None, 1e-5)
     c0 = B.config_of(si.TINY)
     assert lib.sd2_create_mlp(ctypes.byref(c0), None, None, ctypes.byref(ms), None, 0, None, ctypes.byref(h)) == -1
+
+
+def test_create_noalloc_argument_errors_without_gpu():
+    """Checked before any device call: a workspace larger than the static array, MLP forms."""
+    lib = B.load()
+    h = B.P()
+    assert lib.sd2_workspace_bytes(ctypes.byref(B.config_of(si.LLAMA8B))) > (64 << 20)
+    assert lib.sd2_create_noalloc(ctypes.byref(B.config_of(si.LLAMA8B)), None, None, None, None,
+                                  ctypes.byref(h)) == -2
+    c = B.config_of(si.TINY, steering=B.STEER_MLP)
+    assert lib.sd2_create_noalloc(ctypes.byref(c), None, None, None, None, ctypes.byref(h)) == -1
+    assert lib.sd2_create_noalloc(ctypes.byref(B.config_of(si.TINY)), None, None, None, None, None) == -1
