@@ -54,7 +54,7 @@ def _load():
         lib.oracle_create.restype = P
         lib.oracle_create.argtypes = [P, P, P, P, ctypes.c_int, P, P, P, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int, ctypes.c_int, f32, u64, ctypes.c_int, P, P, P,
-                                      ctypes.c_double]
+                                      ctypes.c_double, P, P, ctypes.c_int]
         lib.oracle_destroy.argtypes = [P]
         lib.oracle_prefill_one.argtypes = [P, ctypes.c_int, P, ctypes.c_int]
         lib.oracle_prefill_one.restype = ctypes.c_int
@@ -70,6 +70,7 @@ def _load():
         lib.oracle_get_ubias.argtypes = [P, ctypes.c_int, P]
         lib.oracle_forward_mlp.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P]
         lib.oracle_mlp_steer.argtypes = [P, P, P]
+        lib.oracle_forward_cond.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P]
         lib.oracle_philox.argtypes = [P, u32, u32, P]
         lib.oracle_uniform.argtypes = [u32]
         lib.oracle_uniform.restype = f32
@@ -142,8 +143,9 @@ class Oracle:
     ``ws`` is W_s [d_D][d_V]; arrays must stay alive (they are referenced).
     ``mlp`` selects the MLP steering of eq. (2) instead: a dict as returned by
     ``sd2_inputs.mlp_steer_weights`` (w_s [L_D*F_D][d_V], w_hml [d_V][3 d_V],
-    ln_gain, ln_bias, ln_eps; form 2, the bias after every MLP: w_s [d_D][d_V]);
-    ``ws`` is then ignored.
+    ln_gain, ln_bias, ln_eps; form 2, the bias after every MLP: w_s [d_D][d_V];
+    form 3, the conditional bias: w_s = V^g [L_D*R][d_V], w_cf = V^f [L_D*R][d_D],
+    w_cu = U [L_D*F_D][R], rank R); ``ws`` is then ignored.
     """
 
     def __init__(self, wl, wv, wd, ws, max_batch=None, cap=None, temperature=None, k=None, max_new=None,
@@ -171,6 +173,12 @@ class Oracle:
             form = int(mlp.get("form", 1))
             extra = (mlp["w_hml"].ctypes.data, mlp["ln_gain"].ctypes.data, mlp["ln_bias"].ctypes.data,
                      float(mlp["ln_eps"]))
+            if form == 3:
+                for key in ("w_cf", "w_cu"):
+                    assert mlp[key].flags["C_CONTIGUOUS"]
+                extra += (mlp["w_cf"].ctypes.data, mlp["w_cu"].ctypes.data, int(mlp["rank"]))
+        if len(extra) == 4:
+            extra += (None, None, 0)
         self.h = lib.oracle_create(self._dv.ctypes.data, self._rv.ctypes.data, self._dd.ctypes.data,
                                    self._rd.ctypes.data, 1 if wl.dtype == "bf16" else 0, self._pv, self._pd,
                                    self._ws.ctypes.data, self.k, self.max_batch, self.cap, self.max_new,
@@ -262,11 +270,15 @@ class Oracle:
 
     def _bias_shape(self):
         dm = self.wl.drafter
-        return (dm.n_layers, dm.d_ff) if int(self.mlp.get("form", 1)) == 1 else (dm.d_model,)
+        form = int(self.mlp.get("form", 1))
+        if form == 3:
+            return (dm.n_layers, int(self.mlp["rank"]))
+        return (dm.n_layers, dm.d_ff) if form == 1 else (dm.d_model,)
 
     def ubias(self, b):
         """MLP steering: the biases of sequence b for its next round: per-layer up-projection
-        biases [L_D][F_D] (form 1) or the bias after every MLP [d_D] (form 2)."""
+        biases [L_D][F_D] (form 1), the bias after every MLP [d_D] (form 2), or the g parts
+        V_l^g g of the conditional biases [L_D][R] (form 3)."""
         out = np.zeros(self._bias_shape(), dtype=np.float64)
         self.lib.oracle_get_ubias(self.h, b, out.ctypes.data)
         return out
@@ -300,3 +312,19 @@ class Oracle:
         ub = np.zeros(self._bias_shape(), dtype=np.float64)
         self.lib.oracle_mlp_steer(self.h, z.ctypes.data, ub.ctypes.data)
         return ub
+
+    def forward_cond(self, which, toks, c=None):
+        """Whole-sequence forward with the conditional MLP bias of form 3 on every row, for the g
+        whose parts V_l^g g are c [L][R] (None: no bias); returns (hF [n][d], logits [n][V])."""
+        dm = self.wl.verifier if which == 0 else self.wl.drafter
+        toks = np.ascontiguousarray(toks, dtype=np.int32)
+        n = len(toks)
+        hF = np.zeros((n, dm.d_model), dtype=np.float64)
+        lg = np.zeros((n, dm.vocab), dtype=np.float64)
+        cp = None
+        if c is not None:
+            c = np.ascontiguousarray(c, dtype=np.float64)
+            assert c.shape == (dm.n_layers, int(self.mlp["rank"]))
+            cp = c.ctypes.data
+        self.lib.oracle_forward_cond(self.h, which, toks.ctypes.data, n, cp, hF.ctypes.data, lg.ctypes.data)
+        return hF, lg

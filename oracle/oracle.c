@@ -47,6 +47,14 @@
  *   - the ablation "Inv. bias after MLP" (Sec. "Ablation", the simplest of the
  *     three steering mechanisms compared there): the same g, and one bias
  *     W_s g of d_model values added to the output of every drafter MLP.
+ *   - the ablation "Cond. bias in MLP" (same paragraph: the bias depends on
+ *     g and on the previous layer's output): a two-layer MLP per drafter
+ *     layer l, b = U_l SiLU(V_l [f; g]), where f is the residual stream that
+ *     enters layer l (the output of layer l-1; the embedding for l = 0) at the
+ *     token's own position, V_l [R][d_D + d_V] and U_l [d_ff][R]; b is added to
+ *     the up projection as in eq. (2).  V_l [f; g] = V_l^f f + V_l^g g: the
+ *     g part is computed once per round (like eq. (2)'s bias), the f part per
+ *     token and layer.
  *   - greedy regime (T = 0): argmax drafts, accept iff the draft equals the
  *     verifier's argmax, final token = verifier argmax (Sec. "Decoding
  *     Parameters").
@@ -189,20 +197,31 @@ static void tap_layers(int L, int out[3]) {
     out[2] = 2;
 }
 
+/* Conditional bias in the MLP: per layer l, b = U_l SiLU(Vf_l f + c_l) with
+ * c_l = Vg_l g precomputed for the round (rows l*R .. (l+1)*R-1 of c). */
+typedef struct {
+    const void* vf;            /* [L*R][d]: V_l^f, the columns of V_l that multiply f */
+    const void* u;             /* [L*d_ff][R]: U_l */
+    int rank;                  /* R */
+    const double* c;           /* [L*R]: V_l^g g for this sequence and round */
+} ocond;
+
 /*
  * Forward of m consecutive tokens at positions pos0..pos0+m-1 of one sequence
  * whose cache holds positions 0..pos0-1.  `add` (d doubles, may be NULL) is
  * added to every input embedding (the steering injection).  `ubias` (NULL for
  * none) holds one bias of d_ff values per layer, added to the up projection
  * before the gating product (eq. (2)); `obias` (d values, NULL for none) is
- * added to the output of every layer's MLP.  `taps` (NULL for none) receives, per
+ * added to the output of every layer's MLP; `cond` (NULL for none) adds the
+ * conditional bias U_l SiLU(V_l [f; g]) of every row to its up projection, f
+ * being the row's residual stream as it enters the layer.  `taps` (NULL for none) receives, per
  * row, the residual stream after the three tap blocks: taps[m][3][d].  Writes
  * the final-norm hidden state of every row to hF[m][d] and, when
  * logits != NULL, the logits of every row to logits[m][vocab].
  */
 static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32_t* toks,
-                          const double* add, const double* ubias, const double* obias, double* taps, double* hF,
-                          double* logits) {
+                          const double* add, const double* ubias, const double* obias, const ocond* cond,
+                          double* taps, double* hF, double* logits) {
     const odims* dm = &M->dm;
     int d = dm->d_model, H = dm->n_heads, Hkv = dm->n_kv_heads, F = dm->d_ff;
     int hd = d / H, group = H / Hkv;
@@ -215,6 +234,8 @@ static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32
     double* proj = calloc((size_t)m * d, sizeof(double));
     double* gate = calloc((size_t)m * F, sizeof(double));
     double* up = calloc((size_t)m * F, sizeof(double));
+    double* cb = cond ? calloc((size_t)m * F, sizeof(double)) : NULL;          /* [m][F] conditional bias */
+    double* ch = cond ? calloc((size_t)m * cond->rank, sizeof(double)) : NULL; /* [m][R] its hidden layer */
     int maxlen = pos0 + m;
     for (int r = 0; r < m; ++r)
         for (int i = 0; i < d; ++i)
@@ -222,6 +243,17 @@ static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32
 
     for (int l = 0; l < dm->n_layers; ++l) {
         const void** Wl = M->layers + (size_t)l * W_PER_LAYER;
+        if (cond) {
+            /* b = U_l SiLU(V_l^f f + V_l^g g), f = x as it enters the layer */
+            int R = cond->rank;
+            const void* vf = (const char*)cond->vf + (size_t)l * R * d * (M->bf16 ? 2 : 4);
+            const void* u = (const char*)cond->u + (size_t)l * F * R * (M->bf16 ? 2 : 4);
+            matmul_rows(M->bf16, vf, R, d, x, m, ch);
+            for (int r = 0; r < m; ++r)
+                for (int i = 0; i < R; ++i)
+                    ch[(size_t)r * R + i] = silu(ch[(size_t)r * R + i] + cond->c[(size_t)l * R + i]);
+            matmul_rows(M->bf16, u, F, R, ch, m, cb);
+        }
         /* attention sub-block */
         for (int r = 0; r < m; ++r) rmsnorm(M->bf16, Wl[W_ATTN_NORM], d, dm->rms_eps, x + (size_t)r * d, nrm + (size_t)r * d);
         matmul_rows(M->bf16, Wl[W_Q], H * hd, d, nrm, m, q);
@@ -272,7 +304,7 @@ static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32
         matmul_rows(M->bf16, Wl[W_GATE], F, d, nrm, m, gate);
         matmul_rows(M->bf16, Wl[W_UP], F, d, nrm, m, up);
         for (size_t i = 0; i < (size_t)m * F; ++i) {
-            double u = up[i] + (ubias ? ubias[(size_t)l * F + i % F] : 0.0);
+            double u = up[i] + (ubias ? ubias[(size_t)l * F + i % F] : 0.0) + (cb ? cb[i] : 0.0);
             gate[i] = silu(gate[i]) * u;
         }
         matmul_rows(M->bf16, Wl[W_DOWN], d, F, gate, m, proj);
@@ -289,6 +321,7 @@ static void forward_block(const omodel* M, okv* kv, int pos0, int m, const int32
     for (int r = 0; r < m; ++r) rmsnorm(M->bf16, M->final_norm, d, dm->rms_eps, x + (size_t)r * d, hF + (size_t)r * d);
     if (logits) matmul_rows(M->bf16, M->lm_head, dm->vocab, d, hF, m, logits);
     free(x); free(nrm); free(q); free(kk); free(vv); free(att); free(proj); free(gate); free(up);
+    free(cb); free(ch);
 }
 
 /* ----------------------------------------------------------------------- */
@@ -420,10 +453,14 @@ void oracle_accept_final(int k, int V, float T, uint64_t seed, int t, int b, con
 typedef struct {
     omodel V, D;
     const void* w_s;           /* form 0: [d_D][d_V]; form 1: [L_D*F_D][d_V]; storage type of the models */
-    int form;                  /* 0: input-embedding steering; 1: MLP steering (eq. (2)); 2: bias after the MLP */
+    int form;                  /* 0: input-embedding steering; 1: MLP steering (eq. (2)); 2: bias after the MLP;
+                                  3: conditional bias in the MLP */
+    const void *w_cf, *w_cu;   /* form 3: V^f [L_D*R][d_D], U [L_D*F_D][R]; W_s holds V^g [L_D*R][d_V] */
+    int rank;                  /* form 3: R */
     const void *w_hml, *ln_gain, *ln_bias;   /* form 1: W_hml [d_V][3 d_V], LayerNorm gain and shift [d_V] */
     double ln_eps;
-    double* ub;                /* form 1: [max_batch][L_D*F_D] up-projection biases; form 2: [max_batch][d_D] */
+    double* ub;                /* form 1: [max_batch][L_D*F_D] up-projection biases; form 2: [max_batch][d_D];
+                                  form 3: [max_batch][L_D*R] the g parts V_l^g g */
     int nb;                    /* bias values per sequence */
     int k, max_batch, cap, max_new;
     float temperature;
@@ -450,9 +487,10 @@ ostate* oracle_create(const int32_t* dims_v, const double* rope_eps_v, const int
                       const double* rope_eps_d, int bf16, const void* const* ptrs_v, const void* const* ptrs_d,
                       const void* w_s, int k, int max_batch, int cap, int max_new, float temperature,
                       uint64_t seed, int form, const void* w_hml, const void* ln_gain, const void* ln_bias,
-                      double ln_eps) {
+                      double ln_eps, const void* w_cf, const void* w_cu, int rank) {
     /* MLP steering taps decoder block 3: the verifier needs at least three layers */
-    if (form != 0 && ((form != 1 && form != 2) || dims_v[0] < 3 || !w_hml || !ln_gain || !ln_bias)) return NULL;
+    if (form != 0 && ((form < 1 || form > 3) || dims_v[0] < 3 || !w_hml || !ln_gain || !ln_bias)) return NULL;
+    if (form == 3 && (!w_cf || !w_cu || rank < 1)) return NULL;
     ostate* st = calloc(1, sizeof(ostate));
     omodel* ms[2] = {&st->V, &st->D};
     const int32_t* dims[2] = {dims_v, dims_d};
@@ -473,7 +511,10 @@ ostate* oracle_create(const int32_t* dims_v, const double* rope_eps_v, const int
     st->w_s = w_s;
     st->form = form;
     st->w_hml = w_hml; st->ln_gain = ln_gain; st->ln_bias = ln_bias; st->ln_eps = ln_eps;
-    st->nb = form == 1 ? st->D.dm.n_layers * st->D.dm.d_ff : (form == 2 ? st->D.dm.d_model : 0);
+    st->w_cf = w_cf; st->w_cu = w_cu; st->rank = rank;
+    st->nb = form == 1 ? st->D.dm.n_layers * st->D.dm.d_ff
+           : form == 2 ? st->D.dm.d_model
+           : form == 3 ? st->D.dm.n_layers * rank : 0;
     if (form != 0) st->ub = calloc((size_t)max_batch * st->nb, sizeof(double));
     st->k = k; st->max_batch = max_batch; st->cap = cap; st->max_new = max_new;
     st->temperature = temperature; st->seed = seed;
@@ -508,8 +549,9 @@ static void steer(const ostate* st, const double* h, double* s) {
 }
 
 /* MLP steering (eq. (2)): g = LayerNorm(W_hml [h; m; l]), then the biases
- * ub = W_s g: per-layer up-projection biases [L_D*F_D] (form 1) or the one
- * bias after every MLP [d_D] (form 2).  z holds [h; m; l] (3 d_V). */
+ * ub = W_s g: per-layer up-projection biases [L_D*F_D] (form 1), the one
+ * bias after every MLP [d_D] (form 2), or the g parts V_l^g g of the
+ * conditional biases [L_D*R] (form 3).  z holds [h; m; l] (3 d_V). */
 static void mlp_steer(const ostate* st, const double* z, double* ub) {
     int dV = st->V.dm.d_model;
     int nb = st->nb;
@@ -552,14 +594,14 @@ int oracle_prefill_one(ostate* st, int b, const int32_t* prompt, int p) {
     if (p >= 2) {
         double* hF = malloc((size_t)(p - 1) * dV * sizeof(double));
         double* taps = ub ? malloc((size_t)(p - 1) * 3 * dV * sizeof(double)) : NULL;
-        forward_block(&st->V, &st->kv_v[b], 0, p - 1, prompt, NULL, NULL, NULL, taps, hF, NULL);
+        forward_block(&st->V, &st->kv_v[b], 0, p - 1, prompt, NULL, NULL, NULL, NULL, taps, hF, NULL);
         if (ub) mlp_steer(st, taps + (size_t)(p - 2) * 3 * dV, ub);
         else steer(st, hF + (size_t)(p - 2) * dV, s);
         free(hF);
         free(taps);
         /* the drafter processes the prompt without steering */
         double* hD = malloc((size_t)(p - 1) * dD * sizeof(double));
-        forward_block(&st->D, &st->kv_d[b], 0, p - 1, prompt, NULL, NULL, NULL, NULL, hD, NULL);
+        forward_block(&st->D, &st->kv_d[b], 0, p - 1, prompt, NULL, NULL, NULL, NULL, NULL, hD, NULL);
         free(hD);
     }
     st->t[b] = p;
@@ -611,8 +653,9 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
             m = 1;
             in = &drafts[j - 2];
         }
+        ocond cd = {st->w_cf, st->w_cu, st->rank, ub};
         forward_block(&st->D, &st->kv_d[b], pos0, m, in, ub ? NULL : s, st->form == 1 ? ub : NULL,
-                      st->form == 2 ? ub : NULL, NULL, hD, dl);
+                      st->form == 2 ? ub : NULL, st->form == 3 ? &cd : NULL, NULL, hD, dl);
         float* q = qlog + (size_t)(j - 1) * V;
         for (int v = 0; v < V; ++v) q[v] = (float)dl[(size_t)(m - 1) * V + v];
         float margin;
@@ -628,7 +671,7 @@ int oracle_round_one(ostate* st, int b, int32_t* out_tokens, oround_log* lg, flo
     double* hF = malloc((size_t)(k + 1) * dV * sizeof(double));
     double* vl = malloc((size_t)(k + 1) * V * sizeof(double));
     double* taps = ub ? malloc((size_t)(k + 1) * 3 * dV * sizeof(double)) : NULL;
-    forward_block(&st->V, &st->kv_v[b], t - 1, k + 1, blk, NULL, NULL, NULL, taps, hF, vl);
+    forward_block(&st->V, &st->kv_v[b], t - 1, k + 1, blk, NULL, NULL, NULL, NULL, taps, hF, vl);
     for (size_t i = 0; i < (size_t)(k + 1) * V; ++i) plog[i] = (float)vl[i];
 
     /* ---- accept / reject, final token ---- */
@@ -699,11 +742,11 @@ void oracle_forward(const ostate* st, int which, const int32_t* toks, int n, con
     const omodel* M = which == 0 ? &st->V : &st->D;
     okv kv = kv_alloc(&M->dm, n);
     if (!add) {
-        forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, NULL, hF, logits);
+        forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, NULL, NULL, hF, logits);
     } else {
         int d = M->dm.d_model;
         for (int i = 0; i < n; ++i)
-            forward_block(M, &kv, i, 1, toks + i, add + (size_t)i * d, NULL, NULL, NULL, hF + (size_t)i * d,
+            forward_block(M, &kv, i, 1, toks + i, add + (size_t)i * d, NULL, NULL, NULL, NULL, hF + (size_t)i * d,
                           logits ? logits + (size_t)i * M->dm.vocab : NULL);
     }
     free(kv.k);
@@ -723,10 +766,24 @@ void oracle_forward_mlp(const ostate* st, int which, const int32_t* toks, int n,
                         const double* obias, double* taps, double* hF, double* logits) {
     const omodel* M = which == 0 ? &st->V : &st->D;
     okv kv = kv_alloc(&M->dm, n);
-    forward_block(M, &kv, 0, n, toks, NULL, ubias, obias, taps, hF, logits);
+    forward_block(M, &kv, 0, n, toks, NULL, ubias, obias, NULL, taps, hF, logits);
     free(kv.k);
     free(kv.v);
 }
 
 /* MLP steering on its own: ub = W_s LayerNorm(W_hml z), z = [h; m; l] (form 1 or 2 sizes). */
 void oracle_mlp_steer(const ostate* st, const double* z, double* ub) { mlp_steer(st, z, ub); }
+
+/*
+ * Whole-sequence forward of the drafter (which = 1) or verifier with the conditional MLP bias of
+ * form 3 on every row: c [L*R] holds V_l^g g for one g (NULL: no bias).  Outputs as oracle_forward.
+ */
+void oracle_forward_cond(const ostate* st, int which, const int32_t* toks, int n, const double* c, double* hF,
+                         double* logits) {
+    const omodel* M = which == 0 ? &st->V : &st->D;
+    okv kv = kv_alloc(&M->dm, n);
+    ocond cd = {st->w_cf, st->w_cu, st->rank, c};
+    forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, c ? &cd : NULL, NULL, hF, logits);
+    free(kv.k);
+    free(kv.v);
+}

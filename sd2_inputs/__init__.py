@@ -131,15 +131,18 @@ def steer_weights(wl: Workload) -> np.ndarray:
 
 
 def mlp_steer_weights(wl: Workload, hml: str = "normal", ln: str = "normal", ln_eps: float = 1e-5,
-                      form: int = 1) -> dict:
+                      form: int = 1, rank: int = 256, cond_scale: float = WEIGHT_STD) -> dict:
     """Weights of the MLP steering forms: W_s [L_D*F_D][d_V] (form 1: one d_ff block per drafter
-    layer) or [d_D][d_V] (form 2: one bias after every MLP),
+    layer) or [d_D][d_V] (form 2: one bias after every MLP); form 3 (the conditional bias, a
+    two-layer MLP per drafter layer of hidden width `rank`): W_s = V^g [L_D*rank][d_V] plus
+    w_cf = V^f [L_D*rank][d_D] and w_cu = U [L_D*F_D][rank], drawn with std `cond_scale`;
     W_hml [d_V][3 d_V] ("normal" draws, or "identity" for [I I I], which maps [h; m; l] to
     h + m + l), LayerNorm gain and shift [d_V] ("normal": 1 + N(0, 0.02) and N(0, 0.02); "unit":
     ones and zeros)."""
     dV, dD = wl.verifier.d_model, wl.drafter
-    rows = dD.n_layers * dD.d_ff if form == 1 else dD.d_model
-    w_s = normal((rows, dV), wl.dtype, wl.seed, (3 << 20) | (1 if form == 1 else 5))
+    rows = dD.n_layers * dD.d_ff if form == 1 else (dD.n_layers * rank if form == 3 else dD.d_model)
+    purpose = {1: 1, 2: 5, 3: 6}[form]
+    w_s = normal((rows, dV), wl.dtype, wl.seed, (3 << 20) | purpose, cond_scale if form == 3 else WEIGHT_STD)
     if hml == "identity":
         eye = np.eye(dV, dtype=np.float32)
         w = np.concatenate([eye, eye, eye], axis=1)
@@ -154,9 +157,16 @@ def mlp_steer_weights(wl: Workload, hml: str = "normal", ln: str = "normal", ln_
         gain = ((g32.view(np.uint32) + 0x7FFF + ((g32.view(np.uint32) >> 16) & 1)) >> 16).astype(np.uint16) \
             if wl.dtype == "bf16" else g32
         shift = normal((dV,), wl.dtype, wl.seed, (3 << 20) | 4)
-    return {"w_s": np.ascontiguousarray(w_s), "w_hml": np.ascontiguousarray(w_hml),
-            "ln_gain": np.ascontiguousarray(gain), "ln_bias": np.ascontiguousarray(shift), "ln_eps": ln_eps,
-            "form": form}
+    out = {"w_s": np.ascontiguousarray(w_s), "w_hml": np.ascontiguousarray(w_hml),
+           "ln_gain": np.ascontiguousarray(gain), "ln_bias": np.ascontiguousarray(shift), "ln_eps": ln_eps,
+           "form": form}
+    if form == 3:
+        out["w_cf"] = np.ascontiguousarray(normal((dD.n_layers * rank, dD.d_model), wl.dtype, wl.seed,
+                                                  (3 << 20) | 7, cond_scale))
+        out["w_cu"] = np.ascontiguousarray(normal((dD.n_layers * dD.d_ff, rank), wl.dtype, wl.seed,
+                                                  (3 << 20) | 8, cond_scale))
+        out["rank"] = rank
+    return out
 
 
 def prompt_lens(wl: Workload) -> np.ndarray:

@@ -37,13 +37,16 @@ def tap_blocks(L):
     return [L - 2, L // 2, 3]
 
 
-def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False, obias=None):
+def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False, obias=None, cond=None):
     """Causal forward of a whole sequence; returns (final-norm hidden [T][d], logits [T][V]).
 
     ubias: up-projection biases added before the gating product, [L][F] for every row or
     [T][L][F] per row.  obias: a bias added to every layer's MLP output, [d] or [T][d] per row.
-    taps=True also returns the residual stream after the tap blocks,
-    [T][3][d]."""
+    cond: the conditional MLP bias, a dict with vf [L*R][d], vg [L*R][d_V], u [L*F][R] (model
+    dtype), rank R, per-row steering vectors g [T][d_V] and a per-row mask on [T] (rows without
+    a bias): layer l adds U_l SiLU(V_l [f; g]) to the up projection, V_l = [V_l^f V_l^g]
+    concatenated and f the layer's input row.  taps=True also returns the residual stream after
+    the tap blocks, [T][3][d]."""
     T = len(toks)
     d, H, Hkv, hd = dm.d_model, dm.n_heads, dm.n_kv_heads, dm.head_dim
     toks_t = torch.as_tensor(np.asarray(toks, dtype=np.int64))
@@ -59,6 +62,13 @@ def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False, obias=None):
 
     for li, layer in enumerate(w["layers"]):
         an, wq, wk, wv, wo, fn, wg, wu, wd = layer
+        cb = None
+        if cond is not None:
+            R, Fd = cond["rank"], dm.d_ff
+            V = torch.cat([_t(cond["vf"], dtype)[li * R:(li + 1) * R], _t(cond["vg"], dtype)[li * R:(li + 1) * R]], dim=1)
+            fg = torch.cat([x, torch.as_tensor(np.asarray(cond["g"]), dtype=torch.float64)], dim=1)
+            cb = F.silu(fg @ V.T) @ _t(cond["u"], dtype)[li * Fd:(li + 1) * Fd].T
+            cb = cb * torch.as_tensor(np.asarray(cond["on"], dtype=np.float64))[:, None]
         n = norm(x, an)
         q = (n @ _t(wq, dtype).T).view(T, H, hd).transpose(0, 1)
         k = (n @ _t(wk, dtype).T).view(T, Hkv, hd).transpose(0, 1)
@@ -73,6 +83,8 @@ def forward(dm, w, dtype, toks, add=None, ubias=None, taps=False, obias=None):
         up = n2 @ _t(wu, dtype).T
         if ub is not None:
             up = up + (ub[li] if ub.dim() == 2 else ub[:, li, :])
+        if cb is not None:
+            up = up + cb
         x = x + (F.silu(n2 @ _t(wg, dtype).T) * up) @ _t(wd, dtype).T
         if obias is not None:
             x = x + torch.as_tensor(np.asarray(obias), dtype=torch.float64)
@@ -94,3 +106,11 @@ def mlp_steer(z, mlp, dtype, n_layers, d_ff):
                      eps=mlp["ln_eps"])
     out = _t(mlp["w_s"], dtype) @ g
     return (out.reshape(n_layers, d_ff) if int(mlp.get("form", 1)) == 1 else out).numpy()
+
+
+def steer_g(z, mlp, dtype):
+    """g = LayerNorm(W_hml z) for z = [h; m; l]."""
+    zt = torch.as_tensor(np.asarray(z, dtype=np.float64)).reshape(-1)
+    g = _t(mlp["w_hml"], dtype) @ zt
+    return F.layer_norm(g, (g.shape[0],), weight=_t(mlp["ln_gain"], dtype), bias=_t(mlp["ln_bias"], dtype),
+                        eps=mlp["ln_eps"]).numpy()
