@@ -83,8 +83,10 @@ typedef struct {
     int32_t max_new_tokens;        /* generated tokens per sequence; its last round is truncated */
     float temperature;             /* 0 => greedy (argmax drafts, accept iff draft == verifier argmax) */
     uint64_t seed;                 /* Philox4x32-10 key of every random draw */
-    int32_t steering;              /* SD2_STEER_INPUT or SD2_STEER_NONE (sd2_create); SD2_STEER_MLP or
-                                      SD2_STEER_MLP_OUT (sd2_create_mlp) */
+    int32_t steering;              /* SD2_STEER_INPUT or SD2_STEER_NONE (sd2_create); SD2_STEER_MLP,
+                                      SD2_STEER_MLP_OUT or SD2_STEER_MLP_COND (sd2_create_mlp) */
+    int32_t cond_rank;             /* SD2_STEER_MLP_COND: hidden width R of the conditional bias MLP,
+                                      a multiple of 16 in 16..4096; ignored by the other forms */
 } sd2_config;
 
 /* How the drafter is steered by the verifier (sd2_config.steering). */
@@ -98,6 +100,13 @@ typedef struct {
 #define SD2_STEER_MLP_OUT 2 /* the paper's ablation "Inv. bias after MLP" (Sec. Ablation): the same g,
                               and one bias b = W_s g of d_D values added to the output of every
                               drafter MLP (x += W_d(...) + b).  Needs L_V >= 3. */
+#define SD2_STEER_MLP_COND 4 /* the paper's ablation "Cond. bias in MLP" (Sec. Ablation; its formula is
+                              this library's reading): the same g, and per drafter layer l and token
+                              the bias U_l SiLU(V_l [f; g]) added to the up projection as in eq. (2),
+                              f the residual stream entering layer l at the token's position (the
+                              embedding for l = 0), V_l [R][d_D + d_V], U_l [d_ff_D][R].  The g part
+                              V_l^g g is computed once per round.  Runs one kernel per operation
+                              (no persistent launches).  Needs L_V >= 3. */
 #define SD2_STEER_NONE 3   /* no steering: the pretrained drafter the paper compares against (Table 1,
                               "Pretrained"); no steering projection runs and nothing is added to the
                               drafter.  Gives the same outputs as SD2_STEER_INPUT with W_s = 0, without
@@ -106,11 +115,14 @@ typedef struct {
 /* Weights of SD2_STEER_MLP, device pointers in the configuration's dtype, 16-byte aligned. */
 typedef struct {
     const void* w_s;       /* SD2_STEER_MLP: [L_D * d_ff_D][d_V], rows l*d_ff_D .. (l+1)*d_ff_D - 1 give
-                              layer l's bias; SD2_STEER_MLP_OUT: [d_D][d_V] */
+                              layer l's bias; SD2_STEER_MLP_OUT: [d_D][d_V]; SD2_STEER_MLP_COND: V^g
+                              [L_D * R][d_V], rows l*R .. (l+1)*R - 1 the g columns of V_l */
     const void* w_hml;     /* [d_V][3 d_V]: g = W_hml [h; m; l] (columns: h, then m, then l) */
     const void* ln_gain;   /* [d_V] LayerNorm gain */
     const void* ln_bias;   /* [d_V] LayerNorm shift */
     float ln_eps;          /* LayerNorm: (g - mean) / sqrt(var + eps) * gain + shift, population variance */
+    const void* w_cf;      /* SD2_STEER_MLP_COND: V^f [L_D * R][d_D], the f columns of V_l (else unused) */
+    const void* w_cu;      /* SD2_STEER_MLP_COND: U [L_D * d_ff_D][R], rows l*d_ff_D .. the U_l block */
 } sd2_mlp_steering;
 
 /* Bytes of device workspace sd2_create needs for cfg (0 if cfg is invalid). */
@@ -154,7 +166,7 @@ sd2_status sd2_create_noalloc(const sd2_config* cfg, const sd2_weights* verifier
 /*
  * Create a handle whose drafter is steered by the paper's MLP biases (eq. (2); Sec.
  * "Verification" and "Drafting"): cfg->steering must be SD2_STEER_MLP (or SD2_STEER_MLP_OUT, the
- * ablation with one bias after every MLP).  Everything else is as
+ * ablation with one bias after every MLP, or SD2_STEER_MLP_COND, the conditional bias).  Everything else is as
  * sd2_create.  The bias is recomputed at the end of every round from the verifier row whose
  * logits produced the final token, and used for every drafter token of the next round;
  * the drafter processes the prompt without steering, and the first round's bias comes from

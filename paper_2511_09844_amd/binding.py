@@ -36,14 +36,16 @@ class Weights(ctypes.Structure):
 class Config(ctypes.Structure):
     _fields_ = [("verifier", Dims), ("drafter", Dims), ("dtype", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("max_batch", ctypes.c_int32), ("max_seq_len", ctypes.c_int32), ("max_new_tokens", ctypes.c_int32),
-                ("temperature", ctypes.c_float), ("seed", ctypes.c_uint64), ("steering", ctypes.c_int32)]
+                ("temperature", ctypes.c_float), ("seed", ctypes.c_uint64), ("steering", ctypes.c_int32),
+                ("cond_rank", ctypes.c_int32)]
 
 
-STEER_INPUT, STEER_MLP, STEER_MLP_OUT, STEER_NONE = 0, 1, 2, 3
+STEER_INPUT, STEER_MLP, STEER_MLP_OUT, STEER_NONE, STEER_MLP_COND = 0, 1, 2, 3, 4
 
 
 class MlpSteering(ctypes.Structure):
-    _fields_ = [("w_s", P), ("w_hml", P), ("ln_gain", P), ("ln_bias", P), ("ln_eps", ctypes.c_float)]
+    _fields_ = [("w_s", P), ("w_hml", P), ("ln_gain", P), ("ln_bias", P), ("ln_eps", ctypes.c_float),
+                ("w_cf", P), ("w_cu", P)]
 
 
 _lib = None
@@ -95,14 +97,14 @@ def dims_of(dm) -> Dims:
 
 
 def config_of(wl, max_batch=None, max_seq_len=None, max_new_tokens=None, temperature=None, k=None, seed=None,
-              steering=STEER_INPUT):
+              steering=STEER_INPUT, cond_rank=0):
     return Config(dims_of(wl.verifier), dims_of(wl.drafter), 1 if wl.dtype == "bf16" else 0,
                   wl.k if k is None else k,
                   wl.batch if max_batch is None else max_batch,
                   wl.max_seq_len if max_seq_len is None else max_seq_len,
                   wl.new_tokens if max_new_tokens is None else max_new_tokens,
                   wl.temperature if temperature is None else temperature,
-                  wl.seed if seed is None else seed, steering)
+                  wl.seed if seed is None else seed, steering, cond_rank)
 
 
 class Sd2Error(RuntimeError):
@@ -183,7 +185,9 @@ class Engine:
                 check(rc, None, "sd2_create")
             else:
                 ms = MlpSteering(mlp["w_s"].data_ptr(), mlp["w_hml"].data_ptr(), mlp["ln_gain"].data_ptr(),
-                                 mlp["ln_bias"].data_ptr(), float(mlp["ln_eps"]))
+                                 mlp["ln_bias"].data_ptr(), float(mlp["ln_eps"]),
+                                 mlp["w_cf"].data_ptr() if "w_cf" in mlp else None,
+                                 mlp["w_cu"].data_ptr() if "w_cu" in mlp else None)
                 rc = lib.sd2_create_mlp(ctypes.byref(cfg), ctypes.byref(verifier.w), ctypes.byref(drafter.w),
                                         ctypes.byref(ms), base + off, nbytes, self.stream.cuda_stream,
                                         ctypes.byref(self.h))
@@ -235,7 +239,8 @@ class Engine:
             DBG_HIST: ((B, self.cfg.max_seq_len), np.int32), DBG_HIDDEN_V: ((B, k + 1, dV), np.float32),
             DBG_PATH: ((2,), np.int32), DBG_TRACE: ((33, 1024), np.int64),
             DBG_UBIAS: (((B, self.cfg.drafter.n_layers, self.cfg.drafter.d_ff) if self.cfg.steering == STEER_MLP
-                         else (B, self.cfg.drafter.d_model)), np.float32),
+                         else (B, self.cfg.drafter.n_layers, self.cfg.cond_rank)
+                         if self.cfg.steering == STEER_MLP_COND else (B, self.cfg.drafter.d_model)), np.float32),
         }
         shp, dt = shapes[what]
         out = np.zeros(shp, dtype=dt)

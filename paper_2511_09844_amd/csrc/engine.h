@@ -54,7 +54,7 @@ struct Workspace {
     int32_t* row_seq;       // [maxm]
     int32_t* lm_map_d;      // [k][2*max_batch] drafter LM-head output rows per step
     int32_t* steer_map;     // [max_batch]
-    int32_t* ident_map;     // [max_batch] 0..max_batch-1
+    int32_t* ident_map;     // [2 max_batch] 0..2 max_batch-1
     // activations
     float* qkv;             // [maxm][max qkv_dim]
     float* attn;            // [maxm][max H*hd]
@@ -84,7 +84,10 @@ struct Workspace {
     float* taps;            // [3][maxm][d_V] verifier residual after the tap blocks (per-operation path)
     float* tapsel;          // [max_batch][3 d_V] [h; m; l] of each sequence's steering row
     float* gsteer;          // [max_batch][d_V] g = W_hml [h; m; l], then its LayerNorm
-    float* ubias;           // [max_batch][nbias] biases of the current round (L_D x F_D, or d_D)
+    float* ubias;           // [max_batch][nbias] biases of the current round (L_D x F_D, or d_D; the conditional
+                            // bias: the g parts V_l^g g, L_D x R)
+    float* cond_h;          // conditional bias: [2 max_batch][R] hidden layer of the drafter rows
+    float* cond_b;          // conditional bias: [2 max_batch][F_D] one layer's bias of the drafter rows
 };
 
 // Per-launch timing entries (HIP events recorded on the engine's stream).
@@ -102,6 +105,8 @@ struct Engine {
     const void* w_steer;    // SD2_STEER_INPUT: [d_D][d_V]; SD2_STEER_MLP: [L_D*F_D][d_V]; null: SD2_STEER_NONE
     bool mlp;               // cfg.steering is SD2_STEER_MLP or SD2_STEER_MLP_OUT (taps, W_hml, LayerNorm)
     bool bias_after;        // SD2_STEER_MLP_OUT: the bias joins every drafter MLP's output
+    bool cond;              // SD2_STEER_MLP_COND: per-row biases U_l SiLU(V_l^f f + V_l^g g) (one kernel per op)
+    const void *w_cf, *w_cu;  // SD2_STEER_MLP_COND: V^f [L_D R][d_D], U [L_D F_D][R]
     int nbias;              // bias values per sequence: L_D*F_D or d_D
     const void *w_hml, *ln_gain, *ln_bias;
     float ln_eps;
@@ -148,11 +153,14 @@ void launch_init_maps(hipStream_t s, Engine& e);
 enum PlanKind { kPlanDraft1 = 0, kPlanDraftJ = 1, kPlanVerify = 2, kPlanPrefill = 3 };
 void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
                        const int32_t* prompt_len, int max_prompt, int chunk);
+// ub_map (null: the row's sequence) maps rows to bias rows (the conditional bias: one per row).
 // ubias (drafter rounds with MLP steering): this layer's biases, row stride ub_ld, indexed by
 // the row's sequence, added to the up projection, or to the MLP output when bias_after; null
 // for none.
 void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps, const float* ubias = nullptr,
-                  int ub_ld = 0, bool bias_after = false);
+                  int ub_ld = 0, bool bias_after = false, const int32_t* ub_map = nullptr);
+// Conditional bias of drafter layer `layer` for every row: cond_b = U_l SiLU(V_l^f x + c_l[seq]).
+void launch_cond_bias(hipStream_t s, Engine& e, int layer, int rows);
 // Final-norm LM head of `rows` residual rows into Y[out_map[r]] (bf16 path via the projection kernel).
 void launch_lm_head(Engine& e, ModelDev& m, int rows, float* Y, const int32_t* out_map);
 void launch_steer(Engine& e, const float* X, const float* ss, const int32_t* in_map, int rows);

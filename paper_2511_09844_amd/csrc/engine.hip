@@ -69,7 +69,9 @@ bool config_ok(const sd2_config* c) {
     if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // 8192 = 64 spans of 128
     if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
     if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP && c->steering != SD2_STEER_MLP_OUT &&
-        c->steering != SD2_STEER_NONE)
+        c->steering != SD2_STEER_NONE && c->steering != SD2_STEER_MLP_COND)
+        return false;
+    if (c->steering == SD2_STEER_MLP_COND && (c->cond_rank < 16 || c->cond_rank > 4096 || c->cond_rank % 16))
         return false;
     if (mlp_form(*c)) {
         // the low tap is block 3; a steering projection runs on the MFMA kernel when its K is a
@@ -83,10 +85,13 @@ bool config_ok(const sd2_config* c) {
 }
 
 // MLP steering forms (taps, W_hml, LayerNorm, biases in the drafter's MLPs)
-bool mlp_form(const sd2_config& c) { return c.steering == SD2_STEER_MLP || c.steering == SD2_STEER_MLP_OUT; }
+bool mlp_form(const sd2_config& c) {
+    return c.steering == SD2_STEER_MLP || c.steering == SD2_STEER_MLP_OUT || c.steering == SD2_STEER_MLP_COND;
+}
 
 // MLP steering: bias values per sequence (per-layer up-projection biases, or one after-MLP bias)
 int bias_len(const sd2_config& c) {
+    if (c.steering == SD2_STEER_MLP_COND) return c.drafter.n_layers * c.cond_rank;  // the g parts V_l^g g
     return c.steering == SD2_STEER_MLP ? c.drafter.n_layers * c.drafter.d_ff : c.drafter.d_model;
 }
 
@@ -131,7 +136,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
     w.row_seq = cv.take<int32_t>(maxm);
     w.lm_map_d = cv.take<int32_t>((size_t)k * 2 * B);
     w.steer_map = cv.take<int32_t>(B);
-    w.ident_map = cv.take<int32_t>(B);
+    w.ident_map = cv.take<int32_t>(2 * (size_t)B);
     int qkv = std::max(ms[0]->qkv_dim, ms[1]->qkv_dim);
     int att = std::max(c.verifier.n_heads * ms[0]->hd, c.drafter.n_heads * ms[1]->hd);
     int ff = std::max(c.verifier.d_ff, c.drafter.d_ff);
@@ -174,10 +179,15 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                 }
         }
         if (mlp_form(c)) {
-            // W_hml (d_V x 3 d_V) and W_s (bias values x d_V) projections
-            int mshapes[2][2] = {{c.verifier.d_model, 3 * c.verifier.d_model}, {bias_len(c), c.verifier.d_model}};
-            for (int mm = 1; mm <= std::min(B, 16); ++mm)
-                for (auto& sh : mshapes) {
+            // W_hml (d_V x 3 d_V) and W_s (bias values x d_V) projections; the conditional bias's
+            // V^f (R x d_D) and U (d_ff x R) on the drafter's rows
+            const int R = c.steering == SD2_STEER_MLP_COND ? c.cond_rank : 0;
+            int mshapes[4][3] = {{c.verifier.d_model, 3 * c.verifier.d_model, std::min(B, 16)},
+                                 {bias_len(c), c.verifier.d_model, std::min(B, 16)},
+                                 {R, c.drafter.d_model, std::min(2 * B, 16)},
+                                 {c.drafter.d_ff, R, std::min(2 * B, 16)}};
+            for (auto& sh : mshapes)
+                for (int mm = 1; sh[0] > 0 && mm <= sh[2]; ++mm) {
                     WsPlan p = ws_plan(mm, sh[0], sh[1], kEpiStore);
                     if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256);
                 }
@@ -240,6 +250,10 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         w.tapsel = cv.take<float>((size_t)B * 3 * dV);
         w.gsteer = cv.take<float>((size_t)B * dV);
         w.ubias = cv.take<float>((size_t)B * bias_len(c));
+        if (c.steering == SD2_STEER_MLP_COND) {
+            w.cond_h = cv.take<float>((size_t)2 * B * c.cond_rank);
+            w.cond_b = cv.take<float>((size_t)2 * B * c.drafter.d_ff);
+        }
     }
     for (int i = 0; i < 2; ++i) {
         ModelDev* m = ms[i];
@@ -355,10 +369,18 @@ void enqueue_round(Engine& e, int32_t* out_tokens, int32_t* out_counts) {
     for (int j = 1; j <= k; ++j) {
         int rows = j == 1 ? 2 * B : B;
         launch_plan_embed(s, e, e.md, j == 1 ? kPlanDraft1 : kPlanDraftJ, j, rows, nullptr, nullptr, 0, 1);
-        for (int l = 0; l < e.md.dm.n_layers; ++l)
+        for (int l = 0; l < e.md.dm.n_layers; ++l) {
+            if (e.cond) {
+                // this layer's bias of every row, from the row's residual as it enters the layer
+                launch_cond_bias(s, e, l, rows);
+                launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1, e.ws.cond_b, e.md.dm.d_ff, false,
+                             e.ws.ident_map);
+                continue;
+            }
             launch_layer(s, e, e.md, l, rows, j == 1 ? 2 : 1,
                          !e.mlp ? nullptr : e.ws.ubias + (e.bias_after ? 0 : (size_t)l * e.md.dm.d_ff), ub_ld,
                          e.bias_after);
+        }
         launch_lm_head(e, e.md, rows, e.ws.logits_d, e.ws.lm_map_d + (size_t)(j - 1) * 2 * e.cfg.max_batch);
         launch_draft_pick(s, e, j);
     }
@@ -523,6 +545,13 @@ static sd2_status create_impl(const sd2_config* cfg, const sd2_weights* verifier
     e->bias_after = cfg->steering == SD2_STEER_MLP_OUT;
     e->nbias = bias_len(*cfg);
     if (mlp) {
+        e->cond = cfg->steering == SD2_STEER_MLP_COND;
+        if (e->cond && (!aligned16(mlp->w_cf) || !aligned16(mlp->w_cu))) {
+            if (!slot) delete e;
+            return SD2_ERR_INVALID_ARG;
+        }
+        e->w_cf = mlp->w_cf;
+        e->w_cu = mlp->w_cu;
         e->w_hml = mlp->w_hml;
         e->ln_gain = mlp->ln_gain;
         e->ln_bias = mlp->ln_bias;

@@ -29,7 +29,7 @@ void launch_rope_table(hipStream_t s, ModelDev& m, int cap) {
 // only the second (position t-1) produces logits; later steps have one row per sequence.
 __global__ void k_init_maps(int32_t* lm_map_d, int32_t* ident, int max_batch, int k) {
     int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r < max_batch) ident[r] = r;
+    if (r < 2 * max_batch) ident[r] = r;
     for (int j = 0; j < k; ++j) {
         int32_t* mp = lm_map_d + (size_t)j * 2 * max_batch;
         if (j == 0) {
@@ -388,7 +388,8 @@ static WsCall ws_base(Engine& e, ModelDev& m) {
 }
 
 void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, int rps, const float* ubias,
-                  int ub_ld, bool bias_after) {
+                  int ub_ld, bool bias_after, const int32_t* ub_map) {
+    const int32_t* bias_rows = ub_map ? ub_map : e.ws.row_seq;
     const float* up_bias = bias_after ? nullptr : ubias;
     const float* out_bias = bias_after ? ubias : nullptr;
     const sd2_dims& dm = m.dm;
@@ -416,13 +417,13 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, in
         g.X = m.x; g.M = rows; g.K = dm.d_model; g.gamma = W[kFfnNorm]; g.ss = m.ss;
         g.W[0] = W[kWg]; g.W[1] = W[kWu]; g.seg_rows[0] = dm.d_ff; g.seg_rows[1] = dm.d_ff; g.nseg = 2;
         g.mode = kEpiSwiglu; g.Y = e.ws.ffh; g.ldy = dm.d_ff;
-        g.ubias = up_bias; g.ub_ld = ub_ld; g.row_seq = e.ws.row_seq;
+        g.ubias = up_bias; g.ub_ld = ub_ld; g.row_seq = bias_rows;
         launch_wsgemv(&e, s, g);
         // down projection + residual
         WsCall d = ws_base(e, m);
         d.X = e.ws.ffh; d.M = rows; d.K = dm.d_ff; d.W[0] = W[kWd]; d.seg_rows[0] = dm.d_model; d.nseg = 1;
         d.mode = kEpiAdd; d.Y = m.x; d.ldy = dm.d_model; d.ss_out = m.ss;
-        d.ubias = out_bias; d.ub_ld = ub_ld; d.row_seq = e.ws.row_seq;
+        d.ubias = out_bias; d.ub_ld = ub_ld; d.row_seq = bias_rows;
         launch_wsgemv(&e, s, d);
         return;
     }
@@ -453,13 +454,13 @@ void launch_layer(hipStream_t s, Engine& e, ModelDev& m, int layer, int rows, in
         const void* ws[2] = {W[kWg], W[kWu]};
         int rws[2] = {dm.d_ff, dm.d_ff};
         launch_gemv(&e, s, e.bf16, m.x, nullptr, rows, dm.d_model, W[kFfnNorm], dm.rms_eps, ws, rws, 2, kEpiSwiglu,
-                    e.ws.ffh, dm.d_ff, nullptr, up_bias, ub_ld, e.ws.row_seq);
+                    e.ws.ffh, dm.d_ff, nullptr, up_bias, ub_ld, bias_rows);
     }
     {
         const void* ws[1] = {W[kWd]};
         int rws[1] = {dm.d_model};
         launch_gemv(&e, s, e.bf16, e.ws.ffh, nullptr, rows, dm.d_ff, nullptr, 0.f, ws, rws, 1, kEpiAdd, m.x,
-                    dm.d_model, nullptr, out_bias, ub_ld, e.ws.row_seq);
+                    dm.d_model, nullptr, out_bias, ub_ld, bias_rows);
     }
 }
 
@@ -618,6 +619,24 @@ void launch_mlp_steer(Engine& e, const float* const* src, const int32_t* in_map,
                                                             (const float*)e.ln_bias, e.ln_eps);
     prof_end(&e);
     project_rows(e, e.ws.gsteer, rows, dV, e.w_steer, nb, e.ws.ubias);
+}
+
+// Conditional bias, hidden layer: h = SiLU(h + c_l of the row's sequence), in place, [rows][R].
+__global__ void k_cond_act(float* h, int R, const float* c, int c_ld, const int32_t* row_seq) {
+    const int r = blockIdx.x;
+    const float* cr = c + (size_t)row_seq[r] * c_ld;
+    for (int i = threadIdx.x; i < R; i += blockDim.x) h[(size_t)r * R + i] = silu(h[(size_t)r * R + i] + cr[i]);
+}
+
+void launch_cond_bias(hipStream_t s, Engine& e, int layer, int rows) {
+    const int R = e.cfg.cond_rank, d = e.md.dm.d_model, F = e.md.dm.d_ff;
+    const size_t es = e.bf16 ? 2 : 4;
+    // V_l^f f: the raw residual rows as they enter the layer (no norm)
+    project_rows(e, e.md.x, rows, d, (const char*)e.w_cf + (size_t)layer * R * d * es, R, e.ws.cond_h);
+    prof_begin(&e, kProfOther, 0.0);
+    k_cond_act<<<rows, 256, 0, s>>>(e.ws.cond_h, R, e.ws.ubias + (size_t)layer * R, e.nbias, e.ws.row_seq);
+    prof_end(&e);
+    project_rows(e, e.ws.cond_h, rows, R, (const char*)e.w_cu + (size_t)layer * F * R * es, F, e.ws.cond_b);
 }
 
 // ===========================================================================

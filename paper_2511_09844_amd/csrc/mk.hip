@@ -1372,7 +1372,8 @@ bool mk_record(const sd2_config& c, const ModelDev& m, bool verifier, int M, int
 
 // Largest batch for which both launch kinds are supported (0: none).
 int mk_max_batch(const sd2_config& c) {
-    if (c.dtype != SD2_BF16) return 0;
+    // the conditional bias runs one kernel per operation
+    if (c.dtype != SD2_BF16 || c.steering == SD2_STEER_MLP_COND) return 0;
     ModelDev mv{}, md{};
     mv.dm = c.verifier;
     md.dm = c.drafter;

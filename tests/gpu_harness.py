@@ -75,10 +75,11 @@ def parity_run(wl, wv=None, wd=None, ws=None, seqs=None, max_rounds=10**6, check
         ws_dev = B.to_device(ws)
         eng = B.Engine(B.config_of(wl), dv, dd, ws_dev)
     else:
-        ws_dev = {key: B.to_device(mlp[key]) for key in ("w_s", "w_hml", "ln_gain", "ln_bias")}
+        keys = ("w_s", "w_hml", "ln_gain", "ln_bias") + (("w_cf", "w_cu") if int(mlp.get("form", 1)) == 3 else ())
+        ws_dev = {key: B.to_device(mlp[key]) for key in keys}
         ws_dev["ln_eps"] = mlp["ln_eps"]
-        form = B.STEER_MLP if int(mlp.get("form", 1)) == 1 else B.STEER_MLP_OUT
-        eng = B.Engine(B.config_of(wl, steering=form), dv, dd, None, mlp=ws_dev)
+        form = {1: B.STEER_MLP, 2: B.STEER_MLP_OUT, 3: B.STEER_MLP_COND}[int(mlp.get("form", 1))]
+        eng = B.Engine(B.config_of(wl, steering=form, cond_rank=int(mlp.get("rank", 0))), dv, dd, None, mlp=ws_dev)
 
     def steer_err(b, dev):
         # the steering state of sequence b: s (input form) or the per-layer biases (MLP form)

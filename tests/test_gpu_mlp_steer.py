@@ -99,3 +99,29 @@ def test_mlp_steering_8b_shapes_short_prompt(host_8b_mlp):
     wl = si.LLAMA8B.with_(prompt=(16, 16), new_tokens=10)
     wv, wd, mlp = host_8b_mlp
     _run(wl, wv=wv, wd=wd, mlp=mlp, expect_path=1)
+
+
+def _cond(wl, rank, scale=0.1, **kw):
+    """The "Cond. bias in MLP" ablation: per drafter layer and row, U_l SiLU(V_l^f f + V_l^g g)
+    added to the up projection (one kernel per operation); compared where the biases are
+    otherwise: the per-round g parts V_l^g g [L_D][R]."""
+    mlp = si.mlp_steer_weights(wl, form=3, rank=rank, cond_scale=scale)
+    return _run(wl, mlp=mlp, expect_path=0, **kw)
+
+
+def test_cond_bias_bf16_mfma_projections():
+    # R = 256: both bias projections (V^f with K = 512, U with K = 256) on the MFMA kernel
+    _cond(MLP_MK, 256)
+
+
+def test_cond_bias_small_rank_ragged():
+    # R = 64: U takes the vector kernel (K = 64); two sequences with 2- and 9-token prompts
+    _cond(MLP_SMALL, 64)
+
+
+def test_cond_bias_one_token_prompt():
+    _cond(MLP_SMALL.with_(prompt=(1, 1), batch=1), 64)
+
+
+def test_cond_bias_f32():
+    _cond(si.TINY.with_(new_tokens=16), 32)
