@@ -71,6 +71,8 @@ def _load():
         lib.oracle_forward_mlp.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P]
         lib.oracle_mlp_steer.argtypes = [P, P, P]
         lib.oracle_forward_cond.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P]
+        lib.oracle_train_loss.argtypes = [P, P, ctypes.c_int, P, P]
+        lib.oracle_train_loss.restype = ctypes.c_double
         lib.oracle_philox.argtypes = [P, u32, u32, P]
         lib.oracle_uniform.argtypes = [u32]
         lib.oracle_uniform.restype = f32
@@ -328,3 +330,13 @@ class Oracle:
             cp = c.ctypes.data
         self.lib.oracle_forward_cond(self.h, which, toks.ctypes.data, n, cp, hF.ctypes.data, lg.ctypes.data)
         return hF, lg
+
+    def train_loss(self, toks, deltas):
+        """Training-objective forward (input-form steering): per-target KL divergences [n] (entry 0
+        is 0) and their mean over targets 1..n-1, for tokens x_0..x_{n-1} and offsets deltas[tau]."""
+        toks = np.ascontiguousarray(toks, dtype=np.int32)
+        deltas = np.ascontiguousarray(deltas, dtype=np.int32)
+        assert len(deltas) == len(toks)
+        kl = np.zeros(len(toks), dtype=np.float64)
+        mean = self.lib.oracle_train_loss(self.h, toks.ctypes.data, len(toks), deltas.ctypes.data, kl.ctypes.data)
+        return float(mean), kl

@@ -55,6 +55,14 @@
  *     the up projection as in eq. (2).  V_l [f; g] = V_l^f f + V_l^g g: the
  *     g part is computed once per round (like eq. (2)'s bias), the f part per
  *     token and layer.
+ *   - training objective (Sec. "Training"; offset ablation in the appendix):
+ *     for a token sequence and per target position tau an offset delta_tau
+ *     drawn uniformly from [1, k], the loss is the mean over tau of
+ *     KL(pi_V(.|x_<tau) || pi_D(.|x_<tau, g from delta_tau positions back)).
+ *     Reading: the steering that predicts x_tau with offset delta is the one a
+ *     round starting at tau - delta + 1 uses, W_s hF_V(tau - delta - 1) (zero
+ *     before the sequence start); in the one-pass forward every drafter input
+ *     position p carries the steering of the target it predicts, x_{p+1}.
  *   - greedy regime (T = 0): argmax drafts, accept iff the draft equals the
  *     verifier's argmax, final token = verifier argmax (Sec. "Decoding
  *     Parameters").
@@ -786,4 +794,61 @@ void oracle_forward_cond(const ostate* st, int which, const int32_t* toks, int n
     forward_block(M, &kv, 0, n, toks, NULL, NULL, NULL, c ? &cd : NULL, NULL, hF, logits);
     free(kv.k);
     free(kv.v);
+}
+
+/*
+ * Training-objective forward (input-form steering) over tokens x_0..x_{n-1}: deltas[tau] in 1..k
+ * is the offset of target tau (deltas[0] unused).  out_kl[tau] (tau = 1..n-1) receives
+ *   KL(p_V || p_D) = sum_v p_V(v) (log p_V(v) - log p_D(v)),
+ * p_V = softmax of the verifier's logits at position tau-1 and p_D = softmax of the drafter's
+ * logits at position tau-1, where the drafter's input embedding at every position p is
+ * E_D[x_p] + s_{p+1}, s_tau = W_s hF_V(tau - deltas[tau] - 1) (zero when that position is
+ * negative), hF_V(q) the verifier's final-norm hidden state at position q.  out_kl[0] = 0.
+ * Returns the mean of out_kl[1..n-1]; NaN for n < 2.
+ */
+double oracle_train_loss(const ostate* st, const int32_t* toks, int n, const int32_t* deltas, double* out_kl) {
+    if (n < 2) return NAN;
+    int dV = st->V.dm.d_model, dD = st->D.dm.d_model, V = st->V.dm.vocab, m = n - 1;
+    double* hF = malloc((size_t)m * dV * sizeof(double));
+    double* lv = malloc((size_t)m * V * sizeof(double));
+    double* hD = malloc((size_t)dD * sizeof(double));
+    double* ld = malloc((size_t)m * V * sizeof(double));
+    double* sv = malloc((size_t)dD * sizeof(double));
+    okv kvv = kv_alloc(&st->V.dm, m), kvd = kv_alloc(&st->D.dm, m);
+    /* verifier over x_0..x_{n-2}: hidden states and logits of every position */
+    forward_block(&st->V, &kvv, 0, m, toks, NULL, NULL, NULL, NULL, NULL, hF, lv);
+    /* drafter one position at a time, each with the steering of the target it predicts */
+    for (int p = 0; p < m; ++p) {
+        int q = p - deltas[p + 1];
+        if (q >= 0) steer(st, hF + (size_t)q * dV, sv);
+        else
+            for (int i = 0; i < dD; ++i) sv[i] = 0.0;
+        forward_block(&st->D, &kvd, p, 1, toks + p, sv, NULL, NULL, NULL, NULL, hD, ld + (size_t)p * V);
+    }
+    double sum = 0.0;
+    out_kl[0] = 0.0;
+    for (int p = 0; p < m; ++p) {
+        const double* a = lv + (size_t)p * V;
+        const double* b = ld + (size_t)p * V;
+        double ma = -INFINITY, mb = -INFINITY;
+        for (int v = 0; v < V; ++v) {
+            if (a[v] > ma) ma = a[v];
+            if (b[v] > mb) mb = b[v];
+        }
+        double za = 0.0, zb = 0.0;
+        for (int v = 0; v < V; ++v) {
+            za += exp(a[v] - ma);
+            zb += exp(b[v] - mb);
+        }
+        double lsa = ma + log(za), lsb = mb + log(zb), kl = 0.0;
+        for (int v = 0; v < V; ++v) {
+            double lpa = a[v] - lsa, lpb = b[v] - lsb;
+            kl += exp(lpa) * (lpa - lpb);
+        }
+        out_kl[p + 1] = kl;
+        sum += kl;
+    }
+    free(hF); free(lv); free(hD); free(ld); free(sv);
+    free(kvv.k); free(kvv.v); free(kvd.k); free(kvd.v);
+    return sum / m;
 }

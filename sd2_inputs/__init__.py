@@ -45,6 +45,7 @@ def _load():
         lib.gen_prompt.argtypes = [ctypes.c_void_p, u64, u64, u32, i32]
         lib.gen_prompt_lens.argtypes = [ctypes.c_void_p, u64, u64, i32, i32]
         lib.gen_philox_block.argtypes = [ctypes.c_void_p, u64, ctypes.c_void_p]
+        lib.gen_uniform_int.argtypes = [ctypes.c_void_p, u64, u64, u32, u32, i32, i32]
         _lib = lib
     return _lib
 
@@ -193,3 +194,19 @@ def prompts(wl: Workload):
 def bf16_to_f32(a: np.ndarray) -> np.ndarray:
     """Exact widening of bf16 bit patterns (uint16) to float32."""
     return (a.astype(np.uint32) << 16).view(np.float32)
+
+
+# generator purposes of the training-objective inputs (beyond weights 0x10, prompts 0x11, lengths 0x12)
+PURPOSE_TRAIN_TOKENS, PURPOSE_TRAIN_OFFSETS = 0x13, 0x14
+
+
+def loss_inputs(wl: Workload, n: int, stream: int = 0):
+    """Inputs of the training-objective forward: a token sequence of length n, uniform over the
+    vocabulary (standing in for the verifier's own samples, which the paper trains on), and the
+    offset delta_tau of every target, uniform in [1, k] (entry 0 unused).  Both int32 [n]."""
+    lib = _load()
+    toks = np.empty((n,), dtype=np.int32)
+    lib.gen_uniform_int(toks.ctypes.data, n, wl.seed, PURPOSE_TRAIN_TOKENS, stream, 0, wl.verifier.vocab - 1)
+    deltas = np.empty((n,), dtype=np.int32)
+    lib.gen_uniform_int(deltas.ctypes.data, n, wl.seed, PURPOSE_TRAIN_OFFSETS, stream, 1, wl.k)
+    return toks, deltas
