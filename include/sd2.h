@@ -207,6 +207,27 @@ sd2_status sd2_round(sd2_handle_t h, int32_t* out_tokens, int32_t* out_counts);
  */
 sd2_status sd2_round_forced(sd2_handle_t h, const int32_t* forced, int32_t* out_tokens, int32_t* out_counts);
 
+/*
+ * Training-objective forward (paper Sec. "Training"; input-form steering, SD2_STEER_INPUT only):
+ * for one token sequence x_0..x_{n-1} (tokens: device int32 [n], ids in [0, vocab)) and the
+ * offset of every target (deltas: device int32 [n], deltas[tau] in 1..k, entry 0 unused; the
+ * paper draws them uniformly), writes out_kl (device float [n]):
+ *   out_kl[tau] = KL(p_V || p_D) = sum_v p_V(v) (log p_V(v) - log p_D(v)),  tau = 1..n-1,
+ * p_V the verifier's softmax at position tau-1 and p_D the drafter's, whose input embedding at
+ * every position p carries the steering of the target it predicts, s_{p+1} = W_s hF_V(p -
+ * deltas[p+1]) (zero when that position is negative or the offset lies outside 1..k; hF_V = the
+ * verifier's final-norm hidden state), and out_kl[0] = 0; out_loss (device float [1]) receives the mean over tau = 1..n-1.
+ * Both models run rows_per_chunk positions at a time (1..512) in sequence slot 0 of the
+ * handle's caches, so the handle's generation state is lost (sd2_prefill before the next round).
+ * scratch: device buffer of at least sd2_train_loss_scratch_bytes(cfg, n, rows_per_chunk)
+ * bytes, 256-byte aligned, caller-owned.  Errors: SD2_ERR_UNSUPPORTED for the MLP and unsteered
+ * forms, SD2_ERR_CAPACITY when n > max_seq_len, SD2_ERR_INVALID_ARG otherwise.
+ */
+size_t sd2_train_loss_scratch_bytes(const sd2_config* cfg, int32_t max_len, int32_t rows_per_chunk);
+sd2_status sd2_train_loss(sd2_handle_t h, const int32_t* tokens, const int32_t* deltas, int32_t n,
+                          int32_t rows_per_chunk, float* out_kl, float* out_loss, void* scratch,
+                          size_t scratch_bytes);
+
 /* Destroy a handle (NULL is a no-op).  Does not free caller memory. */
 sd2_status sd2_destroy(sd2_handle_t h);
 

@@ -18,7 +18,8 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "capacity", -3: "state", -4: "hip
 DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V, DBG_PATH, \
     DBG_TRACE, DBG_UBIAS = range(1, 13)
 
-EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_create_noalloc", "sd2_create_mlp", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
+EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_create_noalloc", "sd2_create_mlp", "sd2_train_loss",
+           "sd2_train_loss_scratch_bytes", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
            "sd2_status_string", "sd2_last_error", "sd2_debug_read", "sd2_profile", "sd2_profile_read"]
 PROF_GEMV, PROF_ATTN, PROF_SAMPLER, PROF_OTHER, PROF_PROGRAM = 1, 2, 3, 4, 5
 
@@ -66,6 +67,10 @@ def load():
         lib.sd2_create_noalloc.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights),
                                            P, P, ctypes.POINTER(P)]
         lib.sd2_create_noalloc.restype = ctypes.c_int32
+        lib.sd2_train_loss_scratch_bytes.argtypes = [ctypes.POINTER(Config), ctypes.c_int32, ctypes.c_int32]
+        lib.sd2_train_loss_scratch_bytes.restype = ctypes.c_size_t
+        lib.sd2_train_loss.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32, P, P, P, ctypes.c_size_t]
+        lib.sd2_train_loss.restype = ctypes.c_int32
         lib.sd2_create_mlp.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Weights), ctypes.POINTER(Weights),
                                        ctypes.POINTER(MlpSteering), P, ctypes.c_size_t, P, ctypes.POINTER(P)]
         lib.sd2_create_mlp.restype = ctypes.c_int32
@@ -228,6 +233,26 @@ class Engine:
                                            self.out_counts.data_ptr())
         check(rc, self.h, "sd2_round")
         return self.out_tokens[: self.batch], self.out_counts[: self.batch]
+
+    def train_loss(self, tokens: torch.Tensor, deltas: torch.Tensor, rows_per_chunk: int = 512):
+        """Training-objective forward (sd2_train_loss) over one device token sequence and its
+        offsets: returns (mean KL over targets 1..n-1, per-target KL as numpy [n]).  The handle's
+        generation state is lost (prefill again before a round)."""
+        assert tokens.dtype == torch.int32 and deltas.dtype == torch.int32
+        assert tokens.is_contiguous() and deltas.is_contiguous() and tokens.numel() == deltas.numel()
+        n = tokens.numel()
+        nbytes = self.lib.sd2_train_loss_scratch_bytes(ctypes.byref(self.cfg), n, rows_per_chunk)
+        if nbytes == 0:
+            raise Sd2Error("train_loss: unsupported configuration or sizes")
+        scratch = torch.empty(nbytes + 256, dtype=torch.uint8, device=tokens.device)
+        off = (-scratch.data_ptr()) % 256
+        kl = torch.empty(n, dtype=torch.float32, device=tokens.device)
+        loss = torch.empty(1, dtype=torch.float32, device=tokens.device)
+        check(self.lib.sd2_train_loss(self.h, tokens.data_ptr(), deltas.data_ptr(), n, rows_per_chunk, kl.data_ptr(),
+                                      loss.data_ptr(), scratch.data_ptr() + off, nbytes), self.h, "sd2_train_loss")
+        self.batch = 0
+        torch.cuda.synchronize()
+        return float(loss.item()), kl.cpu().numpy()
 
     def debug(self, what: int) -> np.ndarray:
         B, k = self.batch, self.cfg.k

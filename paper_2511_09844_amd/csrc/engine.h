@@ -152,7 +152,7 @@ void launch_rope_table(hipStream_t s, ModelDev& m, int cap);
 void launch_init_maps(hipStream_t s, Engine& e);
 enum PlanKind { kPlanDraft1 = 0, kPlanDraftJ = 1, kPlanVerify = 2, kPlanPrefill = 3 };
 void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
-                       const int32_t* prompt_len, int max_prompt, int chunk);
+                       const int32_t* prompt_len, int max_prompt, int chunk, const float* row_add = nullptr);
 // ub_map (null: the row's sequence) maps rows to bias rows (the conditional bias: one per row).
 // ubias (drafter rounds with MLP steering): this layer's biases, row stride ub_ld, indexed by
 // the row's sequence, added to the up projection, or to the MLP output when bias_after; null
@@ -223,5 +223,17 @@ void launch_prefill_finish(hipStream_t s, Engine& e, int batch, const int32_t* p
 void launch_rmsnorm_rows(hipStream_t s, const float* X, int rows, int d, const void* gamma, bool bf16, float eps,
                          float* Y);
 void launch_set_flag(hipStream_t s, int32_t* flag, int v);
+
+// Training-objective forward (sd2_train_loss): buffers carved from the caller's scratch.
+struct LossScratch {
+    float* lv;      // [chunk][V] verifier logits of a chunk
+    float* ld;      // [chunk][V] drafter logits of a chunk
+    float* hf;      // [nchunks * chunk + 1][d_V] verifier final-norm hidden rows (last: zeros)
+    float* srow;    // [chunk][d_D] steering of every target of a chunk
+    int32_t* src;   // [chunk] source rows of those steering vectors
+    int32_t* len;   // [1] the sequence length
+};
+void launch_train_loss(hipStream_t s, Engine& e, const int32_t* tokens, const int32_t* deltas, int n, int chunk,
+                       const LossScratch& w, float* out_kl, float* out_loss);
 
 }  // namespace sd2

@@ -192,18 +192,28 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
                     if (p.S > 1) pmax = std::max(pmax, (size_t)p.tiles * p.S * 256);
                 }
         }
-        // many-row GEMM with K ranges: [tile][m block][range][subs][4 x 256] partials
+        // many-row GEMM with K ranges: [tile][m block][range][subs][4 x 256] partials.  Besides the
+        // models' projections: W_s over many rows (the training-objective forward) and the MLP
+        // steering projections at batches above 16 rows
+        const int R = c.steering == SD2_STEER_MLP_COND ? c.cond_rank : 0;
+        const bool mf = mlp_form(c);
         for (int i = 0; i < 2; ++i) {
             const sd2_dims& d = *dd[i];
             int hd = d.d_model / d.n_heads;
-            int shapes[5][3] = {{(d.n_heads + 2 * d.n_kv_heads) * hd, d.d_model, 1},
-                                {d.d_model, d.n_heads * hd, 1},
-                                {d.d_ff, d.d_model, 2},
-                                {d.d_model, d.d_ff, 1},
-                                {d.vocab, d.d_model, 1}};
+            int shapes[10][3] = {{(d.n_heads + 2 * d.n_kv_heads) * hd, d.d_model, 1},
+                                 {d.d_model, d.n_heads * hd, 1},
+                                 {d.d_ff, d.d_model, 2},
+                                 {d.d_model, d.d_ff, 1},
+                                 {d.vocab, d.d_model, 1},
+                                 {c.drafter.d_model, c.verifier.d_model, 1},
+                                 {mf ? c.verifier.d_model : 0, 3 * c.verifier.d_model, 1},
+                                 {mf ? bias_len(c) : 0, c.verifier.d_model, 1},
+                                 {R, c.drafter.d_model, 1},
+                                 {R ? c.drafter.d_ff : 0, R, 1}};
             // the split depends on the rows only through their number of 64-row blocks
             for (int nbm = 1; nbm <= (maxm + 63) / 64; ++nbm)
                 for (auto& sh : shapes) {
+                    if (sh[0] <= 0) continue;
                     int S = pg_split(nbm * 64, sh[0], sh[1], sh[2]);
                     size_t nblkm = (size_t)nbm;
                     if (S > 1) {
@@ -611,6 +621,52 @@ sd2_status sd2_create(const sd2_config* cfg, const sd2_weights* verifier, const 
                       const void* w_steer, void* workspace, size_t workspace_bytes, void* hip_stream,
                       sd2_handle_t* out) {
     return create_impl(cfg, verifier, drafter, w_steer, nullptr, workspace, workspace_bytes, hip_stream, out);
+}
+
+// Training-objective forward: buffers for sequences of n tokens in chunks of `chunk` positions.
+static size_t loss_carve(const sd2_config& c, int n, int chunk, char* base, LossScratch* out) {
+    const int nchunks = (n - 1 + chunk - 1) / chunk;
+    const size_t V = c.verifier.vocab, dV = c.verifier.d_model, dD = c.drafter.d_model;
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char* {
+        char* p = base ? base + off : nullptr;
+        off += (bytes + kAlign - 1) / kAlign * kAlign;
+        return p;
+    };
+    LossScratch w{};
+    w.lv = (float*)take(sizeof(float) * chunk * V);
+    w.ld = (float*)take(sizeof(float) * chunk * V);
+    w.hf = (float*)take(sizeof(float) * ((size_t)nchunks * chunk + 1) * dV);
+    w.srow = (float*)take(sizeof(float) * chunk * dD);
+    w.src = (int32_t*)take(sizeof(int32_t) * chunk);
+    w.len = (int32_t*)take(sizeof(int32_t));
+    if (out) *out = w;
+    return off;
+}
+
+size_t sd2_train_loss_scratch_bytes(const sd2_config* cfg, int32_t max_len, int32_t rows_per_chunk) {
+    if (!config_ok(cfg) || cfg->steering != SD2_STEER_INPUT) return 0;
+    if (max_len < 2 || max_len > cfg->max_seq_len || rows_per_chunk < 1 || rows_per_chunk > kPrefillRows) return 0;
+    return loss_carve(*cfg, max_len, rows_per_chunk, nullptr, nullptr);
+}
+
+sd2_status sd2_train_loss(sd2_handle_t h, const int32_t* tokens, const int32_t* deltas, int32_t n,
+                          int32_t rows_per_chunk, float* out_kl, float* out_loss, void* scratch,
+                          size_t scratch_bytes) {
+    if (!h || !tokens || !deltas || !out_kl || !out_loss || !scratch) return SD2_ERR_INVALID_ARG;
+    Engine* e = reinterpret_cast<Engine*>(h);
+    if (e->cfg.steering != SD2_STEER_INPUT) return SD2_ERR_UNSUPPORTED;
+    if (n < 2 || rows_per_chunk < 1 || rows_per_chunk > kPrefillRows) return SD2_ERR_INVALID_ARG;
+    if (n > e->cap) return SD2_ERR_CAPACITY;
+    if ((uintptr_t)scratch % kAlign || scratch_bytes < loss_carve(e->cfg, n, rows_per_chunk, nullptr, nullptr))
+        return SD2_ERR_INVALID_ARG;
+    LossScratch w;
+    loss_carve(e->cfg, n, rows_per_chunk, (char*)scratch, &w);
+    // the forward runs in sequence slot 0 of both caches: the generation state is gone afterwards
+    e->batch = 1;
+    e->prefilled = false;
+    launch_train_loss(e->stream, *e, tokens, deltas, n, rows_per_chunk, w, out_kl, out_loss);
+    return check_launch(e, "train_loss");
 }
 
 sd2_status sd2_create_noalloc(const sd2_config* cfg, const sd2_weights* verifier, const sd2_weights* drafter,

@@ -54,6 +54,7 @@ struct PlanArgs {
     const int32_t *t, *len_d, *done, *hist, *drafts, *prompt_tok, *prompt_len;
     const float* steer;
     int add_steer;
+    const float* row_add;  // [rows][d] added to every active row's embedding, or null
     int32_t *row_pos, *row_seq;
     float* x;
     float* ss;   // [rows][d/16]
@@ -117,6 +118,7 @@ __global__ __launch_bounds__(256) void k_plan_embed(PlanArgs a) {
             if (active) {
                 v = load_scalar<TW>(er, i);
                 if (a.add_steer) v += sr[i];
+                if (a.row_add) v += a.row_add[(size_t)r * a.d + i];
             }
             xr[i] = v;
             acc += v * v;
@@ -126,8 +128,9 @@ __global__ __launch_bounds__(256) void k_plan_embed(PlanArgs a) {
 }
 
 void launch_plan_embed(hipStream_t s, Engine& e, ModelDev& m, int kind, int j, int rows, const int32_t* prompt_tok,
-                       const int32_t* prompt_len, int max_prompt, int chunk) {
+                       const int32_t* prompt_len, int max_prompt, int chunk, const float* row_add) {
     PlanArgs a;
+    a.row_add = row_add;
     a.kind = kind; a.j = j; a.k = e.cfg.k; a.batch = e.batch; a.cap = e.cap; a.vocab = m.dm.vocab;
     a.d = m.dm.d_model; a.chunk = chunk; a.max_prompt = max_prompt;
     a.t = e.ws.t; a.len_d = e.ws.len_d; a.done = e.ws.done; a.hist = e.ws.hist; a.drafts = e.ws.drafts;
@@ -1067,5 +1070,129 @@ void launch_rmsnorm_rows(hipStream_t s, const float* X, int rows, int d, const v
 
 __global__ void k_set_flag(int32_t* f, int v) { *f = v; }
 void launch_set_flag(hipStream_t s, int32_t* flag, int v) { k_set_flag<<<1, 1, 0, s>>>(flag, v); }
+
+// ===========================================================================
+// Training-objective forward: per-target KL divergence between the verifier and the steered
+// drafter (one kernel per operation; see sd2_train_loss).
+// ===========================================================================
+// Length of the one sequence and the zero row that targets without an earlier steering source read.
+__global__ void k_loss_setup(int32_t* len, int n, float* zero_row, int d) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) *len = n;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) zero_row[i] = 0.0f;
+}
+
+// Source row of every drafter input row of a chunk: the verifier position p - delta[p + 1] whose
+// final-norm hidden state gives the steering of target p + 1, or the zero row (before the sequence
+// start, and for offsets outside 1..k).
+__global__ void k_loss_map(int32_t* src, const int32_t* deltas, int pos0, int rows, int n, int k, int zero_row) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rows) return;
+    const int p = pos0 + r;
+    int q = -1;
+    if (p < n - 1) {
+        const int d = deltas[p + 1];
+        if (d >= 1 && d <= k) q = p - d;
+    }
+    src[r] = q >= 0 ? q : zero_row;
+}
+
+// KL(p_V || p_D) of one row of verifier logits A and drafter logits B (temperature 1), three
+// passes over the vocabulary: maxima, normalisers, then sum_v p_V (log p_V - log p_D).
+__global__ __launch_bounds__(256) void k_kl_rows(const float* A, const float* B, int V, int pos0, int n,
+                                                 float* out_kl) {
+    __shared__ float red[2][4];
+    const int r = blockIdx.x, tau = pos0 + r + 1;
+    if (tau > n - 1) return;
+    const float* a = A + (size_t)r * V;
+    const float* b = B + (size_t)r * V;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    auto block2 = [&](float& x, float& y, bool is_max) {
+        x = is_max ? wave_max(x) : wave_sum(x);
+        y = is_max ? wave_max(y) : wave_sum(y);
+        __syncthreads();
+        if (lane == 0) {
+            red[0][wave] = x;
+            red[1][wave] = y;
+        }
+        __syncthreads();
+        float x0 = red[0][0], y0 = red[1][0];
+        for (int w = 1; w < 4; ++w) {
+            x0 = is_max ? fmaxf(x0, red[0][w]) : x0 + red[0][w];
+            y0 = is_max ? fmaxf(y0, red[1][w]) : y0 + red[1][w];
+        }
+        x = x0;
+        y = y0;
+    };
+    float ma = -INFINITY, mb = -INFINITY;
+    for (int v = threadIdx.x; v < V; v += blockDim.x) {
+        ma = fmaxf(ma, a[v]);
+        mb = fmaxf(mb, b[v]);
+    }
+    block2(ma, mb, true);
+    float za = 0.0f, zb = 0.0f;
+    for (int v = threadIdx.x; v < V; v += blockDim.x) {
+        za += expf(a[v] - ma);
+        zb += expf(b[v] - mb);
+    }
+    block2(za, zb, false);
+    const float lsa = ma + logf(za), lsb = mb + logf(zb);
+    float kl = 0.0f, unused = 0.0f;
+    for (int v = threadIdx.x; v < V; v += blockDim.x) {
+        const float lpa = a[v] - lsa, lpb = b[v] - lsb;
+        kl += expf(lpa) * (lpa - lpb);
+    }
+    block2(kl, unused, false);
+    if (threadIdx.x == 0) out_kl[tau] = kl;
+}
+
+// out_kl[0] = 0 and the mean of out_kl[1 .. n-1].
+__global__ __launch_bounds__(256) void k_loss_finish(float* out_kl, int n, float* out_loss) {
+    __shared__ float red[4];
+    float s = 0.0f;
+    for (int i = 1 + threadIdx.x; i < n; i += blockDim.x) s += out_kl[i];
+    s = wave_sum(s);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        out_kl[0] = 0.0f;
+        *out_loss = (red[0] + red[1] + red[2] + red[3]) / (float)(n - 1);
+    }
+}
+
+void launch_train_loss(hipStream_t s, Engine& e, const int32_t* tokens, const int32_t* deltas, int n, int chunk,
+                       const LossScratch& w, float* out_kl, float* out_loss) {
+    const int dV = e.mv.dm.d_model, dD = e.md.dm.d_model, V = e.mv.dm.vocab;
+    const int nchunks = (n - 1 + chunk - 1) / chunk;
+    const int zero_row = nchunks * chunk;
+    k_loss_setup<<<1, 256, 0, s>>>(w.len, n, w.hf + (size_t)zero_row * dV, dV);
+    for (int c = 0; c < nchunks; ++c) {
+        // verifier over the chunk's positions: its final-norm hidden rows (steering sources) and logits
+        launch_plan_embed(s, e, e.mv, kPlanPrefill, c, chunk, tokens, w.len, n, chunk);
+        for (int l = 0; l < e.mv.dm.n_layers; ++l) launch_layer(s, e, e.mv, l, chunk, chunk);
+        launch_rmsnorm_rows(s, e.mv.x, chunk, dV, e.mv.final_norm, e.bf16, e.mv.dm.rms_eps,
+                            w.hf + (size_t)c * chunk * dV);
+        launch_lm_head(e, e.mv, chunk, w.lv, nullptr);
+        // steering of every target of the chunk: W_s applied to its source row
+        k_loss_map<<<(chunk + 255) / 256, 256, 0, s>>>(w.src, deltas, c * chunk, chunk, n, e.cfg.k, zero_row);
+        if (e.bf16) {
+            WsCall p = ws_base(e, e.mv);
+            p.X = w.hf; p.in_map = w.src; p.M = chunk; p.K = dV;
+            p.W[0] = e.w_steer; p.seg_rows[0] = dD; p.nseg = 1; p.mode = kEpiStore;
+            p.Y = w.srow; p.ldy = dD;
+            launch_wsgemv(&e, s, p);
+        } else {
+            const void* ws[1] = {e.w_steer};
+            int rws[1] = {dD};
+            launch_gemv(&e, s, false, w.hf, w.src, chunk, dV, nullptr, 0.f, ws, rws, 1, kEpiStore, w.srow, dD,
+                        nullptr);
+        }
+        // drafter over the same positions, each input embedding plus its target's steering
+        launch_plan_embed(s, e, e.md, kPlanPrefill, c, chunk, tokens, w.len, n, chunk, w.srow);
+        for (int l = 0; l < e.md.dm.n_layers; ++l) launch_layer(s, e, e.md, l, chunk, chunk);
+        launch_lm_head(e, e.md, chunk, w.ld, nullptr);
+        k_kl_rows<<<chunk, 256, 0, s>>>(w.lv, w.ld, V, c * chunk, n, out_kl);
+    }
+    k_loss_finish<<<1, 256, 0, s>>>(out_kl, n, out_loss);
+}
 
 }  // namespace sd2

@@ -134,3 +134,20 @@ def test_create_noalloc_argument_errors_without_gpu():
     c = B.config_of(si.TINY, steering=B.STEER_MLP)
     assert lib.sd2_create_noalloc(ctypes.byref(c), None, None, None, None, ctypes.byref(h)) == -1
     assert lib.sd2_create_noalloc(ctypes.byref(B.config_of(si.TINY)), None, None, None, None, None) == -1
+
+
+def test_train_loss_scratch_sizes_without_gpu():
+    """Scratch of the training-objective forward: the input form only, 2 <= n <= max_seq_len,
+    1..512 rows per chunk; it grows with the chunk (two logit blocks of chunk x vocab floats)."""
+    lib = B.load()
+    c = B.config_of(si.GQA if hasattr(si, "GQA") else si.TINY)
+    a = lib.sd2_train_loss_scratch_bytes(ctypes.byref(c), 20, 8)
+    b = lib.sd2_train_loss_scratch_bytes(ctypes.byref(c), 20, 16)
+    assert a > 0 and b - a >= 2 * 8 * c.verifier.vocab * 4
+    assert lib.sd2_train_loss_scratch_bytes(ctypes.byref(c), 1, 8) == 0
+    assert lib.sd2_train_loss_scratch_bytes(ctypes.byref(c), c.max_seq_len + 1, 8) == 0
+    assert lib.sd2_train_loss_scratch_bytes(ctypes.byref(c), 20, 0) == 0
+    assert lib.sd2_train_loss_scratch_bytes(ctypes.byref(c), 20, 513) == 0
+    for form in (B.STEER_MLP, B.STEER_NONE):
+        assert lib.sd2_train_loss_scratch_bytes(ctypes.byref(B.config_of(si.TINY, steering=form)), 20, 8) == 0
+    assert lib.sd2_train_loss(None, None, None, 20, 8, None, None, None, 0) == -1
