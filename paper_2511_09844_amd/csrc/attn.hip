@@ -235,6 +235,160 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------------------------
+// Long row blocks (prefill chunks, the training-objective forward): causal flash attention on
+// fp32 matrix cores.  A workgroup owns 16 consecutive query rows of one sequence and one KV
+// head; each of its 4 waves takes the query heads wave, wave + 4, ... of that KV head.  Per
+// 16-position key tile, K and V are staged in LDS once for all the group's heads; a wave forms
+// the 16 x 16 score tile S = Q K^T with v_mfma_f32_16x16x4_f32 over the head dimension, keeps
+// an online softmax per query row (rows are held by groups of 16 lanes in the MFMA result
+// layout), moves P through LDS into the operand layout, and accumulates O += P V with the same
+// instruction, HD/16 output tiles of 16 x 16.  fp32 operands keep the cache's precision.
+// ---------------------------------------------------------------------------------------------
+constexpr int kPaQ = 16;   // query rows per workgroup
+constexpr int kPaK = 16;   // key positions per tile
+typedef float pf4 __attribute__((ext_vector_type(4)));
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_pattn(AttnArgs a) {
+    constexpr int KL = HD + 4;             // padded LDS row of K and V
+    __shared__ float ks[kPaK * KL];
+    __shared__ float vs[kPaK * KL];
+    __shared__ float ps[4][kPaQ][kPaK + 1];  // per wave: P in row-major, read back as the A operand
+    __shared__ int qpos[kPaQ];
+    __shared__ int maxpos_s;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = a.H / a.Hkv;
+    const int nqb = (a.rps + kPaQ - 1) / kPaQ;
+    const int qb = blockIdx.x % nqb;
+    const int kvh = (blockIdx.x / nqb) % a.Hkv;
+    const int b = blockIdx.x / (nqb * a.Hkv);
+    const int i0 = qb * kPaQ;
+    if (tid == 0) maxpos_s = -1;
+    __syncthreads();
+    if (tid < kPaQ) {
+        int p = -1;
+        if (i0 + tid < a.rps) p = a.row_pos[b * a.rps + i0 + tid];
+        qpos[tid] = p;
+        if (p >= 0) atomicMax(&maxpos_s, p);
+    }
+    __syncthreads();
+    const int maxpos = maxpos_s;
+    const size_t kvoff = (((size_t)a.layer * a.max_batch + b) * a.Hkv + kvh) * (size_t)a.cap * HD;
+    const float* kg = a.kc + kvoff;
+    const float* vg = a.vc + kvoff;
+    const int col = lane & 15, grp = lane >> 4;  // MFMA layouts: column / row-group of this lane
+    for (int hp = 0; hp * 4 < G; ++hp) {
+        const int hh = hp * 4 + wave;
+        const bool active = hh < G && maxpos >= 0;
+        const int h = kvh * G + (hh < G ? hh : 0);
+        // Q as the A operand: lane holds Q[row col][4 s + grp], pre-scaled
+        float qf[HD / 4];
+        {
+            const int qrow = i0 + col;
+            const bool ok = qrow < a.rps;
+            const float* qp = a.q + (size_t)(b * a.rps + (ok ? qrow : 0)) * a.q_stride + h * HD;
+#pragma unroll
+            for (int s = 0; s < HD / 4; ++s) qf[s] = ok ? qp[4 * s + grp] * a.scale : 0.f;
+        }
+        pf4 o[HD / 16];
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) o[dt] = pf4{0.f, 0.f, 0.f, 0.f};
+        float mrow[4], lrow[4];
+        int qp4[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            mrow[r] = -INFINITY;
+            lrow[r] = 0.f;
+            qp4[r] = qpos[4 * grp + r];
+        }
+        const int ntile = maxpos >= 0 ? maxpos / kPaK + 1 : 0;
+        for (int kt = 0; kt < ntile; ++kt) {
+            // stage the tile's K and V rows (positions past maxpos: zeros)
+            __syncthreads();
+            for (int e4 = tid; e4 < kPaK * HD / 4; e4 += 256) {
+                const int j = (e4 * 4) / HD, d = (e4 * 4) % HD, pos = kt * kPaK + j;
+                float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
+                if (pos <= maxpos) {
+                    kv = *(const float4*)(kg + (size_t)pos * HD + d);
+                    vv = *(const float4*)(vg + (size_t)pos * HD + d);
+                }
+                *(float4*)(ks + j * KL + d) = kv;
+                *(float4*)(vs + j * KL + d) = vv;
+            }
+            __syncthreads();
+            if (!active) continue;
+            // S = Q K^T: B operand K^T[4 s + grp][key col]
+            pf4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < HD / 4; ++s)
+                sc = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[s], ks[col * KL + 4 * s + grp], sc, 0, 0, 0);
+            // online softmax: this lane holds S[4 grp + r][col]; a row's 16 columns are the 16
+            // lanes of its group
+            const int kpos = kt * kPaK + col;
+            float pr[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool valid = qp4[r] >= 0 && kpos <= qp4[r];
+                const float sv = valid ? sc[r] : -INFINITY;
+                float mx = sv;
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
+                const float mnew = fmaxf(mrow[r], mx);
+                const float p = valid ? expf(sv - mnew) : 0.f;
+                float sum = p;
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 16);
+                const float scl = mrow[r] == -INFINITY ? 0.f : expf(mrow[r] - mnew);
+                lrow[r] = lrow[r] * scl + sum;
+                mrow[r] = mnew;
+#pragma unroll
+                for (int dt = 0; dt < HD / 16; ++dt) o[dt][r] *= scl;
+                pr[r] = p;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) ps[wave][4 * grp + r][col] = pr[r];
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's P writes reached LDS
+            __builtin_amdgcn_wave_barrier();
+            // O += P V: A operand P[row col][4 ks + grp], B operand V[4 ks + grp][16 dt + col]
+#pragma unroll
+            for (int k4 = 0; k4 < kPaK / 4; ++k4) {
+                const float pa = ps[wave][col][4 * k4 + grp];
+                const float* vr = vs + (4 * k4 + grp) * KL + col;
+#pragma unroll
+                for (int dt = 0; dt < HD / 16; ++dt)
+                    o[dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, vr[16 * dt], o[dt], 0, 0, 0);
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+        if (active) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = 4 * grp + r, row = i0 + i;
+                if (row >= a.rps) continue;
+                const float inv = (qp4[r] >= 0 && lrow[r] > 0.f) ? 1.f / lrow[r] : 0.f;
+                float* op = a.out + (size_t)(b * a.rps + row) * a.H * HD + h * HD + col;
+#pragma unroll
+                for (int dt = 0; dt < HD / 16; ++dt) op[16 * dt] = o[dt][r] * inv;
+            }
+        }
+    }
+}
+
+static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) {
+    const int nqb = (a.rps + kPaQ - 1) / kPaQ;
+    dim3 grid(nseq * a.Hkv * nqb);
+    ProfEntry* pe = prof_slot(&e, kProfAttn, 0.0);
+    hipEvent_t ea = pe ? pe->a : nullptr, eb = pe ? pe->b : nullptr;
+    switch (a.hd) {
+        case 32: hipExtLaunchKernelGGL(k_pattn<32>, grid, dim3(256), 0, s, ea, eb, 0, a); break;
+        case 64: hipExtLaunchKernelGGL(k_pattn<64>, grid, dim3(256), 0, s, ea, eb, 0, a); break;
+        case 128: hipExtLaunchKernelGGL(k_pattn<128>, grid, dim3(256), 0, s, ea, eb, 0, a); break;
+        default: e.bad_launch = true; pe = nullptr; break;
+    }
+    if (pe) prof_commit(&e);
+}
+
 static size_t attn_lds(int hd) {
     return sizeof(float) * ((size_t)kAttnQT * hd + (size_t)kAttnCL * (hd + 1) + (size_t)kAttnCL * hd +
                             (size_t)kAttnQT * kAttnCL);
@@ -263,6 +417,11 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
     a.nrt = (rps + rows_per_tile - 1) / rows_per_tile;
     a.ngrp = nseq * dm.n_kv_heads * a.nrt;
     a.scale = 1.0f / sqrtf((float)m.hd);
+    if (rps >= kPaQ) {
+        // long row blocks: flash attention on the matrix cores
+        launch_pattn(e, s, a, nseq);
+        return;
+    }
     int members = G / a.hp;
     a.nsplit = attn_nsplit(e.cap);
     a.part = e.ws.attn_part;
