@@ -13,6 +13,8 @@
 // into one L2 only.
 #include <math.h>
 
+#include <algorithm>
+
 #include <hip/hip_ext.h>
 
 #include "device_common.h"
@@ -236,33 +238,43 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Long row blocks (prefill chunks, the training-objective forward): causal flash attention on
-// fp32 matrix cores.  A workgroup owns 16 consecutive query rows of one sequence and one KV
-// head; each of its 4 waves takes the query heads wave, wave + 4, ... of that KV head.  Per
-// 16-position key tile, K and V are staged in LDS once for all the group's heads; a wave forms
-// the 16 x 16 score tile S = Q K^T with v_mfma_f32_16x16x4_f32 over the head dimension, keeps
-// an online softmax per query row (rows are held by groups of 16 lanes in the MFMA result
-// layout), moves P through LDS into the operand layout, and accumulates O += P V with the same
-// instruction, HD/16 output tiles of 16 x 16.  fp32 operands keep the cache's precision.
+// Blocks of many rows per sequence (verify passes of 8 or more rows, prefill chunks, the
+// training-objective forward): causal flash attention on fp32 matrix cores.  A workgroup owns
+// 16 consecutive query rows of one sequence, one KV head and one span of key tiles; each of its
+// 4 waves takes the query heads wave, wave + 4, ... of that KV head.  Per 16-position key tile,
+// K and V are staged in LDS once for all the group's heads (the next tile is requested into
+// registers while the current one is used); a wave forms the 16 x 16 score tile S = Q K^T with
+// v_mfma_f32_16x16x4_f32 over the head dimension, keeps an online softmax per query row (rows
+// are held by groups of 16 lanes in the MFMA result layout), moves P through LDS into the
+// operand layout, and accumulates O += P V with the same instruction, HD/16 output tiles of
+// 16 x 16.  fp32 operands keep the cache's precision.  With few (sequence, KV head, row block)
+// groups the keys are split into at most 16 spans of span_t tiles (about three workgroups per
+// compute unit): every span writes an un-normalised partial into k_attn's partial buffer and
+// the last span of a group to arrive merges them in span order, all spans' loads at once.
 // ---------------------------------------------------------------------------------------------
-constexpr int kPaQ = 16;   // query rows per workgroup
-constexpr int kPaK = 16;   // key positions per tile
+constexpr int kPaQ = 16;                  // query rows per workgroup
+constexpr int kPaK = 16;                  // key positions per tile
+constexpr int kPaMaxSpans = 16;           // spans per group (one merge batch)
+constexpr int kPaMinRows = 8;             // rows per sequence from which blocks take k_pattn
 typedef float pf4 __attribute__((ext_vector_type(4)));
 
 template <int HD>
-__global__ __launch_bounds__(256) void k_pattn(AttnArgs a) {
-    constexpr int KL = HD + 4;             // padded LDS row of K and V
+__global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t) {
+    constexpr int KL = HD + 4;                            // padded LDS row of K and V
+    constexpr int F4 = (kPaK * HD / 4 + 255) / 256;       // float4 of a K (or V) tile per thread
     __shared__ float ks[kPaK * KL];
     __shared__ float vs[kPaK * KL];
     __shared__ float ps[4][kPaQ][kPaK + 1];  // per wave: P in row-major, read back as the A operand
     __shared__ int qpos[kPaQ];
     __shared__ int maxpos_s;
+    __shared__ int last_flag;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int G = a.H / a.Hkv;
     const int nqb = (a.rps + kPaQ - 1) / kPaQ;
-    const int qb = blockIdx.x % nqb;
-    const int kvh = (blockIdx.x / nqb) % a.Hkv;
-    const int b = blockIdx.x / (nqb * a.Hkv);
+    const int grp_id = blockIdx.x / nspan, sp = blockIdx.x % nspan;
+    const int qb = grp_id % nqb;
+    const int kvh = (grp_id / nqb) % a.Hkv;
+    const int b = grp_id / (nqb * a.Hkv);
     const int i0 = qb * kPaQ;
     if (tid == 0) maxpos_s = -1;
     __syncthreads();
@@ -274,13 +286,30 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a) {
     }
     __syncthreads();
     const int maxpos = maxpos_s;
+    const int ntile_all = maxpos >= 0 ? maxpos / kPaK + 1 : 0;
+    // this workgroup's key tiles: all of them, or one span
+    const int t0 = nspan == 1 ? 0 : sp * span_t;
+    const int t1 = nspan == 1 ? ntile_all : min(ntile_all, t0 + span_t);
     const size_t kvoff = (((size_t)a.layer * a.max_batch + b) * a.Hkv + kvh) * (size_t)a.cap * HD;
     const float* kg = a.kc + kvoff;
     const float* vg = a.vc + kvoff;
     const int col = lane & 15, grp = lane >> 4;  // MFMA layouts: column / row-group of this lane
+    auto fetch = [&](int kt, float4 (&pk)[F4], float4 (&pv)[F4]) {
+#pragma unroll
+        for (int i = 0; i < F4; ++i) {
+            const int e4 = tid + 256 * i;
+            const int j = (e4 * 4) / HD, d = (e4 * 4) % HD, pos = kt * kPaK + j;
+            pk[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            pv[i] = pk[i];
+            if (e4 < kPaK * HD / 4 && pos <= maxpos) {
+                pk[i] = *(const float4*)(kg + (size_t)pos * HD + d);
+                pv[i] = *(const float4*)(vg + (size_t)pos * HD + d);
+            }
+        }
+    };
     for (int hp = 0; hp * 4 < G; ++hp) {
         const int hh = hp * 4 + wave;
-        const bool active = hh < G && maxpos >= 0;
+        const bool active = hh < G && t0 < t1;
         const int h = kvh * G + (hh < G ? hh : 0);
         // Q as the A operand: lane holds Q[row col][4 s + grp], pre-scaled
         float qf[HD / 4];
@@ -302,27 +331,31 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a) {
             lrow[r] = 0.f;
             qp4[r] = qpos[4 * grp + r];
         }
-        const int ntile = maxpos >= 0 ? maxpos / kPaK + 1 : 0;
-        for (int kt = 0; kt < ntile; ++kt) {
-            // stage the tile's K and V rows (positions past maxpos: zeros)
+        float4 pk[F4], pv[F4];
+        if (t0 < t1) fetch(t0, pk, pv);
+        for (int kt = t0; kt < t1; ++kt) {
+            // stage this tile's K and V rows (positions past maxpos are zeros), request the next
             __syncthreads();
-            for (int e4 = tid; e4 < kPaK * HD / 4; e4 += 256) {
-                const int j = (e4 * 4) / HD, d = (e4 * 4) % HD, pos = kt * kPaK + j;
-                float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
-                if (pos <= maxpos) {
-                    kv = *(const float4*)(kg + (size_t)pos * HD + d);
-                    vv = *(const float4*)(vg + (size_t)pos * HD + d);
+#pragma unroll
+            for (int i = 0; i < F4; ++i) {
+                const int e4 = tid + 256 * i;
+                if (e4 < kPaK * HD / 4) {
+                    const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
+                    *(float4*)(ks + j * KL + d) = pk[i];
+                    *(float4*)(vs + j * KL + d) = pv[i];
                 }
-                *(float4*)(ks + j * KL + d) = kv;
-                *(float4*)(vs + j * KL + d) = vv;
             }
             __syncthreads();
+            if (kt + 1 < t1) fetch(kt + 1, pk, pv);
             if (!active) continue;
-            // S = Q K^T: B operand K^T[4 s + grp][key col]
-            pf4 sc = {0.f, 0.f, 0.f, 0.f};
+            // S = Q K^T: B operand K^T[4 s + grp][key col]; four independent accumulation chains
+            pf4 sc4[4];
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) sc4[c4] = pf4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < HD / 4; ++s)
-                sc = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[s], ks[col * KL + 4 * s + grp], sc, 0, 0, 0);
+                sc4[s & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[s], ks[col * KL + 4 * s + grp], sc4[s & 3], 0, 0, 0);
+            const pf4 sc = (sc4[0] + sc4[1]) + (sc4[2] + sc4[3]);
             // online softmax: this lane holds S[4 grp + r][col]; a row's 16 columns are the 16
             // lanes of its group
             const int kpos = kt * kPaK + col;
@@ -361,29 +394,93 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a) {
             }
             __builtin_amdgcn_wave_barrier();
         }
-        if (active) {
+        if (hh < G) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int i = 4 * grp + r, row = i0 + i;
                 if (row >= a.rps) continue;
-                const float inv = (qp4[r] >= 0 && lrow[r] > 0.f) ? 1.f / lrow[r] : 0.f;
-                float* op = a.out + (size_t)(b * a.rps + row) * a.H * HD + h * HD + col;
+                const size_t orow = (size_t)(b * a.rps + row);
+                if (nspan == 1) {
+                    const float inv = (qp4[r] >= 0 && lrow[r] > 0.f) ? 1.f / lrow[r] : 0.f;
+                    float* op = a.out + orow * a.H * HD + h * HD + col;
 #pragma unroll
-                for (int dt = 0; dt < HD / 16; ++dt) op[16 * dt] = o[dt][r] * inv;
+                    for (int dt = 0; dt < HD / 16; ++dt) op[16 * dt] = o[dt][r] * inv;
+                } else {
+                    // un-normalised partial of this span: output, max, sum
+                    float* pp = a.part + ((orow * a.H + h) * a.nsplit + sp) * (HD + 2);
+#pragma unroll
+                    for (int dt = 0; dt < HD / 16; ++dt) store_through(pp + 16 * dt + col, o[dt][r]);
+                    if (col == 0) {
+                        store_through(pp + HD, mrow[r]);
+                        store_through(pp + HD + 1, lrow[r]);
+                    }
+                }
             }
         }
+    }
+    if (nspan == 1) return;
+    // the last span of this group to finish merges the live spans in span order: a thread per
+    // (row, head, 4 dimensions), every span's (max, sum) and output requested at once
+    if (!arrive_last(a.cnt + grp_id, nspan, &last_flag)) return;
+    const int nlive = min(nspan, ntile_all > 0 ? (ntile_all - 1) / span_t + 1 : 0);
+    constexpr int D4 = HD / 4;
+    for (int idx = tid; idx < kPaQ * G * D4; idx += 256) {
+        const int i = idx / (G * D4), hh = (idx / D4) % G, d = (idx % D4) * 4;
+        const int row = i0 + i;
+        if (row >= a.rps) continue;
+        const size_t orow = (size_t)(b * a.rps + row);
+        const int h = kvh * G + hh;
+        float4 res = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (qpos[i] >= 0 && nlive > 0) {
+            const float* pp = a.part + (orow * a.H + h) * a.nsplit * (HD + 2);
+            float m2[kPaMaxSpans], l2[kPaMaxSpans];
+            float4 o2[kPaMaxSpans];
+#pragma unroll
+            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) {
+                const float* e2 = pp + (size_t)min(s2, nlive - 1) * (HD + 2);
+                m2[s2] = e2[HD];
+                l2[s2] = e2[HD + 1];
+                o2[s2] = make_float4(e2[d], e2[d + 1], e2[d + 2], e2[d + 3]);
+            }
+            float M = -INFINITY;
+#pragma unroll
+            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) M = s2 < nlive ? fmaxf(M, m2[s2]) : M;
+            float L = 0.f;
+#pragma unroll
+            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) {
+                const float w = (s2 < nlive && m2[s2] != -INFINITY) ? expf(m2[s2] - M) : 0.f;
+                L += w * l2[s2];
+                res.x += w * o2[s2].x;
+                res.y += w * o2[s2].y;
+                res.z += w * o2[s2].z;
+                res.w += w * o2[s2].w;
+            }
+            const float inv = L > 0.f ? 1.f / L : 0.f;
+            res = make_float4(res.x * inv, res.y * inv, res.z * inv, res.w * inv);
+        }
+        *(float4*)(a.out + orow * a.H * HD + h * HD + d) = res;
     }
 }
 
 static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) {
     const int nqb = (a.rps + kPaQ - 1) / kPaQ;
-    dim3 grid(nseq * a.Hkv * nqb);
+    const int groups = nseq * a.Hkv * nqb;
+    // few groups: split the keys into spans so that the chip holds about three workgroups per
+    // compute unit (at most 16 spans, within the decode kernel's partial buffer and counters)
+    int nspan = 1, span_t = 1;
+    if (groups < 256 && (size_t)groups <= e.ws.attn_cnt_n) {
+        const int tiles = (a.cap + kPaK - 1) / kPaK;
+        nspan = std::min(std::min(kPaMaxSpans, a.nsplit), std::max(1, 768 / groups));
+        span_t = (tiles + nspan - 1) / nspan;
+        nspan = (tiles + span_t - 1) / span_t;
+    }
+    dim3 grid(groups * nspan);
     ProfEntry* pe = prof_slot(&e, kProfAttn, 0.0);
     hipEvent_t ea = pe ? pe->a : nullptr, eb = pe ? pe->b : nullptr;
     switch (a.hd) {
-        case 32: hipExtLaunchKernelGGL(k_pattn<32>, grid, dim3(256), 0, s, ea, eb, 0, a); break;
-        case 64: hipExtLaunchKernelGGL(k_pattn<64>, grid, dim3(256), 0, s, ea, eb, 0, a); break;
-        case 128: hipExtLaunchKernelGGL(k_pattn<128>, grid, dim3(256), 0, s, ea, eb, 0, a); break;
+        case 32: hipExtLaunchKernelGGL(k_pattn<32>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
+        case 64: hipExtLaunchKernelGGL(k_pattn<64>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
+        case 128: hipExtLaunchKernelGGL(k_pattn<128>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
         default: e.bad_launch = true; pe = nullptr; break;
     }
     if (pe) prof_commit(&e);
@@ -417,8 +514,11 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
     a.nrt = (rps + rows_per_tile - 1) / rows_per_tile;
     a.ngrp = nseq * dm.n_kv_heads * a.nrt;
     a.scale = 1.0f / sqrtf((float)m.hd);
-    if (rps >= kPaQ) {
-        // long row blocks: flash attention on the matrix cores
+    a.nsplit = attn_nsplit(e.cap);
+    a.part = e.ws.attn_part;
+    a.cnt = e.ws.attn_cnt;
+    if (rps >= kPaMinRows) {
+        // many rows per sequence: flash attention on the matrix cores
         launch_pattn(e, s, a, nseq);
         return;
     }

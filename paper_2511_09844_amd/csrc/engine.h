@@ -80,6 +80,7 @@ struct Workspace {
     size_t ws_part_n, ws_cnt_n;  // their capacities (floats, counters)
     float* attn_part;
     int32_t* attn_cnt;
+    size_t attn_cnt_n;      // its capacity (counters)
     // MLP steering (null unless cfg.steering == SD2_STEER_MLP)
     float* taps;            // [3][maxm][d_V] verifier residual after the tap blocks (per-operation path)
     float* tapsel;          // [max_batch][3 d_V] [h; m; l] of each sequence's steering row

@@ -253,6 +253,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
             }
         }
         w.attn_cnt = cv.take<int32_t>(gmax);
+        w.attn_cnt_n = gmax;
     }
     if (mlp_form(c)) {
         const size_t dV = c.verifier.d_model;
