@@ -71,7 +71,7 @@ def _load():
         lib.oracle_forward_mlp.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P, P, P]
         lib.oracle_mlp_steer.argtypes = [P, P, P]
         lib.oracle_forward_cond.argtypes = [P, ctypes.c_int, P, ctypes.c_int, P, P, P]
-        lib.oracle_train_loss.argtypes = [P, P, ctypes.c_int, P, P]
+        lib.oracle_train_loss.argtypes = [P, P, ctypes.c_int, P, P, P]
         lib.oracle_train_loss.restype = ctypes.c_double
         lib.oracle_philox.argtypes = [P, u32, u32, P]
         lib.oracle_uniform.argtypes = [u32]
@@ -331,12 +331,15 @@ class Oracle:
         self.lib.oracle_forward_cond(self.h, which, toks.ctypes.data, n, cp, hF.ctypes.data, lg.ctypes.data)
         return hF, lg
 
-    def train_loss(self, toks, deltas):
+    def train_loss(self, toks, deltas, spread=False):
         """Training-objective forward (input-form steering): per-target KL divergences [n] (entry 0
-        is 0) and their mean over targets 1..n-1, for tokens x_0..x_{n-1} and offsets deltas[tau]."""
+        is 0) and their mean over targets 1..n-1, for tokens x_0..x_{n-1} and offsets deltas[tau];
+        with spread=True also E_pV|d - KL| per target (d = log p_V - log p_D)."""
         toks = np.ascontiguousarray(toks, dtype=np.int32)
         deltas = np.ascontiguousarray(deltas, dtype=np.int32)
         assert len(deltas) == len(toks)
         kl = np.zeros(len(toks), dtype=np.float64)
-        mean = self.lib.oracle_train_loss(self.h, toks.ctypes.data, len(toks), deltas.ctypes.data, kl.ctypes.data)
-        return float(mean), kl
+        sp = np.zeros(len(toks), dtype=np.float64)
+        mean = self.lib.oracle_train_loss(self.h, toks.ctypes.data, len(toks), deltas.ctypes.data, kl.ctypes.data,
+                                          sp.ctypes.data if spread else None)
+        return (float(mean), kl, sp) if spread else (float(mean), kl)

@@ -804,9 +804,12 @@ void oracle_forward_cond(const ostate* st, int which, const int32_t* toks, int n
  * logits at position tau-1, where the drafter's input embedding at every position p is
  * E_D[x_p] + s_{p+1}, s_tau = W_s hF_V(tau - deltas[tau] - 1) (zero when that position is
  * negative), hF_V(q) the verifier's final-norm hidden state at position q.  out_kl[0] = 0.
- * Returns the mean of out_kl[1..n-1]; NaN for n < 2.
+ * out_spread (NULL for none) receives sum_v p_V(v) |d_v - E_pV[d]| with d = log p_V - log p_D, the
+ * sensitivity of KL to errors in the verifier's logits.  Returns the mean of out_kl[1..n-1]; NaN
+ * for n < 2.
  */
-double oracle_train_loss(const ostate* st, const int32_t* toks, int n, const int32_t* deltas, double* out_kl) {
+double oracle_train_loss(const ostate* st, const int32_t* toks, int n, const int32_t* deltas, double* out_kl,
+                         double* out_spread) {
     if (n < 2) return NAN;
     int dV = st->V.dm.d_model, dD = st->D.dm.d_model, V = st->V.dm.vocab, m = n - 1;
     double* hF = malloc((size_t)m * dV * sizeof(double));
@@ -846,6 +849,11 @@ double oracle_train_loss(const ostate* st, const int32_t* toks, int n, const int
             kl += exp(lpa) * (lpa - lpb);
         }
         out_kl[p + 1] = kl;
+        if (out_spread) {
+            double spread = 0.0;
+            for (int v = 0; v < V; ++v) spread += exp(a[v] - lsa) * fabs((a[v] - lsa) - (b[v] - lsb) - kl);
+            out_spread[p + 1] = spread;
+        }
         sum += kl;
     }
     free(hF); free(lv); free(hD); free(ld); free(sv);

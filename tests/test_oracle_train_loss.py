@@ -13,6 +13,9 @@ Checked against:
   - drafter == verifier with W_s = 0: the loss is exactly zero;
   - W_s = 0: the loss does not depend on the offsets, bit for bit;
   - the KL divergence is never negative.
+
+The spread E_pV|d - KL| (d = log p_V - log p_D), which scales the GPU parity tolerance, is checked
+against the same PyTorch rows and is zero for self-drafting.
 """
 import numpy as np
 import torch
@@ -47,9 +50,10 @@ def _torch_loss(wl, wv, wd, ws, toks, deltas):
         if q >= 0:
             add[p] = (W @ torch.as_tensor(hF[q])).numpy()
     _, ld = torch_ref.forward(wl.drafter, wd, wl.dtype, toks[:-1], add=add)
-    kl = F.kl_div(F.log_softmax(torch.as_tensor(ld), -1), F.log_softmax(torch.as_tensor(lv), -1),
-                  reduction="none", log_target=True).sum(-1).numpy()
-    return kl
+    lp, lq = F.log_softmax(torch.as_tensor(lv), -1), F.log_softmax(torch.as_tensor(ld), -1)
+    kl = F.kl_div(lq, lp, reduction="none", log_target=True).sum(-1)
+    spread = (lp.exp() * (lp - lq - kl[:, None]).abs()).sum(-1)
+    return kl.numpy(), spread.numpy()
 
 
 def test_loss_matches_torch_kl_div():
@@ -57,19 +61,21 @@ def test_loss_matches_torch_kl_div():
     o, wv, wd, ws = _setup(wl)
     toks, deltas = si.loss_inputs(wl, 24)
     assert deltas[1:].min() >= 1 and deltas[1:].max() <= wl.k and len(set(deltas[1:])) == wl.k
-    mean, kl = o.train_loss(toks, deltas)
-    ref = _torch_loss(wl, wv, wd, ws, toks, deltas)
+    mean, kl, spread = o.train_loss(toks, deltas, spread=True)
+    ref, ref_spread = _torch_loss(wl, wv, wd, ws, toks, deltas)
     assert kl[0] == 0.0
     assert np.abs(kl[1:] - ref).max() < 1e-9 * max(1.0, ref.max())
     assert abs(mean - ref.mean()) < 1e-9 * max(1.0, ref.mean())
+    assert ref_spread.min() > 0
+    assert np.abs(spread[1:] - ref_spread).max() < 1e-9 * max(1.0, ref_spread.max())
 
 
 def test_self_drafting_without_steering_has_zero_loss():
     wl = LOSS.with_(drafter=LOSS.verifier)
     o, _, _, _ = _setup(wl, ws_scale=0, same_models=True)
     toks, deltas = si.loss_inputs(wl, 20)
-    mean, kl = o.train_loss(toks, deltas)
-    assert mean == 0.0 and not kl.any()
+    mean, kl, spread = o.train_loss(toks, deltas, spread=True)
+    assert mean == 0.0 and not kl.any() and not spread.any()
 
 
 def test_zero_steering_makes_the_loss_independent_of_offsets():
