@@ -284,7 +284,8 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
         if (st.max_batch > 0) {
             st.prog_cap = mk_phase_count(c);
             st.prog = cv.take<MkPhase>((size_t)st.prog_cap);
-            st.arena = cv.take<char>(mk_arena_bytes(c, st.max_batch));
+            st.arena_bytes = mk_arena_bytes(c, st.max_batch);
+            st.arena = cv.take<char>(st.arena_bytes);
             st.bar = cv.take<int32_t>(kMkBarInts);
             st.err = cv.take<int32_t>(64);
             st.qc = cv.take<int32_t>((size_t)2 * kMkQcLines * kMkLine);

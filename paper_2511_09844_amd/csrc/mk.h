@@ -86,6 +86,7 @@ struct MkState {
     MkPhase* prog;        // phase lists of all launches
     int prog_cap;         // capacity in phases
     char* arena;          // per-launch activation buffers
+    size_t arena_bytes;   // its size (a recorded program must fit in it)
     int32_t* bar;         // grid-barrier state
     uint32_t bar_gen;     // grid barriers completed so far (a launch adds one per phase after the first,
                           // except attention phases that wait on KV-head counters)

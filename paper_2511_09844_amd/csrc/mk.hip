@@ -1451,7 +1451,8 @@ bool mk_build(Engine& e, int batch) {
         Arena ar{s.arena, 0};
         s.off[j] = (int)prog.size();
         if (!mk_record(c, e.md, false, j == 1 ? 2 * batch : batch, j == 1 ? 2 : 1, j, s.G, ar, &e.ws, &prog, &lds,
-                       s.cnt, nullptr, nullptr, &s.bytes[j]))
+                       s.cnt, nullptr, nullptr, &s.bytes[j]) ||
+            ar.off > s.arena_bytes)
             return false;
         s.n[j] = (int)prog.size() - s.off[j];
     }
@@ -1459,7 +1460,8 @@ bool mk_build(Engine& e, int batch) {
         Arena ar{s.arena, 0};
         s.off[0] = (int)prog.size();
         if (!mk_record(c, e.mv, true, batch * (c.k + 1), c.k + 1, 0, s.G, ar, &e.ws, &prog, &lds, s.cnt, &s.final_x,
-                       &s.final_ss, &s.bytes[0], s.tap_x))
+                       &s.final_ss, &s.bytes[0], s.tap_x) ||
+            ar.off > s.arena_bytes)
             return false;
         s.n[0] = (int)prog.size() - s.off[0];
     }
