@@ -336,17 +336,22 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
 }
 
 // ===========================================================================
-// Many-row projections (prefill chunks, large batches): an MFMA GEMM.  A workgroup computes 64
-// activation rows (4 groups of 16) against 8 weight sub-tiles of 16 rows (two per wave), walking
-// K in steps of 256 columns: the step's weight fragments are requested first, the activation
-// slice is staged in LDS as hi/lo bf16 planes (gain applied, as in k_wsgemv), then every weight
-// fragment meets all 4 row groups.  Epilogues are k_wsgemv's, per 16-row group.
+// Many-row projections (prefill chunks, large batches, verify passes of more than 16 rows): an
+// MFMA GEMM.  A workgroup computes 64 activation rows (4 groups of 16) against 8 weight sub-tiles
+// of 16 rows (two per wave), walking K in steps of 128 columns through a two-deep pipeline: the
+// activation slice of step i + 1 sits in the second of two LDS buffers (hi/lo bf16 planes, gain
+// applied, as in k_wsgemv) and its weight fragments in a second register set while step i's
+// MFMAs run, and the loads of step i + 2 are issued as soon as step i + 1's activations have been
+// staged.  Every weight fragment meets all 4 row groups.  Epilogues are k_wsgemv's, per 16-row
+// group.
 // ===========================================================================
 constexpr int kPgRows = 64;           // activation rows per workgroup
 constexpr int kPgTW = 2;              // weight sub-tiles per wave
-constexpr int kPgKC = 256;            // K columns per step
+constexpr int kPgKC = 128;            // K columns per step
 constexpr int kPgLdk = kPgKC + 8;     // padded LDS row stride (bf16 elements)
-constexpr size_t kPgLds = 2 * kPgRows * kPgLdk * 2;  // hi and lo planes (also holds the 32 KB of results)
+constexpr int kPgX4 = kPgRows * kPgKC / 4 / 256;  // float4 of a step's activation slice per thread
+constexpr size_t kPgPlane = (size_t)kPgRows * kPgLdk;           // bf16 elements of one plane
+constexpr size_t kPgLds = 2 * 2 * kPgPlane * 2;  // two buffers of hi and lo planes (also holds the 32 KB of results)
 static_assert(kPgLds >= 4 * kPgTW * 4 * 256 * 4, "result staging must fit the activation planes");
 
 // K ranges for a many-row projection: split while the grid stays within 2 workgroups per CU and
@@ -363,12 +368,12 @@ int pg_split(int M, int N, int K, int subs) {
 }
 
 template <int SUBS>
-__global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
+__global__ __launch_bounds__(256, 2) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ float inv_rms[kPgRows];
     __shared__ int src_row[kPgRows];
-    __shared__ int last_flag;
     constexpr int NT = 4 * kPgTW / SUBS;  // 16-row output tiles per workgroup
+    __shared__ int last_tile[NT];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = lane & 15, q = lane >> 4;
     // block -> (n block, m block): workgroups are dealt to the 8 XCDs in turn, so blocks b, b + 8,
@@ -392,16 +397,6 @@ __global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
         inv_rms[tid] = 1.0f;
     }
     __syncthreads();
-    if (a.gamma) {
-        for (int m = wave; m < kPgRows; m += 4) {
-            const int src = src_row[m];
-            float sm = 0.0f;
-            if (src >= 0)
-                for (int t = lane; t < a.nss; t += 64) sm += a.ss[(size_t)src * a.nss + t];
-            sm = wave_sum(sm);
-            if (lane == 0) inv_rms[m] = rsqrtf(sm / (float)a.K + a.eps);
-        }
-    }
     // this wave's sub-tiles: SwiGLU waves 0, 1 take gate rows and waves 2, 3 the up rows of the
     // same features; a tile past the end is read clamped and never written
     const int sub = SUBS == 2 ? wave >> 1 : 0;
@@ -411,54 +406,63 @@ __global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
         const int tile = tile0 + (SUBS == 2 ? (wave & 1) * kPgTW : wave * kPgTW) + j;
         wrow[j] = tile_row(a, min(tile, a.tiles - 1), sub, n) + 16 * q;
     }
-    uint16_t* xh = (uint16_t*)smem;
-    uint16_t* xl = xh + kPgRows * kPgLdk;
+    uint16_t* const planes = (uint16_t*)smem;  // [buffer][hi, lo][64][kPgLdk]
     floatx4_t acc[kPgTW][4];
 #pragma unroll
     for (int j = 0; j < kPgTW; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) acc[j][g] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-    const int KS = a.K / a.S;
-    for (int k0 = s * KS; k0 < (s + 1) * KS; k0 += kPgKC) {
-        u32x4_t w[kPgTW][4][2];
+    const int KS = a.K / a.S, kb = s * KS, nstep = KS / kPgKC;
+    typedef u32x4_t WFrag[kPgTW][2][2];
+    // weight fragments of step i: lane (n, q) holds row n of each sub-tile, columns
+    // 64 st + 16 q + 8 h + [0, 8) of the step (A is read with the same column order)
+    auto load_w = [&](int i, WFrag& w) {
+        const int k0 = kb + i * kPgKC;
 #pragma unroll
         for (int j = 0; j < kPgTW; ++j)
 #pragma unroll
-            for (int st = 0; st < 4; ++st)
+            for (int st = 0; st < 2; ++st)
 #pragma unroll
                 for (int h = 0; h < 2; ++h) w[j][st][h] = *(const u32x4_t*)(wrow[j] + k0 + st * 64 + 8 * h);
-        // 64 rows x 256 columns of fp32 activations: 16 float4 per thread, row-major
-        float4 xv[16];
+    };
+    // 64 rows x 128 columns of fp32 activations: kPgX4 float4 per thread, row-major (a thread's
+    // float4 all sit at the same 4 columns, so it needs one word pair of the gain per step,
+    // requested with them)
+    const int kk_t = (tid & 31) * 4;
+    auto load_x = [&](int i, float4 (&xv)[kPgX4], uint2& gw) {
+        const int k0 = kb + i * kPgKC;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int idx = tid + i * 256;
-            const int m = idx >> 6, kk = (idx & 63) * 4;
+        for (int e = 0; e < kPgX4; ++e) {
+            const int m = (tid + e * 256) >> 5;
             const int src = src_row[m];
-            xv[i] = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+            xv[e] = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk_t) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        __syncthreads();  // the previous step's MFMAs have read the planes
+        gw = a.gamma ? *(const uint2*)(a.gamma + k0 + kk_t) : make_uint2(0x3f803f80u, 0x3f803f80u);
+    };
+    // gain, then the hi/lo bf16 split of step i's slice into buffer (i & 1)
+    auto stage = [&](int i, const float4 (&xv)[kPgX4], uint2 gw) {
+        uint16_t* xh = planes + (size_t)(i & 1) * 2 * kPgPlane;
+        uint16_t* xl = xh + kPgPlane;
+        const float gm[4] = {bf16_lo(gw.x), bf16_hi(gw.x), bf16_lo(gw.y), bf16_hi(gw.y)};
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int idx = tid + i * 256;
-            const int m = idx >> 6, kk = (idx & 63) * 4;
-            float gm[4] = {1.f, 1.f, 1.f, 1.f};
-            if (a.gamma) {
-                uint2 gw = *(const uint2*)(a.gamma + k0 + kk);
-                gm[0] = bf16_lo(gw.x); gm[1] = bf16_hi(gw.x); gm[2] = bf16_lo(gw.y); gm[3] = bf16_hi(gw.y);
-            }
-            const float vv[4] = {xv[i].x * gm[0], xv[i].y * gm[1], xv[i].z * gm[2], xv[i].w * gm[3]};
+        for (int e = 0; e < kPgX4; ++e) {
+            const int m = (tid + e * 256) >> 5, kk = kk_t;
+            const float vv[4] = {xv[e].x * gm[0], xv[e].y * gm[1], xv[e].z * gm[2], xv[e].w * gm[3]};
             uint16_t hi[4], lo[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                hi[e] = f32_to_bf16_rne(vv[e]);
-                lo[e] = f32_to_bf16_rne(vv[e] - bf16_to_f32(hi[e]));
+            for (int c = 0; c < 4; ++c) {
+                hi[c] = f32_to_bf16_rne(vv[c]);
+                lo[c] = f32_to_bf16_rne(vv[c] - bf16_to_f32(hi[c]));
             }
             *(uint2*)(xh + m * kPgLdk + kk) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
             *(uint2*)(xl + m * kPgLdk + kk) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
         }
-        __syncthreads();
+    };
+    auto mma = [&](int i, const WFrag& w) {
+        const uint16_t* xh = planes + (size_t)(i & 1) * 2 * kPgPlane;
+        const uint16_t* xl = xh + kPgPlane;
 #pragma unroll
-        for (int st = 0; st < 4; ++st) {
+        for (int st = 0; st < 2; ++st) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int kk = st * 64 + 16 * q + 8 * h;
@@ -475,6 +479,56 @@ __global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
                 }
             }
         }
+    };
+    // Pipeline: step i's MFMAs (weights wa for even i, wb for odd), then step i + 1's activations
+    // staged into the other buffer, then the loads of step i + 2 into the registers just freed;
+    // one barrier per step (a buffer is rewritten only after every wave has passed the barrier
+    // that follows its last read).
+    WFrag wa, wb;
+    float4 xv[kPgX4];
+    uint2 gw;
+    load_x(0, xv, gw);
+    load_w(0, wa);
+    // RMSNorm statistics (used by the epilogue only), requested behind the first step's loads:
+    // four threads per row, each summing every fourth float4 of the row's partial sums of squares
+    if (a.gamma) {
+        const int m = tid >> 2, p = tid & 3;
+        const int src = src_row[m];
+        float sm = 0.0f;
+        if (src >= 0) {
+            const float4* sp = (const float4*)(a.ss + (size_t)src * a.nss);
+#pragma unroll 8
+            for (int f = p; f < a.nss / 4; f += 4) {
+                const float4 v = sp[f];
+                sm += (v.x + v.y) + (v.z + v.w);
+            }
+        }
+        sm += __shfl_xor(sm, 1, 4);
+        sm += __shfl_xor(sm, 2, 4);
+        if (p == 0) inv_rms[m] = rsqrtf(sm / (float)a.K + a.eps);
+    }
+    stage(0, xv, gw);
+    if (nstep > 1) {
+        load_x(1, xv, gw);
+        load_w(1, wb);
+    }
+    __syncthreads();
+    for (int i = 0; i < nstep; i += 2) {
+        mma(i, wa);
+        if (i + 1 < nstep) stage(i + 1, xv, gw);
+        if (i + 2 < nstep) {
+            load_x(i + 2, xv, gw);
+            load_w(i + 2, wa);
+        }
+        __syncthreads();
+        if (i + 1 >= nstep) break;
+        mma(i + 1, wb);
+        if (i + 2 < nstep) stage(i + 2, xv, gw);
+        if (i + 3 < nstep) {
+            load_x(i + 3, xv, gw);
+            load_w(i + 3, wb);
+        }
+        __syncthreads();
     }
     __syncthreads();  // planes free: results go to LDS, slot (wave * TW + j, group g)
     float* red = (float*)smem;
@@ -487,37 +541,77 @@ __global__ __launch_bounds__(256) void k_pgemm(WsArgs a, int nblk_m, int nbs) {
     __syncthreads();
     // per output tile and row group: element (m, c) at thread 16 m + c; SwiGLU's up value of
     // local tile lt sits 2 TW slots after its gate value.  With K ranges, each range stores its
-    // sums of (tile, m block) and the last to arrive adds the S partials in range order.
-    for (int lt = 0; lt < NT; ++lt) {
-        const int tile = tile0 + lt;
-        if (tile >= a.tiles) break;
-        float* pt = nullptr;
-        if (a.S > 1) {
-            pt = a.part + (size_t)(tile * nblk_m + mb) * a.S * SUBS * 1024;
+    // sums of every (tile, m block) it holds, waits once for all of those stores, and counts in on
+    // all of its tiles at once; the last range to arrive at a tile adds the S partials in range
+    // order.
+    if (a.S > 1) {
+        for (int lt = 0; lt < NT; ++lt) {
+            const int tile = tile0 + lt;
+            if (tile >= a.tiles) break;
+            float* pt = a.part + (size_t)(tile * nblk_m + mb) * a.S * SUBS * 1024;
 #pragma unroll
             for (int sub = 0; sub < SUBS; ++sub)
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
                     store_through(pt + ((size_t)s * SUBS + sub) * 1024 + g * 256 + tid,
                                   red[((lt + sub * 2 * kPgTW) * 4 + g) * 256 + tid]);
-            if (!arrive_last(a.cnt + tile * nblk_m + mb, a.S, &last_flag)) continue;
+        }
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's stores have completed
+        __syncthreads();
+        if (tid < NT) {
+            const int tile = tile0 + tid;
+            int last = 0;
+            if (tile < a.tiles) {
+                int32_t* c = a.cnt + tile * nblk_m + mb;
+                const int prev = __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                last = prev == a.S - 1;
+                if (last) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            last_tile[tid] = last;
+        }
+        __syncthreads();
+    }
+    for (int lt = 0; lt < NT; ++lt) {
+        const int tile = tile0 + lt;
+        if (tile >= a.tiles) break;
+        if (a.S > 1 && !last_tile[lt]) continue;
+        float sum[4][SUBS];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int sub = 0; sub < SUBS; ++sub) sum[g][sub] = red[((lt + sub * 2 * kPgTW) * 4 + g) * 256 + tid];
+        if (a.S > 1) {
+            // the S ranges' partials of all 4 row groups, 8 ranges per round trip (loads past S
+            // re-read the last range and are not added)
+            const float* pt = a.part + (size_t)(tile * nblk_m + mb) * a.S * SUBS * 1024 + tid;
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int sub = 0; sub < SUBS; ++sub) sum[g][sub] = 0.f;
+            for (int s0 = 0; s0 < a.S; s0 += 8) {
+                float p[8][4][SUBS];
+#pragma unroll
+                for (int r = 0; r < 8; ++r)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+#pragma unroll
+                        for (int sub = 0; sub < SUBS; ++sub)
+                            p[r][g][sub] = pt[((size_t)min(s0 + r, a.S - 1) * SUBS + sub) * 1024 + g * 256];
+#pragma unroll
+                for (int r = 0; r < 8; ++r)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+#pragma unroll
+                        for (int sub = 0; sub < SUBS; ++sub) sum[g][sub] += s0 + r < a.S ? p[r][g][sub] : 0.f;
+            }
         }
         for (int g = 0; g < 4; ++g) {
             const int row0 = m0 + g * 16;
             if (row0 >= M) break;
             const float sc = inv_rms[g * 16 + (tid >> 4)];
-            float v[2] = {0.f, 0.f};
-            if (a.S > 1) {
-                for (int s0 = 0; s0 < a.S; ++s0) {
-                    v[0] += pt[((size_t)s0 * SUBS) * 1024 + g * 256 + tid];
-                    if (SUBS == 2) v[1] += pt[((size_t)s0 * SUBS + 1) * 1024 + g * 256 + tid];
-                }
-            } else {
-                v[0] = red[(lt * 4 + g) * 256 + tid];
-                if (SUBS == 2) v[1] = red[((lt + 2 * kPgTW) * 4 + g) * 256 + tid];
-            }
-            v[0] *= sc;
-            v[1] = SUBS == 2 ? v[1] * sc : v[0];
+            float v[2];
+            v[0] = sum[g][0] * sc;
+            v[1] = SUBS == 2 ? sum[g][SUBS - 1] * sc : v[0];
             tile_epilogue<SUBS>(a, tile, v, row0, min(16, M - row0));
         }
     }
