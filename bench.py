@@ -126,22 +126,30 @@ def _trace_rows(path):
 
 
 def summarize_trace(path):
-    """Per-kernel launches and time per round from a rocprofv3 kernel trace of this script (rounds
-    are counted by k_set_flag, the first kernel of every round; prefill kernels are listed with the
-    rest, under their own names)."""
-    per, rounds = {}, 0
+    """Per-kernel launches and time from a rocprofv3 kernel trace of this script, rounds apart from
+    the rest: a round runs from k_set_flag (its first kernel) to k_commit (its last); every other
+    launch (prefill, set-up) is listed in a second table."""
+    per = {True: {}, False: {}}
+    rounds, in_round = 0, False
     for name, start, end in _trace_rows(path):
         if "k_set_flag" in name:
             rounds += 1
+            in_round = True
         key = name.split("(")[0].replace("void ", "").replace("sd2::", "")
-        c = per.setdefault(key, [0, 0])
+        c = per[in_round].setdefault(key, [0, 0])
         c[0] += 1
         c[1] += end - start
-    print(f"{rounds} rounds in the trace")
-    for key, (n, ns) in sorted(per.items(), key=lambda x: -x[1][1])[:20]:
-        print(f"  {key[:40]:40s} {n:7d} launches {n / max(1, rounds):6.2f}/round  {ns / 1e6:10.2f} ms total  "
-              f"avg {ns / n / 1e3:9.2f} us")
-    mk = [v for k, v in per.items() if k.startswith("k_mk<")]
+        if "k_commit" in name:
+            in_round = False
+    for inside, title in ((True, f"{rounds} rounds in the trace; kernels inside rounds"),
+                          (False, "kernels outside rounds (prefill, set-up)")):
+        tab = per[inside]
+        tot = sum(v[1] for v in tab.values())
+        print(f"{title}: {tot / 1e6:.2f} ms" + (f", {tot / 1e6 / max(1, rounds):.3f} ms/round" if inside else ""))
+        for key, (n, ns) in sorted(tab.items(), key=lambda x: -x[1][1])[:20]:
+            print(f"  {key[:40]:40s} {n:7d} launches {n / max(1, rounds):6.2f}/round  {ns / 1e6:10.2f} ms total  "
+                  f"avg {ns / n / 1e3:9.2f} us")
+    mk = [v for k, v in per[True].items() if k.startswith("k_mk<")]
     if mk:
         n, ns = sum(v[0] for v in mk), sum(v[1] for v in mk)
         print(f"k_mk, all instances: {n} launches, average {ns / n / 1e3:.2f} us")
@@ -201,6 +209,32 @@ def stored_traffic(workload):
     if rec.get("workload") != workload or rec.get("source_sha256") != _source_hash():
         return None
     return rec.get("traffic_bytes_per_launch")
+
+
+def phase_table(trace, wl, path):
+    """Per-phase times of one profiled round of the persistent path, from SD2_DBG_TRACE (device clock
+    at 100 MHz as seen by workgroup 0: entry 0 the start of launch j, entry p + 1 the end of its
+    phase p).  Phases of a launch: per layer Q|K|V (+ RoPE, cache append; layer 0 also stages the
+    embedding), attention, O, gate|up, down, then the LM head.  Writes a markdown table."""
+    import numpy as np
+    kinds = ["qkv", "attn", "o", "gu", "down"]
+    lines = ["| launch | total us | " + " | ".join(f"{k} us (median per layer)" for k in kinds) + " | LM head us |",
+             "|---|---|" + "---|" * len(kinds) + "---|"]
+    for j in range(0, wl.k + 1):
+        L = wl.verifier.n_layers if j == 0 else wl.drafter.n_layers
+        n = 5 * L + 1
+        t = trace[j, : n + 1].astype(np.float64) / 100.0
+        if not (t[1:] >= t[:-1]).all() or t[-1] <= t[0]:
+            continue
+        d = np.diff(t)
+        per = [np.median(d[i : 5 * L : 5]) for i in range(5)]
+        name = "verify pass (k_mk<128>)" if j == 0 else f"drafter step {j} (k_mk<64>)"
+        lines.append(f"| {name} | {t[-1] - t[0]:.1f} | " + " | ".join(f"{v:.2f}" for v in per) + f" | {d[-1]:.2f} |")
+    txt = "\n".join(lines) + "\n"
+    log("phase trace:\n" + txt)
+    if path:
+        with open(path, "w") as f:
+            f.write(txt)
 
 
 def cpu_model():
@@ -305,6 +339,9 @@ def main():
     ap.add_argument("--calib-copy", action="store_true",
                     help="after the rounds, copy one 1 GiB buffer (a plain copy of known size, the reference "
                          "point for scaling hardware traffic counters)")
+    ap.add_argument("--phase-trace", metavar="PATH",
+                    help="after the timed generations, profile one round of the persistent path and write its "
+                         "per-phase times (SD2_DBG_TRACE) as a markdown table to PATH")
     ap.add_argument("--maps-out", metavar="PATH",
                     help="write this process's /proc/self/maps to PATH after teardown (resolves the frames "
                          "of a crash at exit)")
@@ -407,6 +444,14 @@ def main():
                 kv_prof += gb[r][1]
             eng.profile(False)
         torch.cuda.synchronize()
+        if args.phase_trace and int(eng.debug(B.DBG_PATH)[0]) == 1:
+            # one round of a fresh generation at its prompt's length, every phase timed on device
+            eng.prefill(t_tok, t_len, wl.max_prompt)
+            eng.profile(True)
+            eng.round()
+            eng.profile(False)
+            torch.cuda.synchronize()
+            phase_table(eng.debug(B.DBG_TRACE), wl, args.phase_trace)
         # steering overhead: the same generation with the unsteered (pretrained) drafter
         overhead = None
         if not args.no_steer_overhead:
