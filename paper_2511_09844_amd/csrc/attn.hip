@@ -24,7 +24,6 @@ namespace sd2 {
 
 constexpr int kAttnCL = 64;   // cache positions per chunk
 constexpr int kSplit = 128;   // cache positions per workgroup
-constexpr int kMaxSplit = 64; // spans per query vector (cache capacity up to 8192 positions)
 constexpr int kAttnQT = 32;   // query vectors per workgroup
 constexpr int kAttnT = 256;
 constexpr int kXcds = 8;
@@ -208,28 +207,33 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
         float res = 0.f;
         if (pos >= 0) {
             const float* pp = a.part + ((size_t)qrow[qi] * a.H + qhead[qi]) * a.nsplit * (HD + 2);
-            float mv[kMaxSplit], lv[kMaxSplit], ov[kMaxSplit];
+            // batches of 16 spans, every load of a batch issued before any is used (loads past
+            // nlive re-read the last live span and are not added; a load behind a "live" test
+            // would cost one memory round trip each), folded into a running maximum and sums
+            float M = -INFINITY, L = 0.f, O = 0.f;
+            for (int s0 = 0; s0 < nlive; s0 += 16) {
+                float mv[16], lv[16], ov[16];
 #pragma unroll
-            for (int s2 = 0; s2 < kMaxSplit; ++s2) {
-                if (s2 < nlive) {
-                    const float* e = pp + (size_t)s2 * (HD + 2);
-                    mv[s2] = e[HD];
-                    lv[s2] = e[HD + 1];
-                    ov[s2] = e[d];
+                for (int i = 0; i < 16; ++i) {
+                    const float* e = pp + (size_t)min(s0 + i, nlive - 1) * (HD + 2);
+                    mv[i] = e[HD];
+                    lv[i] = e[HD + 1];
+                    ov[i] = e[d];
                 }
-            }
-            float M = -INFINITY;
+                float Mn = M;
 #pragma unroll
-            for (int s2 = 0; s2 < kMaxSplit; ++s2)
-                if (s2 < nlive) M = fmaxf(M, mv[s2]);
-            float L = 0.f, O = 0.f;
+                for (int i = 0; i < 16; ++i) Mn = s0 + i < nlive ? fmaxf(Mn, mv[i]) : Mn;
+                const float sc = M == -INFINITY ? 0.f : expf(M - Mn);
+                L *= sc;
+                O *= sc;
 #pragma unroll
-            for (int s2 = 0; s2 < kMaxSplit; ++s2) {
-                if (s2 < nlive && mv[s2] != -INFINITY) {
-                    float w = expf(mv[s2] - M);
-                    L += w * lv[s2];
-                    O += w * ov[s2];
+                for (int i = 0; i < 16; ++i) {
+                    const bool live = s0 + i < nlive && mv[i] != -INFINITY;
+                    const float w = live ? expf(mv[i] - Mn) : 0.f;
+                    L += w * lv[i];
+                    O += w * ov[i];
                 }
+                M = Mn;
             }
             res = L > 0.f ? O / L : 0.f;
         }
@@ -248,7 +252,7 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
 // are held by groups of 16 lanes in the MFMA result layout), moves P through LDS into the
 // operand layout, and accumulates O += P V with the same instruction, HD/16 output tiles of
 // 16 x 16.  fp32 operands keep the cache's precision.  With few (sequence, KV head, row block)
-// groups the keys are split into at most 16 spans of span_t tiles (about three workgroups per
+// groups the keys are split into at most 16 spans of span_t tiles (about eight workgroups per
 // compute unit): every span writes an un-normalised partial into k_attn's partial buffer and
 // the last span of a group to arrive merges them in span order, all spans' loads at once.
 // ---------------------------------------------------------------------------------------------
@@ -465,12 +469,13 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t
 static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) {
     const int nqb = (a.rps + kPaQ - 1) / kPaQ;
     const int groups = nseq * a.Hkv * nqb;
-    // few groups: split the keys into spans so that the chip holds about three workgroups per
-    // compute unit (at most 16 spans, within the decode kernel's partial buffer and counters)
+    // few groups: split the keys into spans for about 2048 workgroups, eight per compute unit,
+    // since spans past a sequence's length exit at once (at most 16 spans, within the decode
+    // kernel's partial buffer and counters)
     int nspan = 1, span_t = 1;
     if (groups < 256 && (size_t)groups <= e.ws.attn_cnt_n) {
         const int tiles = (a.cap + kPaK - 1) / kPaK;
-        nspan = std::min(std::min(kPaMaxSpans, a.nsplit), std::max(1, 768 / groups));
+        nspan = std::min(std::min(kPaMaxSpans, a.nsplit), std::max(1, 2048 / groups));
         span_t = (tiles + nspan - 1) / nspan;
         nspan = (tiles + span_t - 1) / span_t;
     }

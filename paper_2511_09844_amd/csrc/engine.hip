@@ -66,7 +66,7 @@ bool config_ok(const sd2_config* c) {
     if (c->k < 1 || c->k > kMaxK) return false;
     if (c->max_batch < 1 || c->max_batch > 256) return false;
     if (c->max_new_tokens < 1) return false;
-    if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // 8192 = 64 spans of 128
+    if (c->max_seq_len < c->k + 3 || c->max_seq_len > 8192) return false;  // the capacity the kernels are tested to
     if (!(c->temperature >= 0.f) || c->temperature > 1e4f) return false;
     if (c->steering != SD2_STEER_INPUT && c->steering != SD2_STEER_MLP && c->steering != SD2_STEER_MLP_OUT &&
         c->steering != SD2_STEER_NONE && c->steering != SD2_STEER_MLP_COND)

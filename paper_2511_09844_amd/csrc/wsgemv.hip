@@ -624,6 +624,10 @@ hipError_t wsgemv_setup() {
 }
 
 constexpr int kLdsBudget = 160 * 1024 - 2048;
+// Activation bytes a workgroup stages: K is split until each workgroup's slice of the rows fits
+// this (16 rows of 2048 columns would be 128 KB read from L2 by every workgroup for one 64 KB
+// weight tile, at one workgroup per CU); without such a split, the smallest that fits LDS.
+constexpr size_t kWsStageMax = 64 * 1024;
 
 static size_t lds_bytes(int rows, int KR, int NW) {
     return (size_t)rows * (KR + 8) * 2 * 2 + (size_t)NW * 256 * 4;
@@ -636,10 +640,13 @@ WsPlan ws_plan(int M, int N, int K, int mode) {
     int rows = M < 16 ? M : 16;
     (void)mode;
     p.tiles = N / 16;
+    // first pass: the smallest split whose staged slice fits kWsStageMax; second: any that fits
+    for (int pass = 0; pass < 2 && !p.S; ++pass)
     for (int S = 1; S <= K / 256; ++S) {
         if (K % S) continue;
         int KR = K / S;
         if (KR % 256) continue;
+        if (pass == 0 && (size_t)rows * KR * 4 > kWsStageMax) continue;
         // waves: each a multiple of 64 columns; two fragment buffers of 8*steps VGPRs each must
         // leave room in the 512-entry register file (8 steps with <= 8 waves, 4 with 16 waves)
         int NW = 0, steps = 0;
