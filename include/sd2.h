@@ -258,6 +258,9 @@ const char* sd2_last_error(sd2_handle_t h);
 #define SD2_DBG_UBIAS 12      /* float [batch][L_D][d_ff_D]: current up-projection biases (SD2_STEER_MLP),
                                  float [batch][d_D]: the bias after every MLP (SD2_STEER_MLP_OUT);
                                  SD2_ERR_STATE for SD2_STEER_INPUT */
+#define SD2_DBG_NONFINITE 13  /* int32 [1]: 1 if a verifier or drafter logit of a round since the last read of
+                                 this selector was a NaN or an infinity (every logit the round's decisions use
+                                 is checked as the sampler reads it), else 0; the read clears it */
 
 /* Copy a debug buffer of the last round into host memory dst (bytes must match). */
 sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t bytes);

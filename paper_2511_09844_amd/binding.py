@@ -16,7 +16,7 @@ P = ctypes.c_void_p
 SD2_OK = 0
 STATUS = {0: "ok", -1: "invalid argument", -2: "capacity", -3: "state", -4: "hip error", -5: "unsupported"}
 DBG_LOGITS_V, DBG_LOGITS_D, DBG_STEER, DBG_OWN_DRAFTS, DBG_OWN_N, DBG_OWN_Y, DBG_STATE, DBG_HIST, DBG_HIDDEN_V, DBG_PATH, \
-    DBG_TRACE, DBG_UBIAS = range(1, 13)
+    DBG_TRACE, DBG_UBIAS, DBG_NONFINITE = range(1, 14)
 
 EXPORTS = ["sd2_workspace_bytes", "sd2_create", "sd2_create_noalloc", "sd2_create_mlp", "sd2_train_loss",
            "sd2_train_loss_scratch_bytes", "sd2_prefill", "sd2_round", "sd2_round_forced", "sd2_destroy",
@@ -262,7 +262,7 @@ class Engine:
             DBG_STEER: ((B, dD), np.float32), DBG_OWN_DRAFTS: ((B, k), np.int32), DBG_OWN_N: ((B,), np.int32),
             DBG_OWN_Y: ((B,), np.int32), DBG_STATE: ((B, 5), np.int32),
             DBG_HIST: ((B, self.cfg.max_seq_len), np.int32), DBG_HIDDEN_V: ((B, k + 1, dV), np.float32),
-            DBG_PATH: ((2,), np.int32), DBG_TRACE: ((33, 1024), np.int64),
+            DBG_PATH: ((2,), np.int32), DBG_TRACE: ((33, 1024), np.int64), DBG_NONFINITE: ((1,), np.int32),
             DBG_UBIAS: (((B, self.cfg.drafter.n_layers, self.cfg.drafter.d_ff) if self.cfg.steering == STEER_MLP
                          else (B, self.cfg.drafter.n_layers, self.cfg.cond_rank)
                          if self.cfg.steering == STEER_MLP_COND else (B, self.cfg.drafter.d_model)), np.float32),

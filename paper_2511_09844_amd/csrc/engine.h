@@ -80,6 +80,7 @@ struct Workspace {
     size_t ws_part_n, ws_cnt_n;  // their capacities (floats, counters)
     float* attn_part;
     int32_t* attn_cnt;
+    int32_t* nonfinite;     // set to 1 by the sampler when a logit row it reads holds a NaN or an infinity
     size_t attn_cnt_n;      // its capacity (counters)
     // MLP steering (null unless cfg.steering == SD2_STEER_MLP)
     float* taps;            // [3][maxm][d_V] verifier residual after the tap blocks (per-operation path)

@@ -253,6 +253,7 @@ size_t carve(const sd2_config& c, char* base, Workspace* ws, ModelDev* mv, Model
             }
         }
         w.attn_cnt = cv.take<int32_t>(gmax);
+        w.nonfinite = cv.take<int32_t>(4);
         w.attn_cnt_n = gmax;
     }
     if (mlp_form(c)) {
@@ -862,6 +863,7 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
         case SD2_DBG_STATE: want = sizeof(int32_t) * (size_t)B * 5; break;
         case SD2_DBG_HIDDEN_V: src = e->ws.hidden_dbg; want = sizeof(float) * (size_t)B * (k + 1) * e->mv.dm.d_model; break;
         case SD2_DBG_PATH: want = sizeof(int32_t) * 2; break;
+        case SD2_DBG_NONFINITE: src = e->ws.nonfinite; want = sizeof(int32_t); break;
         case SD2_DBG_TRACE:
             if (!e->mk.trace) return SD2_ERR_STATE;
             src = e->mk.trace;
@@ -907,6 +909,12 @@ sd2_status sd2_debug_read(sd2_handle_t h, int32_t what, void* dst_host, size_t b
     }
     err = hipMemcpy(dst_host, src, want, hipMemcpyDeviceToHost);
     if (err != hipSuccess) return hip_fail(e, err, "hipMemcpy");
+    if (what == SD2_DBG_NONFINITE) {
+        // the read clears the flag (outside any captured round, so a plain memset)
+        err = hipMemsetAsync(e->ws.nonfinite, 0, sizeof(int32_t), e->stream);
+        if (err == hipSuccess) err = hipStreamSynchronize(e->stream);
+        if (err != hipSuccess) return hip_fail(e, err, "hipMemsetAsync");
+    }
     return SD2_OK;
 }
 

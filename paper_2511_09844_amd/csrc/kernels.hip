@@ -657,6 +657,7 @@ struct SampArgs {
     VPart* part;
     float *lse_v, *lse_d;
     int32_t* argmax_v;
+    int32_t* nonfinite;  // set to 1 when a logit read here is a NaN or an infinity
     int j;
     int32_t *out_tokens, *out_counts, *len_v, *len_d, *produced, *hist, *tt, *done_w;
     int cap, max_new;
@@ -744,6 +745,8 @@ __global__ __launch_bounds__(256) void k_row_partial(SampArgs a) {
                                 : a.logits_d + ((size_t)b * a.k + (i - a.k - 1)) * a.V;
     int v0 = c * a.chunk, v1 = min(a.V, v0 + a.chunk);
     VPart& p = a.part[(size_t)rowid * kVocabChunks + c];
+    // every logit of the round's 2k+1 rows passes here: any NaN or infinity raises the flag
+    bool nonfinite = false;
     if (a.T > 0.0f) {
         float m = -INFINITY, sm = 0.0f;
         // 8 logits per thread are read (index clamped) before they are merged, in the same order
@@ -752,8 +755,10 @@ __global__ __launch_bounds__(256) void k_row_partial(SampArgs a) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) x[i] = row[min(vb + i * (int)blockDim.x, v1 - 1)];
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 8; ++i) {
+                nonfinite |= !isfinite(x[i]);
                 if (vb + i * (int)blockDim.x < v1) lse_merge(m, sm, x[i] / a.T, 1.0f);
+            }
         }
         wave_lse(m, sm);
         int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
@@ -765,21 +770,24 @@ __global__ __launch_bounds__(256) void k_row_partial(SampArgs a) {
             p.s = sm;
         }
     } else {
+        // greedy: argmax partials of the verifier rows; the drafter rows are only checked
         ArgBest best{-INFINITY, 0x7fffffff};
-        if (i <= a.k)
-            for (int vb = v0 + threadIdx.x; vb < v1; vb += 8 * blockDim.x) {
-                float x[8];
+        for (int vb = v0 + threadIdx.x; vb < v1; vb += 8 * blockDim.x) {
+            float x[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) x[e] = row[min(vb + e * (int)blockDim.x, v1 - 1)];
+            for (int e = 0; e < 8; ++e) x[e] = row[min(vb + e * (int)blockDim.x, v1 - 1)];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int v = vb + e * (int)blockDim.x;
-                    if (v < v1 && better(x[e], v, best.s, best.i)) best = ArgBest{x[e], v};
-                }
+            for (int e = 0; e < 8; ++e) {
+                nonfinite |= !isfinite(x[e]);
+                const int v = vb + e * (int)blockDim.x;
+                if (i <= a.k && v < v1 && better(x[e], v, best.s, best.i)) best = ArgBest{x[e], v};
             }
+        }
         block_argbest(best, sha);
         if (threadIdx.x == 0) { p.best = best.s; p.idx = best.i; }
     }
+    // one store of 1 (idempotent: no read-modify-write needed) per workgroup that saw one
+    if (__syncthreads_or(nonfinite) && threadIdx.x == 0) store_through_i(a.nonfinite, 1);
 }
 
 // Accept/reject: one wave per sequence.  Every row's partials and every draft's two logits are
@@ -961,6 +969,7 @@ static SampArgs samp_args(Engine& e) {
     a.own_y = e.ws.own_y; a.steer_map = e.ws.steer_map;
     a.forced = e.ws.forced; a.forced_on = e.ws.forced_on;
     a.part = e.ws.part; a.lse_v = e.ws.lse_v; a.lse_d = e.ws.lse_d; a.argmax_v = e.ws.argmax_v;
+    a.nonfinite = e.ws.nonfinite;
     a.j = 0;
     a.out_tokens = nullptr; a.out_counts = nullptr;
     a.len_v = e.ws.len_v; a.len_d = e.ws.len_d; a.produced = e.ws.produced; a.hist = e.ws.hist; a.tt = e.ws.t;
