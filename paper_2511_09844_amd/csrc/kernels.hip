@@ -665,6 +665,10 @@ struct SampArgs {
 
 __device__ __forceinline__ int clamp_tok(int v, int V) { return v < 0 ? 0 : (v >= V ? V - 1 : v); }
 
+__device__ __forceinline__ void store_through_i(int32_t* p, int32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ void block_argbest(ArgBest& a, ArgBest* sh) {
     int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     a = wave_argbest(a);
