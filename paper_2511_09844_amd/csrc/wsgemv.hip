@@ -355,15 +355,17 @@ constexpr size_t kPgLds = 2 * 2 * kPgPlane * 2;  // two buffers of hi and lo pla
 static_assert(kPgLds >= 4 * kPgTW * 4 * 256 * 4, "result staging must fit the activation planes");
 
 // K ranges for a many-row projection: split while the grid stays within 2 workgroups per CU and
-// every range keeps at least 1024 columns (a multiple of 256).  Shared by the launch and the
-// workspace sizing.
+// every range keeps at least 1024 columns (a multiple of 256); 512 with a single 64-row block,
+// whose grid is the smallest (the 32-row first drafter step of a 16-sequence batch).  Shared by
+// the launch and the workspace sizing.
 int pg_split(int M, int N, int K, int subs) {
     const int nt = 4 * kPgTW / subs;
     const int nblk_m = (M + kPgRows - 1) / kPgRows;
     const int nblk_n = (N / 16 + nt - 1) / nt;
     const int blocks = 8 * nblk_m * ((nblk_n + 7) / 8);
     int S = 1;
-    while (blocks * S * 2 <= 512 && (K / (S * 2)) % 256 == 0 && K / (S * 2) >= 1024 && K % (S * 2) == 0) S *= 2;
+    const int min_range = nblk_m == 1 ? 512 : 1024;
+    while (blocks * S * 2 <= 512 && (K / (S * 2)) % 256 == 0 && K / (S * 2) >= min_range && K % (S * 2) == 0) S *= 2;
     return S;
 }
 
