@@ -90,6 +90,14 @@ RAG16 = Workload(
     drafter=Dims(1, 512, 8, 2, 1024, 4096, 5e5),
     dtype="bf16", k=7, batch=16, prompt=(256, 2048), new_tokens=16, temperature=0.7, seed=42)
 RAG16_SHORTEST, RAG16_LONGEST = 1, 8
+# The 70B shape's verify attention at long contexts: 8 query heads per KV head (k_pattn's two
+# passes of 4 heads), 9 rows per sequence (k = 8), head dim 128, prompts of 731 and 1026 tokens:
+# flash attention over several key spans merged by the last span to arrive.  18
+# verify rows, so the per-operation path runs it.
+G8LONG = Workload(
+    name="g8-hd128-long", verifier=Dims(1, 2048, 16, 2, 4096, 4096, 5e5),
+    drafter=Dims(1, 1024, 8, 2, 2048, 4096, 5e5),
+    dtype="bf16", k=8, batch=2, prompt=(600, 1100), new_tokens=18, temperature=1.0, seed=37)
 
 
 def scaled_set(wl, scale):

@@ -2,7 +2,7 @@
 CPU oracle on small shapes that path takes, and the one-kernel-per-operation path on the same."""
 import pytest
 
-from oracle_fixtures import MK1, MK2, MK3, MK4, MK5, MK6, RAG16, RAG16_LONGEST, RAG16_SHORTEST
+from oracle_fixtures import G8LONG, MK1, MK2, MK3, MK4, MK5, MK6, RAG16, RAG16_LONGEST, RAG16_SHORTEST
 
 pytestmark = pytest.mark.gpu
 
@@ -69,3 +69,8 @@ def test_unsteered_drafter_persistent():
 
 def test_unsteered_drafter_separate_kernels():
     _run(MK2, expect_path=0, separate_kernels=True, unsteered=True)
+
+
+def test_gqa8_nine_rows_long_contexts_per_operation():
+    # the 70B shape's verify attention (8 query heads per KV head, 9 rows) over several key spans
+    _run(G8LONG, expect_path=0)
