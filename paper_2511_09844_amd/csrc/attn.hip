@@ -247,11 +247,16 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
 // 16 consecutive query rows of one sequence, one KV head and one span of key tiles; each of its
 // 4 waves takes the query heads wave, wave + 4, ... of that KV head.  Per 16-position key tile,
 // K and V are staged in LDS once for all the group's heads (the next tile is requested into
-// registers while the current one is used); a wave forms the 16 x 16 score tile S = Q K^T with
-// v_mfma_f32_16x16x4_f32 over the head dimension, keeps an online softmax per query row (rows
-// are held by groups of 16 lanes in the MFMA result layout), moves P through LDS into the
-// operand layout, and accumulates O += P V with the same instruction, HD/16 output tiles of
-// 16 x 16.  fp32 operands keep the cache's precision.  With few (sequence, KV head, row block)
+// registers while the current one is used).  A wave computes the transposed products, with
+// v_mfma_f32_16x16x4_f32 (fp32 operands keep the cache's precision):
+//   S^T = K Q^T   (16 keys x 16 queries; the head dimension walked as dim = g * HD/4 + s for
+//                  lane group g and step s, so a lane's K operands are HD/4 adjacent floats)
+//   O^T += V^T P^T (HD/16 tiles; output dim = i * HD/16 + t for tile row i and tile t, so a
+//                  lane's V operands are HD/16 adjacent floats per key)
+// In the result layout of S^T a lane holds four keys of one query (its column), which is also
+// the layout P^T needs as an operand and the layout of that query's O^T rows: the online softmax
+// runs in registers, with its max and sum taken over the four lane groups of a column by two
+// lane-swap steps, and P never goes through LDS.  With few (sequence, KV head, row block)
 // groups the keys are split into at most 16 spans of span_t tiles (about eight workgroups per
 // compute unit): every span writes an un-normalised partial into k_attn's partial buffer and
 // the last span of a group to arrive merges them in span order, all spans' loads at once.
@@ -261,14 +266,32 @@ constexpr int kPaK = 16;                  // key positions per tile
 constexpr int kPaMaxSpans = 16;           // spans per group (one merge batch)
 constexpr int kPaMinRows = 8;             // rows per sequence from which blocks take k_pattn
 typedef float pf4 __attribute__((ext_vector_type(4)));
+typedef float pf2 __attribute__((ext_vector_type(2)));
+
+// Max and sum over the four 16-lane groups of a wave (lanes l, l^16, l^32, l^48 hold one column).
+__device__ __forceinline__ float pa_colmax(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float pa_colsum(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 template <int HD>
 __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t) {
     constexpr int KL = HD + 4;                            // padded LDS row of K and V
     constexpr int F4 = (kPaK * HD / 4 + 255) / 256;       // float4 of a K (or V) tile per thread
-    __shared__ float ks[kPaK * KL];
-    __shared__ float vs[kPaK * KL];
-    __shared__ float ps[4][kPaQ][kPaK + 1];  // per wave: P in row-major, read back as the A operand
+    constexpr int QD = HD / 4;                            // head dims per lane group in S^T
+    constexpr int VD = HD / 16;                           // output dims per lane and key in O^T
+    static_assert(QD % 4 == 0 && (VD % 4 == 0 || VD == 2), "head dim");
+    __shared__ __attribute__((aligned(16))) float ks[kPaK * KL];
+    __shared__ __attribute__((aligned(16))) float vs[kPaK * KL];
+    __shared__ __attribute__((aligned(16))) float ot[4 * kPaQ * KL];  // per wave: O rows of one head
     __shared__ int qpos[kPaQ];
     __shared__ int maxpos_s;
     __shared__ int last_flag;
@@ -298,6 +321,7 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t
     const float* kg = a.kc + kvoff;
     const float* vg = a.vc + kvoff;
     const int col = lane & 15, grp = lane >> 4;  // MFMA layouts: column / row-group of this lane
+    const int myq = qpos[col];                    // position of this lane's query row (-1: none)
     auto fetch = [&](int kt, float4 (&pk)[F4], float4 (&pv)[F4]) {
 #pragma unroll
         for (int i = 0; i < F4; ++i) {
@@ -315,26 +339,25 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t
         const int hh = hp * 4 + wave;
         const bool active = hh < G && t0 < t1;
         const int h = kvh * G + (hh < G ? hh : 0);
-        // Q as the A operand: lane holds Q[row col][4 s + grp], pre-scaled
-        float qf[HD / 4];
+        // Q as the B operand of S^T: lane holds Q[row col][grp * QD + s], pre-scaled (rows past
+        // the block re-read row 0 and are zeroed by the scale: no load depends on a branch,
+        // which would cost one memory round trip per load)
+        float qf[QD];
         {
             const int qrow = i0 + col;
             const bool ok = qrow < a.rps;
-            const float* qp = a.q + (size_t)(b * a.rps + (ok ? qrow : 0)) * a.q_stride + h * HD;
+            const float* qp = a.q + (size_t)(b * a.rps + (ok ? qrow : 0)) * a.q_stride + h * HD + grp * QD;
+            const float qs = ok ? a.scale : 0.f;
 #pragma unroll
-            for (int s = 0; s < HD / 4; ++s) qf[s] = ok ? qp[4 * s + grp] * a.scale : 0.f;
+            for (int s = 0; s < QD; s += 4) {
+                const pf4 x = *(const pf4*)(qp + s) * qs;
+                qf[s] = x[0]; qf[s + 1] = x[1]; qf[s + 2] = x[2]; qf[s + 3] = x[3];
+            }
         }
-        pf4 o[HD / 16];
+        pf4 o[VD];  // o[t][r] = O[query col][(4 grp + r) * VD + t]
 #pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt) o[dt] = pf4{0.f, 0.f, 0.f, 0.f};
-        float mrow[4], lrow[4];
-        int qp4[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            mrow[r] = -INFINITY;
-            lrow[r] = 0.f;
-            qp4[r] = qpos[4 * grp + r];
-        }
+        for (int t = 0; t < VD; ++t) o[t] = pf4{0.f, 0.f, 0.f, 0.f};
+        float m_run = -INFINITY, l_run = 0.f;
         float4 pk[F4], pv[F4];
         if (t0 < t1) fetch(t0, pk, pv);
         for (int kt = t0; kt < t1; ++kt) {
@@ -352,71 +375,106 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t
             __syncthreads();
             if (kt + 1 < t1) fetch(kt + 1, pk, pv);
             if (!active) continue;
-            // S = Q K^T: B operand K^T[4 s + grp][key col]; four independent accumulation chains
+            // operands from LDS, all requested before the first product: K[key col][grp*QD + s]
+            // and V[key 4 grp + r][col * VD + t]
+            float kf[QD], vf[4][VD];
+#pragma unroll
+            for (int s = 0; s < QD; s += 4) {
+                const pf4 x = *(const pf4*)(ks + col * KL + grp * QD + s);
+                kf[s] = x[0]; kf[s + 1] = x[1]; kf[s + 2] = x[2]; kf[s + 3] = x[3];
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float* vr = vs + (4 * grp + r) * KL + col * VD;
+                if constexpr (VD == 2) {
+                    const pf2 x = *(const pf2*)vr;
+                    vf[r][0] = x[0]; vf[r][1] = x[1];
+                } else {
+#pragma unroll
+                    for (int t = 0; t < VD; t += 4) {
+                        const pf4 x = *(const pf4*)(vr + t);
+                        vf[r][t] = x[0]; vf[r][t + 1] = x[1]; vf[r][t + 2] = x[2]; vf[r][t + 3] = x[3];
+                    }
+                }
+            }
+            // S^T = K Q^T in four independent accumulation chains; this lane then holds
+            // S[query col][key 4 grp + r]
             pf4 sc4[4];
 #pragma unroll
             for (int c4 = 0; c4 < 4; ++c4) sc4[c4] = pf4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int s = 0; s < HD / 4; ++s)
-                sc4[s & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(qf[s], ks[col * KL + 4 * s + grp], sc4[s & 3], 0, 0, 0);
+            for (int s = 0; s < QD; ++s)
+                sc4[s & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[s], qf[s], sc4[s & 3], 0, 0, 0);
             const pf4 sc = (sc4[0] + sc4[1]) + (sc4[2] + sc4[3]);
-            // online softmax: this lane holds S[4 grp + r][col]; a row's 16 columns are the 16
-            // lanes of its group
-            const int kpos = kt * kPaK + col;
-            float pr[4];
+            // online softmax of query col over this tile's 16 keys
+            const int kb = kt * kPaK + 4 * grp;
+            float sv[4], mx = -INFINITY;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const bool valid = qp4[r] >= 0 && kpos <= qp4[r];
-                const float sv = valid ? sc[r] : -INFINITY;
-                float mx = sv;
-#pragma unroll
-                for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
-                const float mnew = fmaxf(mrow[r], mx);
-                const float p = valid ? expf(sv - mnew) : 0.f;
-                float sum = p;
-#pragma unroll
-                for (int off = 8; off > 0; off >>= 1) sum += __shfl_xor(sum, off, 16);
-                const float scl = mrow[r] == -INFINITY ? 0.f : expf(mrow[r] - mnew);
-                lrow[r] = lrow[r] * scl + sum;
-                mrow[r] = mnew;
-#pragma unroll
-                for (int dt = 0; dt < HD / 16; ++dt) o[dt][r] *= scl;
-                pr[r] = p;
+                sv[r] = (myq >= 0 && kb + r <= myq) ? sc[r] : -INFINITY;
+                mx = fmaxf(mx, sv[r]);
             }
+            mx = pa_colmax(mx);
+            const float mnew = fmaxf(m_run, mx);
+            float pr[4], sum = 0.f;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) ps[wave][4 * grp + r][col] = pr[r];
-            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's P writes reached LDS
-            __builtin_amdgcn_wave_barrier();
-            // O += P V: A operand P[row col][4 ks + grp], B operand V[4 ks + grp][16 dt + col]
-#pragma unroll
-            for (int k4 = 0; k4 < kPaK / 4; ++k4) {
-                const float pa = ps[wave][col][4 * k4 + grp];
-                const float* vr = vs + (4 * k4 + grp) * KL + col;
-#pragma unroll
-                for (int dt = 0; dt < HD / 16; ++dt)
-                    o[dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(pa, vr[16 * dt], o[dt], 0, 0, 0);
+            for (int r = 0; r < 4; ++r) {
+                pr[r] = sv[r] == -INFINITY ? 0.f : expf(sv[r] - mnew);
+                sum += pr[r];
             }
-            __builtin_amdgcn_wave_barrier();
+            sum = pa_colsum(sum);
+            const float scl = m_run == -INFINITY ? 0.f : expf(m_run - mnew);
+            l_run = l_run * scl + sum;
+            m_run = mnew;
+#pragma unroll
+            for (int t = 0; t < VD; ++t) o[t] *= scl;
+            // O^T += V^T P^T: step r pairs key 4 grp + r with this lane's k slot
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int t = 0; t < VD; ++t)
+                    o[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf[r][t], pr[r], o[t], 0, 0, 0);
         }
+        // O through LDS into row-major order, then whole rows stored by the wave (a lane's own
+        // values belong to one row: stored directly, each store would touch 16 rows)
         if (hh < G) {
+            float* ow = ot + wave * (kPaQ * KL);
+            const float inv = nspan == 1 ? ((myq >= 0 && l_run > 0.f) ? 1.f / l_run : 0.f) : 1.f;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int i = 4 * grp + r, row = i0 + i;
-                if (row >= a.rps) continue;
-                const size_t orow = (size_t)(b * a.rps + row);
-                if (nspan == 1) {
-                    const float inv = (qp4[r] >= 0 && lrow[r] > 0.f) ? 1.f / lrow[r] : 0.f;
-                    float* op = a.out + orow * a.H * HD + h * HD + col;
-#pragma unroll
-                    for (int dt = 0; dt < HD / 16; ++dt) op[16 * dt] = o[dt][r] * inv;
+                float* dst = ow + col * KL + (4 * grp + r) * VD;
+                if constexpr (VD == 2) {
+                    *(pf2*)dst = pf2{o[0][r] * inv, o[1][r] * inv};
                 } else {
-                    // un-normalised partial of this span: output, max, sum
-                    float* pp = a.part + ((orow * a.H + h) * a.nsplit + sp) * (HD + 2);
 #pragma unroll
-                    for (int dt = 0; dt < HD / 16; ++dt) store_through(pp + 16 * dt + col, o[dt][r]);
-                    if (col == 0) {
-                        store_through(pp + HD, mrow[r]);
-                        store_through(pp + HD + 1, lrow[r]);
+                    for (int t = 0; t < VD; t += 4)
+                        *(pf4*)(dst + t) = pf4{o[t][r] * inv, o[t + 1][r] * inv, o[t + 2][r] * inv, o[t + 3][r] * inv};
+                }
+            }
+            if (nspan > 1 && grp == 0 && i0 + col < a.rps) {
+                // this span's max and sum of the lane's row
+                float* pp = a.part + (((size_t)(b * a.rps + i0 + col) * a.H + h) * a.nsplit + sp) * (HD + 2);
+                store_through(pp + HD, m_run);
+                store_through(pp + HD + 1, l_run);
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's rows are in LDS
+            __builtin_amdgcn_wave_barrier();
+            constexpr int RW = (HD + 63) / 64;  // values of one row per lane
+            float rv[kPaQ][RW];                   // every row read before any is stored
+#pragma unroll
+            for (int i = 0; i < kPaQ; ++i)
+#pragma unroll
+                for (int j = 0; j < RW; ++j) rv[i][j] = ow[i * KL + min(lane + 64 * j, HD - 1)];
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int i = 0; i < kPaQ; ++i) {
+                const size_t orow = (size_t)(b * a.rps + i0 + i);
+#pragma unroll
+                for (int j = 0; j < RW; ++j) {
+                    const int d = lane + 64 * j;
+                    if (i0 + i < a.rps && d < HD) {
+                        if (nspan == 1) a.out[orow * a.H * HD + h * HD + d] = rv[i][j];
+                        else store_through(a.part + ((orow * a.H + h) * a.nsplit + sp) * (HD + 2) + d, rv[i][j]);
                     }
                 }
             }
@@ -467,6 +525,11 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t
 }
 
 static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) {
+    // the kernel reads query rows and writes output rows as 16-byte vectors
+    if (a.q_stride % 4 || ((uintptr_t)a.q & 15) || ((uintptr_t)a.out & 15)) {
+        e.bad_launch = true;
+        return;
+    }
     const int nqb = (a.rps + kPaQ - 1) / kPaQ;
     const int groups = nseq * a.Hkv * nqb;
     // few groups: split the keys into spans for about 2048 workgroups, eight per compute unit,

@@ -147,6 +147,22 @@ __device__ __forceinline__ void tile_epilogue(const WsArgs& a, int tile, const f
     }
 }
 
+// Sum of one row's slice sums of squares over a wave (lane l takes slices l, l + 64, ...): loads in
+// batches of eight per lane with clamped indexes, so that none waits for the one before it.
+// row < 0: 0.
+__device__ __forceinline__ float row_sumsq(const float* ss, int nss, int row, int lane) {
+    const float* rp = ss + (size_t)max(row, 0) * nss;
+    float sm = 0.0f;
+    for (int t0 = 0; t0 < nss; t0 += 512) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = rp[min(t0 + lane + 64 * u, nss - 1)];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sm += (row >= 0 && t0 + lane + 64 * u < nss) ? v[u] : 0.f;
+    }
+    return sm;
+}
+
 template <int NW, int STEPS, int SUBS>
 __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -205,16 +221,24 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
             xv[i] = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
+    // the gain words of the same columns, all requested before any is used (a load under a
+    // per-element test would wait for everything in flight, the weights included)
+    uint2 gv[XB];
+    if (a.gamma) {
+#pragma unroll
+        for (int i = 0; i < XB; ++i) {
+            const int idx = min(tid + i * NW * 64, nx - 1);
+            gv[i] = *(const uint2*)(a.gamma + k0 + (idx % n4) * 4);
+        }
+    }
     if (nsub_mine > 0) issue(wa, 0);
     float ssum = 0.0f;
     const int ss_row = wave < M ? src_row[wave] : -1;
-    if (a.gamma && ss_row >= 0)
-        for (int t = lane; t < a.nss; t += 64) ssum += a.ss[(size_t)ss_row * a.nss + t];
-    auto stage = [&](const float4& v, int idx) {
+    if (a.gamma) ssum = row_sumsq(a.ss, a.nss, ss_row, lane);
+    auto stage = [&](const float4& v, int idx, uint2 gw) {
         const int m = idx / n4, kk = (idx % n4) * 4;
         float gm[4] = {1.f, 1.f, 1.f, 1.f};
         if (a.gamma) {
-            uint2 gw = *(const uint2*)(a.gamma + k0 + kk);
             gm[0] = bf16_lo(gw.x); gm[1] = bf16_hi(gw.x); gm[2] = bf16_lo(gw.y); gm[3] = bf16_hi(gw.y);
         }
         float vv[4] = {v.x * gm[0], v.y * gm[1], v.z * gm[2], v.w * gm[3]};
@@ -230,14 +254,15 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
 #pragma unroll
     for (int i = 0; i < XB; ++i) {
         const int idx = tid + i * NW * 64;
-        if (idx < nx) stage(xv[i], idx);
+        if (idx < nx) stage(xv[i], idx, gv[i]);
     }
     // slices larger than XB float4 per thread (not used by the planned shapes) stage the rest here
     for (int idx = tid + XB * NW * 64; idx < nx; idx += NW * 64) {
         const int m = idx / n4, kk = (idx % n4) * 4;
         const int src = src_row[m];
         float4 v = src >= 0 ? *(const float4*)(a.X + (size_t)src * a.ldx + k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
-        stage(v, idx);
+        const uint2 gw = a.gamma ? *(const uint2*)(a.gamma + k0 + kk) : make_uint2(0x3f803f80u, 0x3f803f80u);
+        stage(v, idx, gw);
     }
     if (nsub_mine > 1) issue(wb, 1);
     if (a.gamma) {
@@ -245,10 +270,7 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
         if (lane == 0 && wave < M) inv_rms[wave] = rsqrtf(ssum / (float)a.K + a.eps);
         // rows beyond the number of waves (M > NW)
         for (int m = NW + wave; m < M; m += NW) {
-            const int src = src_row[m];
-            float sm = 0.0f;
-            if (src >= 0)
-                for (int t = lane; t < a.nss; t += 64) sm += a.ss[(size_t)src * a.nss + t];
+            float sm = row_sumsq(a.ss, a.nss, src_row[m], lane);
             sm = wave_sum(sm);
             if (lane == 0) inv_rms[m] = rsqrtf(sm / (float)a.K + a.eps);
         }
@@ -497,13 +519,17 @@ __global__ __launch_bounds__(256, 2) void k_pgemm(WsArgs a, int nblk_m, int nbs)
         const int m = tid >> 2, p = tid & 3;
         const int src = src_row[m];
         float sm = 0.0f;
-        if (src >= 0) {
-            const float4* sp = (const float4*)(a.ss + (size_t)src * a.nss);
-#pragma unroll 8
-            for (int f = p; f < a.nss / 4; f += 4) {
-                const float4 v = sp[f];
-                sm += (v.x + v.y) + (v.z + v.w);
-            }
+        // eight float4 per thread in flight at once, indexes clamped and the extra ones dropped
+        // (loads under a loop test would each wait for the previous one)
+        const float4* sp = (const float4*)(a.ss + (size_t)max(src, 0) * a.nss);
+        const int n4s = a.nss / 4;
+        for (int f0 = 0; f0 < n4s; f0 += 32) {
+            float4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = sp[min(f0 + p + 4 * u, n4s - 1)];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                sm += (src >= 0 && f0 + p + 4 * u < n4s) ? (v[u].x + v[u].y) + (v[u].z + v[u].w) : 0.f;
         }
         sm += __shfl_xor(sm, 1, 4);
         sm += __shfl_xor(sm, 2, 4);
