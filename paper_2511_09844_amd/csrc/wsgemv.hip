@@ -29,10 +29,18 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+typedef float wf2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 wbf2_t __attribute__((ext_vector_type(2)));
+
+// hi/lo bf16 split of two fp32 values, packed as two bf16 words each (element 0 in the low
+// half): hi = x rounded to nearest even, lo = (x - hi) rounded likewise; one hardware packed
+// conversion per word (integer rounding took about six VALU operations per value)
+__device__ __forceinline__ void split_hilo(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+    const wf2_t v = {x0, x1};
+    const wbf2_t h = __builtin_convertvector(v, wbf2_t);
+    const wbf2_t l = __builtin_convertvector(v - __builtin_convertvector(h, wf2_t), wbf2_t);
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = __builtin_bit_cast(uint32_t, l);
 }
 
 struct WsArgs {
@@ -241,15 +249,11 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
         if (a.gamma) {
             gm[0] = bf16_lo(gw.x); gm[1] = bf16_hi(gw.x); gm[2] = bf16_lo(gw.y); gm[3] = bf16_hi(gw.y);
         }
-        float vv[4] = {v.x * gm[0], v.y * gm[1], v.z * gm[2], v.w * gm[3]};
-        uint16_t hi[4], lo[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            hi[e] = f32_to_bf16_rne(vv[e]);
-            lo[e] = f32_to_bf16_rne(vv[e] - bf16_to_f32(hi[e]));
-        }
-        *(uint2*)(xh + (size_t)m * ldk + kk) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-        *(uint2*)(xl + (size_t)m * ldk + kk) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+        uint32_t h0, h1, l0, l1;
+        split_hilo(v.x * gm[0], v.y * gm[1], h0, l0);
+        split_hilo(v.z * gm[2], v.w * gm[3], h1, l1);
+        *(uint2*)(xh + (size_t)m * ldk + kk) = make_uint2(h0, h1);
+        *(uint2*)(xl + (size_t)m * ldk + kk) = make_uint2(l0, l1);
     };
 #pragma unroll
     for (int i = 0; i < XB; ++i) {
@@ -471,15 +475,11 @@ __global__ __launch_bounds__(256, 2) void k_pgemm(WsArgs a, int nblk_m, int nbs)
 #pragma unroll
         for (int e = 0; e < kPgX4; ++e) {
             const int m = (tid + e * 256) >> 5, kk = kk_t;
-            const float vv[4] = {xv[e].x * gm[0], xv[e].y * gm[1], xv[e].z * gm[2], xv[e].w * gm[3]};
-            uint16_t hi[4], lo[4];
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                hi[c] = f32_to_bf16_rne(vv[c]);
-                lo[c] = f32_to_bf16_rne(vv[c] - bf16_to_f32(hi[c]));
-            }
-            *(uint2*)(xh + m * kPgLdk + kk) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-            *(uint2*)(xl + m * kPgLdk + kk) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+            uint32_t h0, h1, l0, l1;
+            split_hilo(xv[e].x * gm[0], xv[e].y * gm[1], h0, l0);
+            split_hilo(xv[e].z * gm[2], xv[e].w * gm[3], h1, l1);
+            *(uint2*)(xh + m * kPgLdk + kk) = make_uint2(h0, h1);
+            *(uint2*)(xl + m * kPgLdk + kk) = make_uint2(l0, l1);
         }
     };
     auto mma = [&](int i, const WFrag& w) {
