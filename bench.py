@@ -164,6 +164,38 @@ def _source_hash():
     return h.hexdigest()
 
 
+def summarize_stages(path, k):
+    """Per-round kernel time of a rocprofv3 kernel trace of this script, split by stage of the
+    round: drafter step 1, drafter steps 2..k (each ends with its k_pick_final), the verify pass
+    (up to the accept test) and the sampling and commit kernels after it."""
+    stages = ["drafter step 1", f"drafter steps 2-{k}", "verify pass", "accept, commit"]
+    per = [dict() for _ in stages]
+    rounds, st = 0, None
+    for name, start, end in _trace_rows(path):
+        key = name.split("(")[0].replace("void ", "").replace("sd2::", "")
+        if "k_set_flag" in key:
+            rounds, st, picks = rounds + 1, 0, 0
+        if st is None:
+            continue
+        if key.startswith("k_row_partial") or key.startswith("k_accept"):
+            st = 3
+        c = per[st].setdefault(key, [0, 0])
+        c[0] += 1
+        c[1] += end - start
+        if key.startswith("k_pick_final"):
+            picks += 1
+            st = 1 if picks < k else 2
+        if key.startswith("k_commit"):
+            st = None
+    print(f"{rounds} rounds")
+    for title, tab in zip(stages, per):
+        tot = sum(v[1] for v in tab.values())
+        print(f"{title}: {tot / 1e6 / max(1, rounds):.3f} ms/round")
+        for key, (n, ns) in sorted(tab.items(), key=lambda x: -x[1][1])[:8]:
+            print(f"  {key[:40]:40s} {n / max(1, rounds):7.2f}/round  {ns / 1e6 / max(1, rounds):8.3f} ms/round"
+                  f"  avg {ns / n / 1e3:9.2f} us")
+
+
 def summarize_pmc(fetch_csv, write_csv, write_json):
     """HBM traffic per k_mk launch (persistent drafter-step and verify-pass launches) from
     FETCH_SIZE and WRITE_SIZE runs (KiB per dispatch), each scaled by what the same counter reads
@@ -347,6 +379,9 @@ def main():
                          "of a crash at exit)")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print the per-round breakdown of a rocprofv3 kernel trace of this script and exit")
+    ap.add_argument("--summarize-stages", metavar="KERNEL_TRACE_CSV",
+                    help="print the per-stage breakdown (drafter steps, verify pass) of the rounds of a "
+                         "rocprofv3 kernel trace of this script with --workload, and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print k_mk HBM traffic from two rocprofv3 --pmc runs of this script with "
                          "--calib-copy and exit")
@@ -357,6 +392,9 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, TRAFFIC_FILE if args.write_traffic else None)
+        return
+    if args.summarize_stages:
+        summarize_stages(args.summarize_stages, si.BY_NAME[args.workload].k)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the round runs on one device); --gpus {args.gpus} is not supported", file=sys.stderr)
