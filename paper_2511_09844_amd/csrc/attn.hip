@@ -282,6 +282,54 @@ __device__ __forceinline__ float pa_colsum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// The last span of a (sequence, KV head, row block) group to finish merges the live spans in
+// span order: a thread per (row, head, 4 dimensions), every span's (max, sum) and output
+// requested at once.  qpos holds the block's row positions (-1: no row).
+template <int HD>
+__device__ void pa_span_merge(const AttnArgs& a, int grp_id, int nspan, int span_t, int ntile_all, int b, int kvh,
+                              int i0, const int* qpos, int* last_flag) {
+    if (!arrive_last(a.cnt + grp_id, nspan, last_flag)) return;
+    const int tid = threadIdx.x, G = a.H / a.Hkv;
+    const int nlive = min(nspan, ntile_all > 0 ? (ntile_all - 1) / span_t + 1 : 0);
+    constexpr int D4 = HD / 4;
+    for (int idx = tid; idx < kPaQ * G * D4; idx += 256) {
+        const int i = idx / (G * D4), hh = (idx / D4) % G, d = (idx % D4) * 4;
+        const int row = i0 + i;
+        if (row >= a.rps) continue;
+        const size_t orow = (size_t)(b * a.rps + row);
+        const int h = kvh * G + hh;
+        float4 res = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (qpos[i] >= 0 && nlive > 0) {
+            const float* pp = a.part + (orow * a.H + h) * a.nsplit * (HD + 2);
+            float m2[kPaMaxSpans], l2[kPaMaxSpans];
+            float4 o2[kPaMaxSpans];
+#pragma unroll
+            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) {
+                const float* e2 = pp + (size_t)min(s2, nlive - 1) * (HD + 2);
+                m2[s2] = e2[HD];
+                l2[s2] = e2[HD + 1];
+                o2[s2] = make_float4(e2[d], e2[d + 1], e2[d + 2], e2[d + 3]);
+            }
+            float M = -INFINITY;
+#pragma unroll
+            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) M = s2 < nlive ? fmaxf(M, m2[s2]) : M;
+            float L = 0.f;
+#pragma unroll
+            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) {
+                const float w = (s2 < nlive && m2[s2] != -INFINITY) ? expf(m2[s2] - M) : 0.f;
+                L += w * l2[s2];
+                res.x += w * o2[s2].x;
+                res.y += w * o2[s2].y;
+                res.z += w * o2[s2].z;
+                res.w += w * o2[s2].w;
+            }
+            const float inv = L > 0.f ? 1.f / L : 0.f;
+            res = make_float4(res.x * inv, res.y * inv, res.z * inv, res.w * inv);
+        }
+        *(float4*)(a.out + orow * a.H * HD + h * HD + d) = res;
+    }
+}
+
 template <int HD>
 __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t) {
     constexpr int KL = HD + 4;                            // padded LDS row of K and V
@@ -481,47 +529,227 @@ __global__ __launch_bounds__(256) void k_pattn(AttnArgs a, int nspan, int span_t
         }
     }
     if (nspan == 1) return;
-    // the last span of this group to finish merges the live spans in span order: a thread per
-    // (row, head, 4 dimensions), every span's (max, sum) and output requested at once
-    if (!arrive_last(a.cnt + grp_id, nspan, &last_flag)) return;
-    const int nlive = min(nspan, ntile_all > 0 ? (ntile_all - 1) / span_t + 1 : 0);
-    constexpr int D4 = HD / 4;
-    for (int idx = tid; idx < kPaQ * G * D4; idx += 256) {
-        const int i = idx / (G * D4), hh = (idx / D4) % G, d = (idx % D4) * 4;
-        const int row = i0 + i;
-        if (row >= a.rps) continue;
-        const size_t orow = (size_t)(b * a.rps + row);
-        const int h = kvh * G + hh;
-        float4 res = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (qpos[i] >= 0 && nlive > 0) {
-            const float* pp = a.part + (orow * a.H + h) * a.nsplit * (HD + 2);
-            float m2[kPaMaxSpans], l2[kPaMaxSpans];
-            float4 o2[kPaMaxSpans];
-#pragma unroll
-            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) {
-                const float* e2 = pp + (size_t)min(s2, nlive - 1) * (HD + 2);
-                m2[s2] = e2[HD];
-                l2[s2] = e2[HD + 1];
-                o2[s2] = make_float4(e2[d], e2[d + 1], e2[d + 2], e2[d + 3]);
-            }
-            float M = -INFINITY;
-#pragma unroll
-            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) M = s2 < nlive ? fmaxf(M, m2[s2]) : M;
-            float L = 0.f;
-#pragma unroll
-            for (int s2 = 0; s2 < kPaMaxSpans; ++s2) {
-                const float w = (s2 < nlive && m2[s2] != -INFINITY) ? expf(m2[s2] - M) : 0.f;
-                L += w * l2[s2];
-                res.x += w * o2[s2].x;
-                res.y += w * o2[s2].y;
-                res.z += w * o2[s2].z;
-                res.w += w * o2[s2].w;
-            }
-            const float inv = L > 0.f ? 1.f / L : 0.f;
-            res = make_float4(res.x * inv, res.y * inv, res.z * inv, res.w * inv);
-        }
-        *(float4*)(a.out + orow * a.H * HD + h * HD + d) = res;
+    pa_span_merge<HD>(a, grp_id, nspan, span_t, ntile_all, b, kvh, i0, qpos, &last_flag);
+}
+
+// Verify blocks of exactly 8 rows per sequence (k = 7), 4n query heads per KV head: two heads
+// of 8 rows fill the 16 query columns of one S^T tile, so a key tile costs half the matrix work
+// of the one-head layout (whose columns 8-15 would be empty).  Waves 0 and 1 take head pairs
+// (0, 1) and (2, 3) of each pass of four heads over the even key tiles of the span, waves 2 and
+// 3 the same pairs over the odd tiles; two tiles are staged per barrier pair.  The odd-tile wave
+// of a pair hands its running max, sum and output to the even-tile wave through LDS (same lane
+// layout), which merges them and stores the rows.  Arithmetic per product as in k_pattn.
+template <int HD>
+__global__ __launch_bounds__(256) void k_pattn_pk(AttnArgs a, int nspan, int span_t) {
+    constexpr int KL = HD + 4;
+    constexpr int F4 = (kPaK * HD / 4 + 255) / 256;
+    constexpr int QD = HD / 4;
+    constexpr int VD = HD / 16;
+    static_assert(QD % 4 == 0 && (VD % 4 == 0 || VD == 2), "head dim");
+    __shared__ __attribute__((aligned(16))) float ks[2][kPaK * KL];
+    __shared__ __attribute__((aligned(16))) float vs[2][kPaK * KL];
+    __shared__ __attribute__((aligned(16))) float ot[2 * kPaQ * KL];  // per head pair: hand-off, then O rows
+    __shared__ float mlh[2][2][64];                                    // per head pair: max, sum per lane
+    __shared__ int qpos[kPaQ];
+    __shared__ int maxpos_s;
+    __shared__ int last_flag;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int G = a.H / a.Hkv;
+    const int grp_id = blockIdx.x / nspan, sp = blockIdx.x % nspan;
+    const int kvh = grp_id % a.Hkv;
+    const int b = grp_id / a.Hkv;
+    if (tid == 0) maxpos_s = -1;
+    __syncthreads();
+    if (tid < kPaQ) {
+        int p = -1;
+        if (tid < 8) p = a.row_pos[b * 8 + tid];
+        qpos[tid] = p;
+        if (p >= 0) atomicMax(&maxpos_s, p);
     }
+    __syncthreads();
+    const int maxpos = maxpos_s;
+    const int ntile_all = maxpos >= 0 ? maxpos / kPaK + 1 : 0;
+    const int t0 = nspan == 1 ? 0 : sp * span_t;
+    const int t1 = nspan == 1 ? ntile_all : min(ntile_all, t0 + span_t);
+    const size_t kvoff = (((size_t)a.layer * a.max_batch + b) * a.Hkv + kvh) * (size_t)a.cap * HD;
+    const float* kg = a.kc + kvoff;
+    const float* vg = a.vc + kvoff;
+    const int col = lane & 15, grp = lane >> 4;
+    const int pr = wave & 1, half = wave >> 1;  // head pair of the pass, key-tile parity
+    const int myq = qpos[col & 7];              // column col: row col % 8 of head 2 pr + col / 8
+    // tiles kt and kt + 1 (the second past t1: zeros)
+    auto fetch = [&](int kt, float4 (&pk)[2][F4], float4 (&pv)[2][F4]) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < F4; ++i) {
+                const int e4 = tid + 256 * i;
+                const int j = (e4 * 4) / HD, d = (e4 * 4) % HD, pos = (kt + u) * kPaK + j;
+                pk[u][i] = make_float4(0.f, 0.f, 0.f, 0.f);
+                pv[u][i] = pk[u][i];
+                if (e4 < kPaK * HD / 4 && kt + u < t1 && pos <= maxpos) {
+                    pk[u][i] = *(const float4*)(kg + (size_t)pos * HD + d);
+                    pv[u][i] = *(const float4*)(vg + (size_t)pos * HD + d);
+                }
+            }
+    };
+    for (int hp = 0; hp * 4 < G; ++hp) {
+        const int hh = hp * 4 + 2 * pr + (col >> 3);  // this lane column's head within the group
+        const int h = kvh * G + hh;
+        float qf[QD];
+        {
+            const float* qp = a.q + (size_t)(b * 8 + (col & 7)) * a.q_stride + h * HD + grp * QD;
+#pragma unroll
+            for (int s = 0; s < QD; s += 4) {
+                const pf4 x = *(const pf4*)(qp + s) * a.scale;
+                qf[s] = x[0]; qf[s + 1] = x[1]; qf[s + 2] = x[2]; qf[s + 3] = x[3];
+            }
+        }
+        pf4 o[VD];  // o[t][r] = O[column col][(4 grp + r) * VD + t]
+#pragma unroll
+        for (int t = 0; t < VD; ++t) o[t] = pf4{0.f, 0.f, 0.f, 0.f};
+        float m_run = -INFINITY, l_run = 0.f;
+        float4 pk[2][F4], pv[2][F4];
+        if (t0 < t1) fetch(t0, pk, pv);
+        for (int kt = t0; kt < t1; kt += 2) {
+            __syncthreads();
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int i = 0; i < F4; ++i) {
+                    const int e4 = tid + 256 * i;
+                    if (e4 < kPaK * HD / 4) {
+                        const int j = (e4 * 4) / HD, d = (e4 * 4) % HD;
+                        *(float4*)(ks[u] + j * KL + d) = pk[u][i];
+                        *(float4*)(vs[u] + j * KL + d) = pv[u][i];
+                    }
+                }
+            __syncthreads();
+            if (kt + 2 < t1) fetch(kt + 2, pk, pv);
+            const int mt = kt + half;
+            if (mt >= t1) continue;  // uniform per wave; the next barrier is at the loop top
+            const float* kss = ks[half];
+            const float* vss = vs[half];
+            float kf[QD], vf[4][VD];
+#pragma unroll
+            for (int s = 0; s < QD; s += 4) {
+                const pf4 x = *(const pf4*)(kss + col * KL + grp * QD + s);
+                kf[s] = x[0]; kf[s + 1] = x[1]; kf[s + 2] = x[2]; kf[s + 3] = x[3];
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float* vr = vss + (4 * grp + r) * KL + col * VD;
+                if constexpr (VD == 2) {
+                    const pf2 x = *(const pf2*)vr;
+                    vf[r][0] = x[0]; vf[r][1] = x[1];
+                } else {
+#pragma unroll
+                    for (int t = 0; t < VD; t += 4) {
+                        const pf4 x = *(const pf4*)(vr + t);
+                        vf[r][t] = x[0]; vf[r][t + 1] = x[1]; vf[r][t + 2] = x[2]; vf[r][t + 3] = x[3];
+                    }
+                }
+            }
+            pf4 sc4[4];
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) sc4[c4] = pf4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < QD; ++s)
+                sc4[s & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(kf[s], qf[s], sc4[s & 3], 0, 0, 0);
+            const pf4 sc = (sc4[0] + sc4[1]) + (sc4[2] + sc4[3]);
+            const int kb = mt * kPaK + 4 * grp;
+            float sv[4], mx = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                sv[r] = (myq >= 0 && kb + r <= myq) ? sc[r] : -INFINITY;
+                mx = fmaxf(mx, sv[r]);
+            }
+            mx = pa_colmax(mx);
+            const float mnew = fmaxf(m_run, mx);
+            float pw[4], sum = 0.f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                pw[r] = sv[r] == -INFINITY ? 0.f : expf(sv[r] - mnew);
+                sum += pw[r];
+            }
+            sum = pa_colsum(sum);
+            const float scl = m_run == -INFINITY ? 0.f : expf(m_run - mnew);
+            l_run = l_run * scl + sum;
+            m_run = mnew;
+#pragma unroll
+            for (int t = 0; t < VD; ++t) o[t] *= scl;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int t = 0; t < VD; ++t)
+                    o[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf[r][t], pw[r], o[t], 0, 0, 0);
+        }
+        // the odd-tile wave of each pair hands its state over (lane layout), the even-tile wave
+        // merges it
+        float* ow = ot + pr * (kPaQ * KL);
+        __syncthreads();
+        if (half == 1) {
+#pragma unroll
+            for (int t = 0; t < VD; ++t) *(pf4*)(ow + (t * 64 + lane) * 4) = o[t];
+            mlh[pr][0][lane] = m_run;
+            mlh[pr][1][lane] = l_run;
+        }
+        __syncthreads();
+        if (half == 0) {
+            const float m2 = mlh[pr][0][lane], l2 = mlh[pr][1][lane];
+            const float M = fmaxf(m_run, m2);
+            const float s1 = m_run == -INFINITY ? 0.f : expf(m_run - M);
+            const float s2 = m2 == -INFINITY ? 0.f : expf(m2 - M);
+#pragma unroll
+            for (int t = 0; t < VD; ++t) o[t] = o[t] * s1 + *(const pf4*)(ow + (t * 64 + lane) * 4) * s2;
+            l_run = l_run * s1 + l2 * s2;
+            m_run = M;
+            // O through LDS into row-major order (this wave's own hand-off area, already read)
+            const float inv = nspan == 1 ? ((myq >= 0 && l_run > 0.f) ? 1.f / l_run : 0.f) : 1.f;
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the hand-off reads are done
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float* dst = ow + col * KL + (4 * grp + r) * VD;
+                if constexpr (VD == 2) {
+                    *(pf2*)dst = pf2{o[0][r] * inv, o[1][r] * inv};
+                } else {
+#pragma unroll
+                    for (int t = 0; t < VD; t += 4)
+                        *(pf4*)(dst + t) = pf4{o[t][r] * inv, o[t + 1][r] * inv, o[t + 2][r] * inv, o[t + 3][r] * inv};
+                }
+            }
+            if (nspan > 1 && grp == 0) {
+                float* pp = a.part + (((size_t)(b * 8 + (col & 7)) * a.H + h) * a.nsplit + sp) * (HD + 2);
+                store_through(pp + HD, m_run);
+                store_through(pp + HD + 1, l_run);
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            __builtin_amdgcn_wave_barrier();
+            constexpr int RW = (HD + 63) / 64;
+            float rv[kPaQ][RW];
+#pragma unroll
+            for (int c = 0; c < kPaQ; ++c)
+#pragma unroll
+                for (int j = 0; j < RW; ++j) rv[c][j] = ow[c * KL + min(lane + 64 * j, HD - 1)];
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int c = 0; c < kPaQ; ++c) {
+                const size_t orow = (size_t)(b * 8 + (c & 7));
+                const int hc = kvh * G + hp * 4 + 2 * pr + (c >> 3);
+#pragma unroll
+                for (int j = 0; j < RW; ++j) {
+                    const int d = lane + 64 * j;
+                    if (d < HD) {
+                        if (nspan == 1) a.out[orow * a.H * HD + hc * HD + d] = rv[c][j];
+                        else store_through(a.part + ((orow * a.H + hc) * a.nsplit + sp) * (HD + 2) + d, rv[c][j]);
+                    }
+                }
+            }
+        }
+    }
+    if (nspan == 1) return;
+    pa_span_merge<HD>(a, grp_id, nspan, span_t, ntile_all, b, kvh, 0, qpos, &last_flag);
 }
 
 static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) {
@@ -535,16 +763,32 @@ static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) 
     // few groups: split the keys into spans for about 2048 workgroups, eight per compute unit,
     // since spans past a sequence's length exit at once (at most 16 spans, within the decode
     // kernel's partial buffer and counters)
+    // blocks of exactly 8 rows with a multiple of 4 query heads per KV head: two heads per
+    // matrix tile (k_pattn_pk), which walks its span's key tiles two at a time
+    const bool packed = a.rps == 8 && (a.H / a.Hkv) % 4 == 0;
     int nspan = 1, span_t = 1;
     if (groups < 256 && (size_t)groups <= e.ws.attn_cnt_n) {
         const int tiles = (a.cap + kPaK - 1) / kPaK;
-        nspan = std::min(std::min(kPaMaxSpans, a.nsplit), std::max(1, 2048 / groups));
+        // (the packed kernel does half the matrix work per tile and measured best at ~768
+        // workgroups: 79.8 us with 6 spans against 86.9 with 15 at the batched verify shape)
+        nspan = std::min(std::min(kPaMaxSpans, a.nsplit), std::max(1, (packed ? 768 : 2048) / groups));
         span_t = (tiles + nspan - 1) / nspan;
+        if (packed) span_t += span_t & 1;
         nspan = (tiles + span_t - 1) / span_t;
     }
     dim3 grid(groups * nspan);
     ProfEntry* pe = prof_slot(&e, kProfAttn, 0.0);
     hipEvent_t ea = pe ? pe->a : nullptr, eb = pe ? pe->b : nullptr;
+    if (packed) {
+        switch (a.hd) {
+            case 32: hipExtLaunchKernelGGL(k_pattn_pk<32>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
+            case 64: hipExtLaunchKernelGGL(k_pattn_pk<64>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
+            case 128: hipExtLaunchKernelGGL(k_pattn_pk<128>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
+            default: e.bad_launch = true; pe = nullptr; break;
+        }
+        if (pe) prof_commit(&e);
+        return;
+    }
     switch (a.hd) {
         case 32: hipExtLaunchKernelGGL(k_pattn<32>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
         case 64: hipExtLaunchKernelGGL(k_pattn<64>, grid, dim3(256), 0, s, ea, eb, 0, a, nspan, span_t); break;
