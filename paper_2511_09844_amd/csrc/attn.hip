@@ -46,6 +46,33 @@ struct AttnArgs {
     int32_t* cnt;    // one arrival counter per workgroup of the split-free grid
 };
 
+// Wave-wide max and sum with DPP steps (quad permutes, row mirrors, row broadcasts), every lane
+// active; the result is read from lane 63 and is uniform.  xor shuffles through LDS took six
+// dependent LDS round trips per reduction.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float at_dpp(float old, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old), __builtin_bit_cast(int, v),
+                                                                 CTRL, ROWS, 0xf, false));
+}
+__device__ __forceinline__ float at_wmax(float v) {
+    v = fmaxf(v, at_dpp<0xB1, 0xf>(v, v));   // quad_perm [1,0,3,2]
+    v = fmaxf(v, at_dpp<0x4E, 0xf>(v, v));   // quad_perm [2,3,0,1]
+    v = fmaxf(v, at_dpp<0x141, 0xf>(v, v));  // row_half_mirror
+    v = fmaxf(v, at_dpp<0x140, 0xf>(v, v));  // row_mirror
+    v = fmaxf(v, at_dpp<0x142, 0xa>(v, v));  // row_bcast:15 into rows 1 and 3
+    v = fmaxf(v, at_dpp<0x143, 0xc>(v, v));  // row_bcast:31 into rows 2 and 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+__device__ __forceinline__ float at_wsum(float v) {
+    v += at_dpp<0xB1, 0xf>(0.f, v);
+    v += at_dpp<0x4E, 0xf>(0.f, v);
+    v += at_dpp<0x141, 0xf>(0.f, v);
+    v += at_dpp<0x140, 0xf>(0.f, v);
+    v += at_dpp<0x142, 0xa>(0.f, v);
+    v += at_dpp<0x143, 0xc>(0.f, v);
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
 // Request chunk c of K and V (positions past maxpos re-read the last valid row; they are masked).
 template <int HD, int F4>
 __device__ __forceinline__ void fetch_chunk(f4_t (&pk)[F4], f4_t (&pv)[F4], const float* kg, const float* vg,
@@ -160,10 +187,10 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
                 s = d0;
             }
             // row max and sum over the 64 keys held by this wave's 64 lanes
-            float mx = wave_max(s);
+            float mx = at_wmax(s);
             float mnew = fmaxf(mrun[qi], mx);
             float p = (s == -INFINITY) ? 0.f : expf(s - mnew);
-            float sum = wave_sum(p);
+            float sum = at_wsum(p);
             ps[qi * kAttnCL + j] = p;
             if (j == 0) {
                 float sc = mrun[qi] == -INFINITY ? 0.f : expf(mrun[qi] - mnew);
