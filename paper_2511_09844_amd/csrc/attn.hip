@@ -136,6 +136,19 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
         if (p >= 0) atomicMax(&maxpos_s, p);
     }
     __syncthreads();
+    // Spans past the group's last row position take no part (every workgroup of the group
+    // derives the same live-span count from the row positions, and only live spans count in);
+    // a group without any active row has its zero outputs written by span 0.
+    const int nlive = maxpos_s >= 0 ? min(a.nsplit, maxpos_s / kSplit + 1) : 0;
+    if (nlive == 0) {
+        if (sp == 0)
+            for (int idx = tid; idx < nq * HD; idx += kAttnT) {
+                const int qi = idx / HD, d = idx % HD;
+                a.out[(size_t)qrow[qi] * a.H * HD + qhead[qi] * HD + d] = 0.f;
+            }
+        return;
+    }
+    if (sp >= nlive) return;
     const int p_lo = sp * kSplit;
     const int maxpos = min(maxpos_s, p_lo + kSplit - 1);  // last position this span scores
     for (int idx = tid; idx < nq * HD; idx += kAttnT) {
@@ -225,9 +238,8 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
             }
         }
     }
-    // the last span of these query vectors to finish merges all spans in span order
-    if (!arrive_last(a.cnt + wg, a.nsplit, &last_flag)) return;
-    const int nlive = maxpos_s >= 0 ? min(a.nsplit, maxpos_s / kSplit + 1) : 0;
+    // the last live span of these query vectors to finish merges them in span order
+    if (!arrive_last(a.cnt + wg, nlive, &last_flag)) return;
     for (int idx = tid; idx < nq * HD; idx += kAttnT) {
         int qi = idx / HD, d = idx % HD;
         int pos = qpos[qi];
