@@ -87,13 +87,13 @@ __device__ __forceinline__ void fetch_chunk(f4_t (&pk)[F4], f4_t (&pv)[F4], cons
     }
 }
 
-template <int HD>
+template <int HD, int QT>
 __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
     extern __shared__ __attribute__((aligned(16))) float sm[];
-    __shared__ int qpos[kAttnQT];
-    __shared__ int qrow[kAttnQT];
-    __shared__ int qhead[kAttnQT];
-    __shared__ float mrun[kAttnQT], lrun[kAttnQT], rescale[kAttnQT];
+    __shared__ int qpos[QT];
+    __shared__ int qrow[QT];
+    __shared__ int qhead[QT];
+    __shared__ float mrun[QT], lrun[QT], rescale[QT];
     __shared__ int maxpos_s;
     __shared__ int last_flag;
     const int tid = threadIdx.x;
@@ -109,19 +109,19 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
     const int kvh = (gi / a.nrt) % a.Hkv;
     const int b = gi / (a.nrt * a.Hkv);
     const int hbase = kvh * G + mi * a.hp;
-    const int rows_per_tile = kAttnQT / a.hp;
+    const int rows_per_tile = QT / a.hp;
     const int r0 = rt * rows_per_tile;
     const int nrows = min(rows_per_tile, a.rps - r0);
     const int nq = nrows * a.hp;
 
     float* qs = sm;                          // [QT][HD]   (pre-scaled queries)
-    float* ks = qs + kAttnQT * HD;           // [CL][HD+1]
+    float* ks = qs + QT * HD;           // [CL][HD+1]
     float* vs = ks + kAttnCL * (HD + 1);     // [CL][HD]
     float* ps = vs + kAttnCL * HD;           // [QT][CL]
 
     if (tid == 0) maxpos_s = -1;
     __syncthreads();
-    if (tid < kAttnQT) {
+    if (tid < QT) {
         int p = -1, row = 0, h = 0;
         if (tid < nq) {
             row = b * a.rps + r0 + tid / a.hp;
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kAttnT) void k_attn(AttnArgs a) {
 
     // output accumulators: thread owns dims d = tid % HD of query vectors qi = tid / HD + j * (T / HD)
     constexpr int QSTEP = kAttnT / HD;
-    constexpr int NACC = kAttnQT / QSTEP;
+    constexpr int NACC = QT / QSTEP;
     float acc[NACC];
 #pragma unroll
     for (int j = 0; j < NACC; ++j) acc[j] = 0.f;
@@ -837,9 +837,8 @@ static void launch_pattn(Engine& e, hipStream_t s, const AttnArgs& a, int nseq) 
     if (pe) prof_commit(&e);
 }
 
-static size_t attn_lds(int hd) {
-    return sizeof(float) * ((size_t)kAttnQT * hd + (size_t)kAttnCL * (hd + 1) + (size_t)kAttnCL * hd +
-                            (size_t)kAttnQT * kAttnCL);
+static size_t attn_lds(int hd, int qt) {
+    return sizeof(float) * ((size_t)qt * hd + (size_t)kAttnCL * (hd + 1) + (size_t)kAttnCL * hd + (size_t)qt * kAttnCL);
 }
 
 // Query heads per workgroup: all heads of a KV group, so that each K/V row is read once for all
@@ -880,10 +879,17 @@ void launch_attn(Engine& e, hipStream_t s, ModelDev& m, int layer, int rows, int
     int nblk = (a.ngrp + kXcds - 1) / kXcds * kXcds * members * a.nsplit;
     ProfEntry* pe = prof_slot(&e, kProfAttn, 0.0);
     hipEvent_t ea = pe ? pe->a : nullptr, eb = pe ? pe->b : nullptr;
-    switch (m.hd) {
-        case 32: hipExtLaunchKernelGGL(k_attn<32>, dim3(nblk), dim3(kAttnT), attn_lds(32), s, ea, eb, 0, a); break;
-        case 64: hipExtLaunchKernelGGL(k_attn<64>, dim3(nblk), dim3(kAttnT), attn_lds(64), s, ea, eb, 0, a); break;
-        case 128: hipExtLaunchKernelGGL(k_attn<128>, dim3(nblk), dim3(kAttnT), attn_lds(128), s, ea, eb, 0, a); break;
+    // eight query-vector slots where a group's rows and heads fit them (decode steps: one or two
+    // rows of a KV group), which quarters the query and score buffers in LDS; the row tiling,
+    // and so the group count, is the same as with 32 slots (one tile)
+    const bool q8 = a.hp * rps <= 8;
+    switch (m.hd * (q8 ? -1 : 1)) {
+        case 32: hipExtLaunchKernelGGL((k_attn<32, kAttnQT>), dim3(nblk), dim3(kAttnT), attn_lds(32, kAttnQT), s, ea, eb, 0, a); break;
+        case 64: hipExtLaunchKernelGGL((k_attn<64, kAttnQT>), dim3(nblk), dim3(kAttnT), attn_lds(64, kAttnQT), s, ea, eb, 0, a); break;
+        case 128: hipExtLaunchKernelGGL((k_attn<128, kAttnQT>), dim3(nblk), dim3(kAttnT), attn_lds(128, kAttnQT), s, ea, eb, 0, a); break;
+        case -32: hipExtLaunchKernelGGL((k_attn<32, 8>), dim3(nblk), dim3(kAttnT), attn_lds(32, 8), s, ea, eb, 0, a); break;
+        case -64: hipExtLaunchKernelGGL((k_attn<64, 8>), dim3(nblk), dim3(kAttnT), attn_lds(64, 8), s, ea, eb, 0, a); break;
+        case -128: hipExtLaunchKernelGGL((k_attn<128, 8>), dim3(nblk), dim3(kAttnT), attn_lds(128, 8), s, ea, eb, 0, a); break;
         default: e.bad_launch = true; pe = nullptr; break;
     }
     if (pe) prof_commit(&e);
