@@ -756,8 +756,12 @@ static bool launch_pgemm(Engine* e, hipStream_t s, const WsCall& c) {
 }
 
 void launch_wsgemv(Engine* e, hipStream_t s, const WsCall& c) {
-    // more than one 16-row group: the GEMM (weights read once per 64 rows, not per 16)
-    if (c.M > 16 && launch_pgemm(e, s, c)) return;
+    // more than one 16-row group: the GEMM (weights read once per 64 rows, not per 16); also a
+    // full 16-row group against a vocabulary-sized weight (the batched drafter steps' LM head),
+    // which the GEMM streams faster
+    int nrows = 0;
+    for (int i = 0; i < c.nseg; ++i) nrows += c.seg_rows[i];
+    if ((c.M > 16 || (c.M == 16 && nrows >= 32768)) && launch_pgemm(e, s, c)) return;
     for (int r0 = 0; r0 < c.M; r0 += 16) {
         int M = c.M - r0 < 16 ? c.M - r0 : 16;
         WsArgs a{};
