@@ -238,6 +238,9 @@ __global__ __launch_bounds__(NW * 64) void k_wsgemv(WsArgs a) {
             const int idx = min(tid + i * NW * 64, nx - 1);
             gv[i] = *(const uint2*)(a.gamma + k0 + (idx % n4) * 4);
         }
+    } else {
+#pragma unroll
+        for (int i = 0; i < XB; ++i) gv[i] = make_uint2(0x3f803f80u, 0x3f803f80u);  // bf16 ones
     }
     if (nsub_mine > 0) issue(wa, 0);
     float ssum = 0.0f;
